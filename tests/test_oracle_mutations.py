@@ -1,0 +1,129 @@
+"""The oracle's pins catch plausible mistakes.
+
+Each case plants one mistake in a copy of an oracle function (on the CPU, via
+monkeypatch) and checks that at least one pin of ``test_oracle_elbo`` fails:
+a dropped 1/t, a missing max shift, a swapped bound branch, a wrong
+derivative of the bound, a sign flip in the backward, a transposed or
+mis-indexed operand.
+"""
+import numpy as np
+import pytest
+
+from oracle import elbo
+import test_oracle_elbo as pins
+
+ALL_PINS = [
+    pins.check_log_softmax,
+    pins.check_t1_cross_entropy,
+    pins.check_brute_force_expectation,
+    pins.check_finite_differences,
+    lambda: pins.check_autograd(on_policy=False),
+    lambda: pins.check_autograd(on_policy=True),
+    pins.check_on_policy_equivalence,
+    pins.check_bound_equality_cases,
+    pins.check_linearity,
+]
+
+
+def _any_pin_fails():
+    for pin in ALL_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin()
+        except (AssertionError, ValueError, IndexError, FloatingPointError):
+            return True
+    return False
+
+
+def _orig(name):
+    return getattr(elbo, name)
+
+
+def mut_no_inv_t(H_b, W, y_b, mask_b, t, _f=_orig("ell_of_mask")):
+    ell, rows, lsm = _f(H_b, W, y_b, mask_b, t)
+    return ell * t, rows, lsm
+
+
+def mut_no_max_shift(z):
+    return z - np.log(np.exp(z).sum(axis=1, keepdims=True))
+
+
+def mut_no_normaliser(z):
+    return z - z.max(axis=1, keepdims=True)
+
+
+def mut_swap_branches(d, A, n_t):
+    if A < 0:
+        return (1.0 + d) * A / n_t, A / n_t
+    e = np.exp(d)
+    return e * A / n_t, e * A / n_t
+
+
+def mut_taylor_everywhere(d, A, n_t):
+    return (1.0 + d) * A / n_t, A / n_t
+
+
+def mut_bound_derivative_missing_nt(d, A, n_t, _f=_orig("bound_term")):
+    g, dg = _f(d, A, n_t)
+    return g, dg * n_t
+
+
+def mut_jensen_derivative_missing_exp(d, A, n_t, _f=_orig("bound_term")):
+    g, dg = _f(d, A, n_t)
+    return g, (A / n_t if A < 0 else dg)
+
+
+def mut_backprop_sign(H_rows, W, y_rows, lsm, s, _f=_orig("backprop_rows")):
+    gx, gw = _f(H_rows, W, y_rows, lsm, s)
+    return -gx, -gw
+
+
+def mut_backprop_no_onehot(H_rows, W, y_rows, lsm, s):
+    dZ = s * np.exp(lsm)
+    return dZ @ W.T, H_rows.T @ dZ
+
+
+def mut_backprop_wrong_target(H_rows, W, y_rows, lsm, s):
+    y = (np.asarray(y_rows).astype(np.int64) + 1) % W.shape[1]
+    dZ = s * np.exp(lsm)
+    dZ[np.arange(y.size), y] -= s
+    return dZ @ W.T, H_rows.T @ dZ
+
+
+def mut_backprop_rows_reversed(H_rows, W, y_rows, lsm, s, _f=_orig("backprop_rows")):
+    gx, gw = _f(H_rows[::-1], W, y_rows, lsm, s)
+    return gx, gw
+
+
+def mut_dx_without_transpose(H_rows, W, y_rows, lsm, s):
+    y = np.asarray(y_rows).astype(np.int64)
+    dZ = s * np.exp(lsm)
+    dZ[np.arange(y.size), y] -= s
+    gx = (dZ[:, :W.shape[0]] if dZ.shape[1] >= W.shape[0] else dZ) @ W[:, :W.shape[0]]
+    return gx, H_rows.T @ dZ
+
+
+MUTATIONS = [
+    ("ell_of_mask", mut_no_inv_t),
+    ("log_softmax_rows", mut_no_max_shift),
+    ("log_softmax_rows", mut_no_normaliser),
+    ("bound_term", mut_swap_branches),
+    ("bound_term", mut_taylor_everywhere),
+    ("bound_term", mut_bound_derivative_missing_nt),
+    ("bound_term", mut_jensen_derivative_missing_exp),
+    ("backprop_rows", mut_backprop_sign),
+    ("backprop_rows", mut_backprop_no_onehot),
+    ("backprop_rows", mut_backprop_wrong_target),
+    ("backprop_rows", mut_backprop_rows_reversed),
+    ("backprop_rows", mut_dx_without_transpose),
+]
+
+
+def test_pins_pass_unmutated():
+    assert not _any_pin_fails()
+
+
+@pytest.mark.parametrize("name,fn", MUTATIONS, ids=[f.__name__ for _, f in MUTATIONS])
+def test_mutation_is_caught(monkeypatch, name, fn):
+    monkeypatch.setattr(elbo, name, fn)
+    assert _any_pin_fails(), f"planted mistake {fn.__name__} in {name} passed every pin"

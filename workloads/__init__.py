@@ -1,0 +1,159 @@
+"""Seeded synthetic inputs for the BGPO masked-diffusion ELBO head.
+
+This module draws the *inputs* only: hidden states, LM-head weights, target
+tokens, response-length masks and per-response advantages.  It holds none of
+the method's arithmetic (no timestep draw, no masking, no log-softmax, no
+bound); those live separately in the float64 oracle and in the HIP path,
+which both consume the arrays produced here.
+
+The paper trains LLaDA-8B-Instruct with response length 512 (math, code) or
+256 (planning), G = 8 responses per prompt and n_t = 16 or 32 Monte-Carlo
+samples (Section 4.1 and Table 5).  Its datasets and trained weights are not
+used; the workloads below stand in for them with the LLaDA head shape
+d = 4096, V = 126464, uniform response lengths, Zipf(1.1) target tokens and
+N(0, 0.02^2) head weights.
+
+Rounding to bfloat16 is round-to-nearest-even on the float32 bit pattern, so
+both consumers see exactly the same bf16 values.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional, Tuple
+
+import numpy as np
+
+T_IID = 0
+T_STRATIFIED = 1
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """Shape and value distributions of one synthetic ELBO-head problem."""
+
+    name: str
+    B: int                      # responses in the batch (G per prompt)
+    L: int                      # padded response length
+    d: int                      # hidden size
+    V: int                      # vocabulary size
+    n_t: int                    # Monte-Carlo samples per response
+    t_mode: int = T_IID         # T_IID: t ~ U(0,1); T_STRATIFIED: t_k = (k+u)/n_t
+    hidden: str = "rmsnorm"     # "normal": N(0,1); "rmsnorm": N(0,1) then per-row RMS normalisation
+    targets: str = "zipf"       # "uniform" over V or "zipf" (exponent 1.1)
+    lengths: Optional[Tuple[int, int]] = None   # inclusive uniform response length; None = all L
+    adv: str = "group"          # "normal": N(0,1) per response; "group": group-normalised over G
+    group: int = 8              # G for group-normalised advantages
+    w_std: float = 0.02         # head weight standard deviation
+    data_seed: int = 1000       # numpy PCG64 seed
+    philox_seed: int = 0xB6B00000
+    seq_id_base: int = 0
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+# The five problem sizes used throughout: a tiny correctness case, the
+# LLaDA-8B head shape at response length 256 and 512 (uniform and ragged
+# lengths), the large-MC regime n_t = 64, and a long-response stress case
+# with stratified timesteps.
+TINY = Workload("tiny_B2_L64_d128_V1024_nt4", B=2, L=64, d=128, V=1024, n_t=4,
+                hidden="normal", targets="uniform", adv="normal",
+                data_seed=1001, philox_seed=0xB6B00001)
+LLADA_L256 = Workload("llada_head_B8_L256_nt16", B=8, L=256, d=4096, V=126464, n_t=16,
+                      data_seed=1002, philox_seed=0xB6B00002)
+LLADA_L512_RAGGED = Workload("llada_head_B8_L512_ragged_nt16", B=8, L=512, d=4096, V=126464,
+                             n_t=16, lengths=(128, 512), data_seed=1003,
+                             philox_seed=0xB6B00003)
+LLADA_L512_NT64 = Workload("llada_head_B8_L512_nt64", B=8, L=512, d=4096, V=126464, n_t=64,
+                           data_seed=1004, philox_seed=0xB6B00004)
+STRESS_L1024 = Workload("llada_head_B16_L1024_ragged_nt32_stratified", B=16, L=1024, d=4096,
+                        V=126464, n_t=32, t_mode=T_STRATIFIED, lengths=(256, 1024),
+                        adv="normal", data_seed=1005, philox_seed=0xB6B00005)
+
+CONFIGS = (TINY, LLADA_L256, LLADA_L512_RAGGED, LLADA_L512_NT64, STRESS_L1024)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bfloat16 (nearest, ties to even); returns uint16 bit patterns."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    return (rounded >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Widen bfloat16 bit patterns to float32 (exact)."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _zipf_tokens(rng: np.random.Generator, V: int, n: int, exponent: float = 1.1) -> np.ndarray:
+    """Zipf(exponent) over V ranks by inverse CDF, then a seeded permutation of token ids."""
+    ranks = np.arange(1, V + 1, dtype=np.float64)
+    cdf = np.cumsum(ranks ** (-exponent))
+    cdf /= cdf[-1]
+    u = rng.random(n)
+    r = np.minimum(np.searchsorted(cdf, u, side="right"), V - 1)
+    perm = rng.permutation(V)
+    return perm[r].astype(np.int32)
+
+
+def generate(w: Workload, *, with_weights: bool = True) -> dict:
+    """Draw every input of workload ``w`` from numpy PCG64(w.data_seed).
+
+    Returns a dict of numpy arrays:
+      hidden    uint16 [B, L, d]  bf16 bits, row-major
+      W         uint16 [d, V]     bf16 bits, row-major (V contiguous)
+      targets   int32  [B, L]     target token per position (defined on padding too)
+      resp_mask uint8  [B, L]     1 on response positions, 0 on padding
+      adv       float32 [B]       per-response advantage
+    plus ``lengths`` (int32 [B]).
+    """
+    rng = np.random.Generator(np.random.PCG64(w.data_seed))
+    B, L, d, V = w.B, w.L, w.d, w.V
+
+    h = rng.standard_normal((B, L, d), dtype=np.float32)
+    if w.hidden == "rmsnorm":
+        rms = np.sqrt(np.mean(h.astype(np.float64) ** 2, axis=-1, keepdims=True) + 1e-6)
+        h = (h / rms).astype(np.float32)
+    hidden = f32_to_bf16_bits(h).reshape(B, L, d)
+    del h
+
+    W = None
+    if with_weights:
+        W = np.empty((d, V), dtype=np.uint16)
+        rows_per_chunk = max(1, (1 << 24) // V)
+        for r0 in range(0, d, rows_per_chunk):
+            r1 = min(d, r0 + rows_per_chunk)
+            chunk = rng.standard_normal((r1 - r0, V), dtype=np.float32) * np.float32(w.w_std)
+            W[r0:r1] = f32_to_bf16_bits(chunk).reshape(r1 - r0, V)
+    else:
+        # keep the stream position identical to the with-weights draw
+        rows_per_chunk = max(1, (1 << 24) // V)
+        for r0 in range(0, d, rows_per_chunk):
+            r1 = min(d, r0 + rows_per_chunk)
+            rng.standard_normal((r1 - r0, V), dtype=np.float32)
+
+    if w.targets == "uniform":
+        targets = rng.integers(0, V, size=(B, L), dtype=np.int64).astype(np.int32)
+    else:
+        targets = _zipf_tokens(rng, V, B * L).reshape(B, L)
+
+    if w.lengths is None:
+        lengths = np.full(B, L, dtype=np.int32)
+    else:
+        lo, hi = w.lengths
+        lengths = rng.integers(lo, hi + 1, size=B, dtype=np.int64).astype(np.int32)
+    resp_mask = (np.arange(L)[None, :] < lengths[:, None]).astype(np.uint8)
+
+    r = rng.standard_normal(B)
+    if w.adv == "group":
+        G = w.group
+        adv = np.empty(B, dtype=np.float64)
+        for g0 in range(0, B, G):
+            rg = r[g0:g0 + G]
+            adv[g0:g0 + G] = (rg - rg.mean()) / (rg.std() + 1e-6)   # population std
+        adv = adv.astype(np.float32)
+    else:
+        adv = r.astype(np.float32)
+
+    return dict(hidden=hidden, W=W, targets=targets, resp_mask=resp_mask, adv=adv,
+                lengths=lengths)
