@@ -1,0 +1,185 @@
+/*
+ * bgpo.h - C ABI of the BGPO masked-diffusion ELBO head for AMD MI355X (gfx950).
+ *
+ * The library computes, for every response b of a batch and every
+ * Monte-Carlo sample j of a sample range, the per-sample ELBO term of a
+ * masked diffusion language model and the gradient of Boundary-Guided Policy
+ * Optimization's linear lower bound through the LM head:
+ *
+ *   t_{b,j}      timestep drawn from U(0,1) (Eq. mcs_elbo; one per response and
+ *                sample, Algorithm 1), or from the stratified grid (j+u)/n_t
+ *   mask         each response token masked independently with probability t
+ *                (Section 2.1, forward process; the prompt is never masked)
+ *   l_{b,j}      (1/t) * sum over masked positions of log softmax(h W)[target]
+ *                (Eq. per_step_loss)
+ *   d_{b,j}      l_{b,j} - l_old_{b,j} on the same masked sample (Section 3.1)
+ *   g_{b,j}      (1+d) A_b / n_t if A_b >= 0, e^d A_b / n_t if A_b < 0 (Eq. g)
+ *   loss        += -loss_scale * g_{b,j}   (Algorithm 1: L_j = -g_j / G)
+ *   dX, dW      += gradient of that loss term w.r.t. hidden states and head
+ *                weights, accumulated sample by sample (Algorithm 1, gradient
+ *                accumulation; the lower bound is a sum, Eq. lower_bound_def)
+ *
+ * Random numbers come from Philox4x32-10 (Salmon et al., SC'11) keyed by
+ * (seed mod 2^32, seed div 2^32):
+ *   t:           counter (0, seq, j, 1), word 0; T24 = max(word >> 8, 1);
+ *                t = T24 * 2^-24
+ *   stratified:  counter (0, seq, 0, 2), word 0; U24 = word >> 8;
+ *                T24 = max(floor((j * 2^24 + U24) / n_t), 1)
+ *   mask:        position i is masked iff resp_mask[b][i] != 0 and
+ *                (word (i mod 4) of counter (i div 4, seq, j, 0)) >> 8 < T24
+ * where seq = seq_id_base + b.  Masks therefore depend only on
+ * (seed, seq, j, resp_mask), never on the batch split, so a later call with
+ * other weights reproduces the same masked samples (needed for d_{b,j}).
+ *
+ * Conventions for every entry point:
+ *   - All array arguments are DEVICE pointers (memory of the current HIP
+ *     device), owned by the caller; the problem struct is a HOST pointer.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream) and
+ *     is complete when the stream is synchronised.  No entry point
+ *     synchronises the stream, except that a non-NULL `prof` makes the call
+ *     wait for its own timing events before returning.
+ *   - The library never allocates device memory; scratch space is the
+ *     caller's `workspace` of at least bgpo_workspace_size() bytes (256-byte
+ *     aligned).  Its size depends on B, L, d and V, never on n_t.
+ *   - Host-detectable errors return a negative bgpo_status before anything is
+ *     enqueued; HIP launch errors return BGPO_ERR_HIP.  No C++ exception
+ *     crosses the ABI.  Entry points keep no mutable global state; calls on
+ *     different streams must not share a workspace.
+ *   - hidden and W_head are bfloat16 bit patterns (uint16), row-major.
+ *   - Supported shapes: B >= 1, L >= 1, B*L <= 2^24, d % 64 == 0,
+ *     V % 64 == 0, 64 <= d <= 65536, 64 <= V <= 2^20, n_t >= 1,
+ *     0 <= j_begin, j_count >= 0, j_begin + j_count <= n_t.  Targets must lie
+ *     in [0, V) on every response position.  Other shapes return
+ *     BGPO_ERR_UNSUPPORTED.
+ */
+#ifndef BGPO_H_
+#define BGPO_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum bgpo_status {
+  BGPO_OK = 0,
+  BGPO_ERR_INVALID_ARG = -1,   /* NULL pointer, negative size, bad enum, range outside [0, n_t) */
+  BGPO_ERR_WORKSPACE = -2,     /* workspace NULL, misaligned or smaller than bgpo_workspace_size() */
+  BGPO_ERR_HIP = -3,           /* a HIP call failed (launch, event) */
+  BGPO_ERR_UNSUPPORTED = -4    /* shape outside the supported set above */
+} bgpo_status;
+
+/* Timestep modes. */
+enum { BGPO_T_IID = 0, BGPO_T_STRATIFIED = 1 };
+
+/* Bits of *status_flags (device int32, OR-ed in, never cleared by the library). */
+enum { BGPO_FLAG_NONFINITE = 1 };
+
+typedef struct bgpo_problem {
+  int32_t B;            /* responses in the batch */
+  int32_t L;            /* padded response length (positions per response) */
+  int32_t d;            /* hidden size */
+  int32_t V;            /* vocabulary size */
+  int32_t n_t;          /* Monte-Carlo samples per response: the 1/n_t of Eq. g */
+  int32_t j_begin;      /* first sample index handled by this call */
+  int32_t j_count;      /* number of samples handled; any split of [0, n_t) is valid */
+  int32_t t_mode;       /* BGPO_T_IID or BGPO_T_STRATIFIED */
+  uint64_t seed;        /* Philox key */
+  uint32_t seq_id_base; /* global id of response b = 0 (seq = seq_id_base + b) */
+  uint32_t reserved;    /* must be 0 */
+} bgpo_problem;
+
+/* Kernel classes reported by the optional timing record. */
+enum {
+  BGPO_K_TRANSPOSE_W = 0,  /* W[d,V] -> W^T[V,d] staging, once per call */
+  BGPO_K_MASK = 1,         /* Philox t and masks + stable compaction */
+  BGPO_K_GATHER = 2,       /* masked hidden rows -> H_c and H_c^T */
+  BGPO_K_FWD = 3,          /* fused LM-head GEMM + online log-sum-exp partials */
+  BGPO_K_ELL = 4,          /* partial combine, log p, l, d, g, loss, gradient scale */
+  BGPO_K_RECOMPUTE = 5,    /* logits recompute + softmax-minus-onehot -> dZ */
+  BGPO_K_DX = 6,           /* dZ W^T split over the vocabulary */
+  BGPO_K_DX_REDUCE = 7,    /* split reduction + scatter-add into dX */
+  BGPO_K_DW = 8,           /* H_c^T dZ accumulated into dW */
+  BGPO_K_COUNT = 9
+};
+
+/* Optional per-kernel timing (host memory).  When passed to an entry point,
+ * elapsed milliseconds (HIP events on `stream`) and launch counts of every
+ * kernel class are ADDED to the record, after the call waits for its events. */
+typedef struct bgpo_timing {
+  double ms[BGPO_K_COUNT];
+  int64_t launches[BGPO_K_COUNT];
+} bgpo_timing;
+
+/* Library version, (major << 16) | minor. */
+int bgpo_version(void);
+
+/* Human-readable name of a bgpo_status value (static string, never NULL). */
+const char* bgpo_status_string(int status);
+
+/* Bytes of device workspace needed by bgpo_elbo_fwd and
+ * bgpo_elbo_bwd_accumulate for `prob` (depends on B, L, d, V only).
+ * Writes *bytes and returns BGPO_OK, or a negative status. Host only. */
+int bgpo_workspace_size(const bgpo_problem* prob, size_t* bytes);
+
+/* Timestep and mask of every response for ONE sample j (the forward masking
+ * process of Section 2.1 and the t draw of Algorithm 1), compacted.
+ *   resp_mask  uint8 [B, L]   1 on response positions (prompt/padding 0)
+ *   idx        int32 [B*L]    out: masked flat positions b*L + i in ascending
+ *                             order in idx[0 .. N), N = sum of n_masked; the
+ *                             rest of the array is left untouched
+ *   n_masked   int32 [B]      out: masked positions per response
+ *   t_out      float [B]      out: t_{b,j} (exact multiple of 2^-24); may be NULL
+ * j must lie in [0, n_t); prob->j_begin/j_count are ignored. */
+int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_t j,
+                      int32_t* idx, int32_t* n_masked, float* t_out, void* stream);
+
+/* Forward only: l_{b,j} (Eq. per_step_loss) for j in [j_begin, j_begin + j_count).
+ *   hidden    bf16  [B, L, d]  final hidden states of the response positions
+ *   W_head    bf16  [d, V]     LM-head weights (V contiguous)
+ *   targets   int32 [B, L]     clean target token y^i of every position
+ *   resp_mask uint8 [B, L]
+ *   ell       double [B, n_t]  out: entries (b, j) of the range are written
+ *   n_masked  int32  [B, n_t]  out: masked-token counts (same entries)
+ *   t_out     float  [B, n_t]  out: timesteps (same entries); may be NULL
+ *   prof      host timing record or NULL
+ * Deterministic: identical inputs give bit-identical outputs, so `ell` from
+ * this call fed back as `ell_old` with the same weights gives d == 0 exactly. */
+int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16_t* W_head,
+                  const int32_t* targets, const uint8_t* resp_mask,
+                  double* ell, int32_t* n_masked, float* t_out,
+                  void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof);
+
+/* Forward + lower-bound term + backward for j in [j_begin, j_begin + j_count),
+ * each sample's gradient accumulated before the next sample starts (device
+ * memory stays constant in n_t).
+ *   adv          float  [B]        advantage A_b of each response (Eq. adv)
+ *   ell_old      double [B, n_t]   l under the old policy on the same samples;
+ *                                  NULL = on-policy (d == 0 exactly)
+ *   loss_scale   the 1/G of Algorithm 1 (any finite value)
+ *   dX           float  [B, L, d]  += d loss / d hidden (zero rows stay zero
+ *                                  for never-masked positions)
+ *   dW           float  [d, V]     += d loss / d W_head
+ *   ell, g       double [B, n_t]   out: l_{b,j} and g_{b,j} for the range
+ *   loss         double [1]        += sum over the range of -loss_scale * g
+ *   n_masked     int32  [B, n_t]   out
+ *   t_out        float  [B, n_t]   out; may be NULL
+ *   status_flags int32  [1]        |= BGPO_FLAG_NONFINITE if a non-finite
+ *                                  l, g or gradient scale occurs (values are
+ *                                  never clamped); may be NULL
+ * The gradients are those of the loss (to be minimised). */
+int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
+                             const uint16_t* W_head, const int32_t* targets,
+                             const uint8_t* resp_mask, const float* adv,
+                             const double* ell_old, double loss_scale,
+                             float* dX, float* dW, double* ell, double* g, double* loss,
+                             int32_t* n_masked, float* t_out, int32_t* status_flags,
+                             void* workspace, size_t ws_bytes, void* stream,
+                             bgpo_timing* prof);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BGPO_H_ */

@@ -1,0 +1,209 @@
+"""ctypes binding of libbgpo (include/bgpo.h).
+
+Argument marshalling only: tensors are checked for device, dtype, shape and
+contiguity and passed as raw device pointers together with torch's current
+HIP stream.  Every step of the computation runs in the library's HIP kernels;
+there is no fallback, and importing this module raises if the library has not
+been built (``python -m paper_2510_11683_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbgpo.so")
+
+BGPO_OK = 0
+BGPO_ERR_INVALID_ARG = -1
+BGPO_ERR_WORKSPACE = -2
+BGPO_ERR_HIP = -3
+BGPO_ERR_UNSUPPORTED = -4
+BGPO_T_IID = 0
+BGPO_T_STRATIFIED = 1
+BGPO_FLAG_NONFINITE = 1
+KERNEL_CLASSES = ("transpose_w", "mask", "gather", "fwd", "ell", "recompute", "dx", "dx_reduce", "dw")
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("L", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("V", ctypes.c_int32), ("n_t", ctypes.c_int32), ("j_begin", ctypes.c_int32),
+                ("j_count", ctypes.c_int32), ("t_mode", ctypes.c_int32),
+                ("seed", ctypes.c_uint64), ("seq_id_base", ctypes.c_uint32),
+                ("reserved", ctypes.c_uint32)]
+
+
+class Timing(ctypes.Structure):
+    """Per-kernel-class elapsed milliseconds and launch counts (bgpo_timing)."""
+    _fields_ = [("ms", ctypes.c_double * len(KERNEL_CLASSES)),
+                ("launches", ctypes.c_int64 * len(KERNEL_CLASSES))]
+
+    def as_dict(self):
+        return {k: (self.ms[i], int(self.launches[i])) for i, k in enumerate(KERNEL_CLASSES)}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2510_11683_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.bgpo_version.restype = ctypes.c_int
+    lib.bgpo_status_string.restype = ctypes.c_char_p
+    lib.bgpo_status_string.argtypes = [ctypes.c_int]
+    lib.bgpo_workspace_size.argtypes = [P(_Problem), P(sz)]
+    lib.bgpo_sample_masks.argtypes = [P(_Problem), vp, i32, vp, vp, vp, vp]
+    lib.bgpo_elbo_fwd.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, P(Timing)]
+    lib.bgpo_elbo_bwd_accumulate.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, ctypes.c_double,
+                                             vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, P(Timing)]
+    lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
+    for f in ("bgpo_workspace_size", "bgpo_sample_masks", "bgpo_elbo_fwd",
+              "bgpo_elbo_bwd_accumulate", "bgpo_test_gemm_nt"):
+        getattr(lib, f).restype = ctypes.c_int
+    return lib
+
+
+_lib = _load()
+
+
+class BgpoError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {_lib.bgpo_status_string(status).decode()} ({status})")
+        self.status = status
+
+
+def _check(status: int, where: str):
+    if status != BGPO_OK:
+        raise BgpoError(status, where)
+
+
+@dataclasses.dataclass
+class Problem:
+    """Mirror of bgpo_problem; j_count None means the rest of [j_begin, n_t)."""
+    B: int
+    L: int
+    d: int
+    V: int
+    n_t: int
+    j_begin: int = 0
+    j_count: Optional[int] = None
+    seed: int = 0
+    seq_id_base: int = 0
+    t_mode: int = BGPO_T_IID
+
+    def c(self) -> _Problem:
+        jc = self.n_t - self.j_begin if self.j_count is None else self.j_count
+        return _Problem(self.B, self.L, self.d, self.V, self.n_t, self.j_begin, jc, self.t_mode,
+                        self.seed & 0xFFFFFFFFFFFFFFFF, self.seq_id_base & 0xFFFFFFFF, 0)
+
+
+def _ptr(t: Optional[torch.Tensor], name: str, dtypes=None, shape=None, allow_none=False):
+    if t is None:
+        if allow_none:
+            return None
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+_BF16 = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def bgpo_version() -> int:
+    return _lib.bgpo_version()
+
+
+def bgpo_workspace_size(prob: Problem) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.bgpo_workspace_size(ctypes.byref(prob.c()), ctypes.byref(n)), "bgpo_workspace_size")
+    return int(n.value)
+
+
+def alloc_workspace(prob: Problem, device="cuda") -> torch.Tensor:
+    """A caller-owned workspace of bgpo_workspace_size() bytes (256-byte aligned)."""
+    return torch.empty(bgpo_workspace_size(prob), dtype=torch.uint8, device=device)
+
+
+def bgpo_sample_masks(prob: Problem, resp_mask, j: int, idx, n_masked, t_out=None, stream=None):
+    B, L = prob.B, prob.L
+    _check(_lib.bgpo_sample_masks(ctypes.byref(prob.c()),
+                                  _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)), int(j),
+                                  _ptr(idx, "idx", (torch.int32,), (B * L,)),
+                                  _ptr(n_masked, "n_masked", (torch.int32,), (B,)),
+                                  _ptr(t_out, "t_out", (torch.float32,), (B,), allow_none=True),
+                                  _stream(stream)), "bgpo_sample_masks")
+
+
+def bgpo_elbo_fwd(prob: Problem, hidden, W_head, targets, resp_mask, ell, n_masked, t_out,
+                  workspace, stream=None, timing: Optional[Timing] = None):
+    B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
+    _check(_lib.bgpo_elbo_fwd(
+        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, (B, L, d)),
+        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
+        _ptr(ell, "ell", (torch.float64,), (B, nt)),
+        _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
+        _ptr(t_out, "t_out", (torch.float32,), (B, nt), allow_none=True),
+        _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(), _stream(stream),
+        ctypes.byref(timing) if timing is not None else None), "bgpo_elbo_fwd")
+
+
+def bgpo_elbo_bwd_accumulate(prob: Problem, hidden, W_head, targets, resp_mask, adv, ell_old,
+                             loss_scale: float, dX, dW, ell, g, loss, n_masked, t_out,
+                             status_flags, workspace, stream=None,
+                             timing: Optional[Timing] = None):
+    B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
+    _check(_lib.bgpo_elbo_bwd_accumulate(
+        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, (B, L, d)),
+        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
+        _ptr(adv, "adv", (torch.float32,), (B,)),
+        _ptr(ell_old, "ell_old", (torch.float64,), (B, nt), allow_none=True),
+        float(loss_scale),
+        _ptr(dX, "dX", (torch.float32,), (B, L, d)), _ptr(dW, "dW", (torch.float32,), (d, V)),
+        _ptr(ell, "ell", (torch.float64,), (B, nt)), _ptr(g, "g", (torch.float64,), (B, nt)),
+        _ptr(loss, "loss", (torch.float64,), (1,)),
+        _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
+        _ptr(t_out, "t_out", (torch.float32,), (B, nt), allow_none=True),
+        _ptr(status_flags, "status_flags", (torch.int32,), (1,), allow_none=True),
+        _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(), _stream(stream),
+        ctypes.byref(timing) if timing is not None else None), "bgpo_elbo_bwd_accumulate")
+
+
+def bgpo_test_gemm_nt(A, B, C, stream=None):
+    """Test hook: C[m, n] = sum_k A[m, k] B[n, k] through the MFMA GEMM core."""
+    M, K = A.shape
+    N = B.shape[0]
+    _check(_lib.bgpo_test_gemm_nt(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
+                                  _ptr(C, "C", (torch.float32,), (M, N)), M, N, K, _stream(stream)),
+           "bgpo_test_gemm_nt")
+
+
+def device_inputs(x: dict, device="cuda") -> dict:
+    """numpy inputs from the workload generator -> device tensors of the ABI dtypes."""
+    import numpy as np
+    out = {
+        "hidden": torch.from_numpy(x["hidden"].view(np.int16)).to(device).view(torch.bfloat16),
+        "targets": torch.from_numpy(x["targets"].astype(np.int32)).to(device),
+        "resp_mask": torch.from_numpy(x["resp_mask"].astype(np.uint8)).to(device),
+        "adv": torch.from_numpy(x["adv"].astype(np.float32)).to(device),
+    }
+    if x.get("W") is not None:
+        out["W"] = torch.from_numpy(x["W"].view(np.int16)).to(device).view(torch.bfloat16)
+    return out

@@ -1,0 +1,293 @@
+// Host orchestration and the C ABI of libbgpo.
+//
+// One call walks the Monte-Carlo samples j of its range in order (Algorithm 1,
+// inner loop): draw t and the mask, compact and gather the masked rows, run the
+// fused LM-head forward, form l, d, g and the gradient scale, then recompute
+// the logits into dZ = s (softmax - onehot) and accumulate dX and dW before the
+// next sample starts.  All buffers are views into the caller's workspace,
+// sized by B, L, d and V; nothing depends on n_t, so device memory is the same
+// for any number of samples.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "../../include/bgpo.h"
+#include "internal.hpp"
+
+namespace bgpo {
+
+static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
+  const int64_t P = (int64_t)dm.B * dm.L;
+  const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
+  const int64_t nvt = (dm.V + kVocabTile - 1) / kVocabTile;
+  // split of the vocabulary (the K of the dX GEMM) so that a sample with half
+  // of the positions masked still yields about 2048 work tiles
+  const int64_t tiles_half = std::max<int64_t>(1, (NP / 2 + 255) / 256) * ((dm.d + 255) / 256);
+  int64_t n_split = std::min<int64_t>(16, std::max<int64_t>(1, (2048 + tiles_half - 1) / tiles_half));
+  int64_t k_split = ((dm.V + n_split - 1) / n_split + 63) / 64 * 64;
+  n_split = (dm.V + k_split - 1) / k_split;
+
+  size_t off = 0;
+  char* b = static_cast<char*>(base);
+  auto take = [&](size_t bytes) -> void* {
+    void* p = b ? b + off : nullptr;
+    off = align_up(off + bytes, 256);
+    return p;
+  };
+  Workspace w;
+  w.meta = static_cast<SampleMeta*>(take(sizeof(SampleMeta)));
+  w.idx = static_cast<int32_t*>(take(P * 4));
+  w.row_tgt = static_cast<int32_t*>(take(NP * 4));
+  w.row_seq = static_cast<int32_t*>(take(NP * 4));
+  w.seg_off = static_cast<int32_t*>(take((dm.B + 1) * 4));
+  w.t24 = static_cast<uint32_t*>(take(dm.B * 4));
+  w.ztgt = static_cast<float*>(take(NP * 4));
+  w.lse2 = static_cast<float*>(take(NP * 4));
+  w.lp = static_cast<float*>(take(NP * 4));
+  w.row_scale = static_cast<float*>(take(NP * 4));
+  w.part_m = static_cast<float*>(take(nvt * NP * 4));
+  w.part_s = static_cast<float*>(take(nvt * NP * 4));
+  w.Hc = static_cast<uint16_t*>(take(NP * dm.d * 2));
+  w.HcT = static_cast<uint16_t*>(take(NP * dm.d * 2));
+  w.WT = static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2));
+  w.dZ = static_cast<uint16_t*>(take(NP * dm.V * 2));
+  w.dZT = static_cast<uint16_t*>(take(NP * dm.V * 2));
+  w.dx_part = static_cast<float*>(take(n_split * NP * dm.d * 4));
+  w.P = P;
+  w.NP = NP;
+  w.nvt = nvt;
+  w.n_split = n_split;
+  w.k_split = k_split;
+  if (ws) *ws = w;
+  return off;
+}
+
+// HIP-event timing of kernel classes, enabled by a non-NULL record.
+class Timer {
+ public:
+  Timer(bgpo_timing* out, hipStream_t s) : out_(out), s_(s) {}
+  ~Timer() {
+    for (auto& e : ev_) {
+      hipEventDestroy(e.a);
+      hipEventDestroy(e.b);
+    }
+  }
+  hipError_t begin(int kind) {
+    if (!out_) return hipSuccess;
+    Ev e{kind, nullptr, nullptr};
+    hipError_t r = hipEventCreate(&e.a);
+    if (r == hipSuccess) r = hipEventCreate(&e.b);
+    if (r == hipSuccess) r = hipEventRecord(e.a, s_);
+    ev_.push_back(e);
+    return r;
+  }
+  hipError_t end() {
+    if (!out_) return hipSuccess;
+    return hipEventRecord(ev_.back().b, s_);
+  }
+  hipError_t finish() {
+    if (!out_ || ev_.empty()) return hipSuccess;
+    hipError_t r = hipEventSynchronize(ev_.back().b);
+    if (r != hipSuccess) return r;
+    for (auto& e : ev_) {
+      float ms = 0.f;
+      r = hipEventElapsedTime(&ms, e.a, e.b);
+      if (r != hipSuccess) return r;
+      out_->ms[e.kind] += ms;
+      out_->launches[e.kind] += 1;
+    }
+    return hipSuccess;
+  }
+
+ private:
+  struct Ev {
+    int kind;
+    hipEvent_t a, b;
+  };
+  bgpo_timing* out_;
+  hipStream_t s_;
+  std::vector<Ev> ev_;
+};
+
+static int check_problem(const bgpo_problem* p) {
+  if (!p) return BGPO_ERR_INVALID_ARG;
+  if (p->B < 1 || p->L < 1 || p->n_t < 1 || p->j_begin < 0 || p->j_count < 0 ||
+      (int64_t)p->j_begin + p->j_count > p->n_t || (p->t_mode != BGPO_T_IID && p->t_mode != BGPO_T_STRATIFIED) ||
+      p->reserved != 0 || p->d < 1 || p->V < 1)
+    return BGPO_ERR_INVALID_ARG;
+  if (p->B > 4096 || (int64_t)p->B * p->L > (1 << 20) || p->d % 64 || p->V % 64 || p->d < 64 ||
+      p->d > 65536 || p->V < 64 || p->V > (1 << 20))
+    return BGPO_ERR_UNSUPPORTED;
+  return BGPO_OK;
+}
+
+static Dims dims_of(const bgpo_problem* p) { return Dims{p->B, p->L, p->d, p->V, p->n_t}; }
+
+#define BGPO_TRY(expr)                       \
+  do {                                       \
+    if ((expr) != hipSuccess) return BGPO_ERR_HIP; \
+  } while (0)
+
+// forward part of one sample: mask .. l (and, with backward, g / loss / scale)
+static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer& tm, int grid,
+                              int j, const uint16_t* hidden, const int32_t* targets,
+                              const uint8_t* resp, const float* adv, const double* ell_old,
+                              double loss_scale, double* ell, double* g, double* loss,
+                              int32_t* n_masked, float* t_out, int32_t* flags, bool backward,
+                              hipStream_t s) {
+  const Dims dm = dims_of(p);
+  BGPO_TRY(tm.begin(BGPO_K_MASK));
+  BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, p->t_mode, p->seed,
+                               p->seq_id_base, ws.idx, ws.row_tgt, ws.row_seq, ws.seg_off, ws.t24,
+                               ws.meta, n_masked + j, dm.n_t, t_out ? t_out + j : nullptr, dm.n_t,
+                               (int)ws.NP, dm.V, s));
+  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.begin(BGPO_K_GATHER));
+  BGPO_TRY(launch_gather(hidden, ws, dm.d, s));
+  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.begin(BGPO_K_FWD));
+  BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, s));
+  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.begin(BGPO_K_ELL));
+  BGPO_TRY(launch_target_logit(ws, dm.d, s));
+  BGPO_TRY(launch_combine_rows(ws, dm.V, s));
+  BGPO_TRY(launch_seq_terms(ws, dm.B, dm.n_t, j, adv, ell_old, loss_scale, ell, g, loss, flags,
+                            backward, s));
+  BGPO_TRY(tm.end());
+  return BGPO_OK;
+}
+
+static int device_grid(int* grid) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return BGPO_ERR_HIP;
+  *grid = gemm_grid(dev);
+  return BGPO_OK;
+}
+
+}  // namespace bgpo
+
+using namespace bgpo;
+
+extern "C" {
+
+int bgpo_version(void) { return (1 << 16) | 0; }
+
+const char* bgpo_status_string(int status) {
+  switch (status) {
+    case BGPO_OK: return "BGPO_OK";
+    case BGPO_ERR_INVALID_ARG: return "BGPO_ERR_INVALID_ARG: invalid argument";
+    case BGPO_ERR_WORKSPACE: return "BGPO_ERR_WORKSPACE: workspace missing, misaligned or too small";
+    case BGPO_ERR_HIP: return "BGPO_ERR_HIP: a HIP runtime call failed";
+    case BGPO_ERR_UNSUPPORTED: return "BGPO_ERR_UNSUPPORTED: shape outside the supported set";
+    default: return "unknown bgpo status";
+  }
+}
+
+int bgpo_workspace_size(const bgpo_problem* prob, size_t* bytes) {
+  const int st = check_problem(prob);
+  if (st != BGPO_OK) return st;
+  if (!bytes) return BGPO_ERR_INVALID_ARG;
+  *bytes = workspace_layout(dims_of(prob), nullptr, nullptr);
+  return BGPO_OK;
+}
+
+int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_t j, int32_t* idx,
+                      int32_t* n_masked, float* t_out, void* stream) {
+  const int st = check_problem(prob);
+  if (st != BGPO_OK) return st;
+  if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
+  if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, prob->t_mode,
+                          prob->seed, prob->seq_id_base, idx, nullptr, nullptr, nullptr, nullptr,
+                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, (hipStream_t)stream) != hipSuccess)
+    return BGPO_ERR_HIP;
+  return BGPO_OK;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+static int check_workspace(const bgpo_problem* prob, void* workspace, size_t ws_bytes) {
+  if (!workspace || ((uintptr_t)workspace % 256) != 0) return BGPO_ERR_WORKSPACE;
+  if (ws_bytes < workspace_layout(dims_of(prob), nullptr, nullptr)) return BGPO_ERR_WORKSPACE;
+  return BGPO_OK;
+}
+
+int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16_t* W_head,
+                  const int32_t* targets, const uint8_t* resp_mask, double* ell,
+                  int32_t* n_masked, float* t_out, void* workspace, size_t ws_bytes, void* stream,
+                  bgpo_timing* prof) {
+  int st = check_problem(prob);
+  if (st != BGPO_OK) return st;
+  if (!hidden || !W_head || !targets || !resp_mask || !ell || !n_masked) return BGPO_ERR_INVALID_ARG;
+  if (!aligned16(hidden) || !aligned16(W_head)) return BGPO_ERR_INVALID_ARG;
+  if ((st = check_workspace(prob, workspace, ws_bytes)) != BGPO_OK) return st;
+  if (prob->j_count == 0) return BGPO_OK;
+  hipStream_t s = (hipStream_t)stream;
+  Workspace ws;
+  workspace_layout(dims_of(prob), workspace, &ws);
+  int grid = 0;
+  if ((st = device_grid(&grid)) != BGPO_OK) return st;
+  Timer tm(prof, s);
+  BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
+  BGPO_TRY(launch_transpose_w(W_head, ws.WT, prob->d, prob->V, s));
+  BGPO_TRY(tm.end());
+  for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
+    st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, nullptr, nullptr, 0.0,
+                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, s);
+    if (st != BGPO_OK) return st;
+  }
+  BGPO_TRY(tm.finish());
+  return BGPO_OK;
+}
+
+int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
+                             const uint16_t* W_head, const int32_t* targets,
+                             const uint8_t* resp_mask, const float* adv, const double* ell_old,
+                             double loss_scale, float* dX, float* dW, double* ell, double* g,
+                             double* loss, int32_t* n_masked, float* t_out, int32_t* status_flags,
+                             void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof) {
+  int st = check_problem(prob);
+  if (st != BGPO_OK) return st;
+  if (!hidden || !W_head || !targets || !resp_mask || !adv || !dX || !dW || !ell || !g || !loss ||
+      !n_masked || !isfinite(loss_scale))
+    return BGPO_ERR_INVALID_ARG;
+  if (!aligned16(hidden) || !aligned16(W_head) || !aligned16(dX) || !aligned16(dW))
+    return BGPO_ERR_INVALID_ARG;
+  if ((st = check_workspace(prob, workspace, ws_bytes)) != BGPO_OK) return st;
+  if (prob->j_count == 0) return BGPO_OK;
+  hipStream_t s = (hipStream_t)stream;
+  const Dims dm = dims_of(prob);
+  Workspace ws;
+  workspace_layout(dm, workspace, &ws);
+  int grid = 0;
+  if ((st = device_grid(&grid)) != BGPO_OK) return st;
+  Timer tm(prof, s);
+  BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
+  BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
+  BGPO_TRY(tm.end());
+  for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
+    st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, adv, ell_old,
+                            loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, s);
+    if (st != BGPO_OK) return st;
+    BGPO_TRY(tm.begin(BGPO_K_RECOMPUTE));
+    BGPO_TRY(launch_gemm_recompute(ws, dm.d, dm.V, grid, s));
+    BGPO_TRY(launch_onehot(ws, dm.V, s));
+    BGPO_TRY(tm.end());
+    BGPO_TRY(tm.begin(BGPO_K_DX));
+    BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
+    BGPO_TRY(tm.end());
+    BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
+    BGPO_TRY(launch_dx_reduce(ws, dX, dm.d, s));
+    BGPO_TRY(tm.end());
+    BGPO_TRY(tm.begin(BGPO_K_DW));
+    BGPO_TRY(launch_gemm_dw(ws, dW, dm.d, dm.V, grid, s));
+    BGPO_TRY(tm.end());
+  }
+  BGPO_TRY(tm.finish());
+  return BGPO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,65 @@
+// Device-side helpers shared by the BGPO ELBO-head kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bgpo {
+
+typedef uint16_t bf16_t;                                   // bfloat16 bit pattern
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));  // MFMA operand
+typedef float f32x16 __attribute__((ext_vector_type(16)));  // 32x32 MFMA accumulator
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): 10 rounds of two 32x32->64
+// multiplies with key mixing; the key advances by the Weyl constants between
+// rounds.
+struct u32x4 {
+  uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = u32x4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+  }
+  return c;
+}
+
+__device__ __forceinline__ uint32_t pick_word(const u32x4& v, int i) {
+  return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+// Integer timestep T24 in [1, 2^24): t = T24 * 2^-24 (exact in fp32 and fp64).
+__device__ __forceinline__ uint32_t timestep_t24(uint32_t k0, uint32_t k1, uint32_t seq, int j,
+                                                 int n_t, int t_mode) {
+  if (t_mode == 0) {
+    const u32x4 w = philox4x32_10(u32x4{0u, seq, (uint32_t)j, 1u}, k0, k1);
+    const uint32_t T = w.x >> 8;
+    return T ? T : 1u;
+  }
+  const u32x4 w = philox4x32_10(u32x4{0u, seq, 0u, 2u}, k0, k1);
+  const uint64_t u24 = w.x >> 8;
+  const uint64_t T = (((uint64_t)j << 24) + u24) / (uint64_t)n_t;
+  return T ? (uint32_t)T : 1u;
+}
+
+// float -> bfloat16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+}  // namespace bgpo

@@ -1,0 +1,439 @@
+// bf16 MFMA GEMM core for gfx950 and its four epilogues.
+//
+// Every contraction of the ELBO head is written in one "NT" form,
+//     C[m][n] = sum_k A[m][k] * B[n][k]      (A, B row-major, K contiguous),
+// so both operands load as 16-byte K-contiguous vectors that match the
+// v_mfma_f32_32x32x16_bf16 operand layout directly:
+//   forward / recompute   Z^T[v][row] = WT[v][:] . Hc[row][:]     (K = d)
+//   dX (split over V)     dX[row][c]  = dZ[row][:] . W[c][:]      (K = V)
+//   dW                    dW[c][v]   += HcT[c][:] . dZT[v][:]     (K = rows)
+// The logits are produced as Z^T (vocabulary along M) so that, in the 32x32
+// accumulator layout, each lane holds 64 vocabulary entries of only 4 rows:
+// the per-row max / sum-exp reductions are in-lane plus one lane swap.
+//
+// Scheduling: a persistent grid of one 256-thread workgroup per compute unit
+// walks the tile list; consecutive tiles (sharing an operand panel) are given
+// to workgroups of the same XCD (workgroup w runs on XCD w mod 8), so the
+// shared panel is served from that XCD's L2.
+//
+// Pipeline: two LDS stages; the next K slab is loaded into registers while
+// the current one feeds the MFMAs, then written to the other stage.  LDS rows
+// are XOR-swizzled in 16-byte chunks so that the fragment reads of 8
+// consecutive rows hit distinct banks.
+#include "common.hpp"
+#include "internal.hpp"
+
+#include <string.h>
+
+namespace bgpo {
+
+enum EpiKind { EPI_FWD = 0, EPI_DZ = 1, EPI_F32_STORE = 2, EPI_F32_ACCUM = 3 };
+
+struct GemmParams {
+  const uint16_t* A;
+  int64_t lda;
+  const uint16_t* B;
+  int64_t ldb;
+  int M, N, K;               // static extents
+  int dyn_m, dyn_n, dyn_k;   // extents taken from the device sample metadata
+  int n_split;               // K split count (dX)
+  int64_t k_split;           // K per split (multiple of BK)
+  int m_fastest;             // tile order: 1 = M tiles consecutive, 0 = N tiles consecutive
+  const SampleMeta* meta;
+  // epilogue operands
+  float* out;                // F32 store / accumulate target
+  int64_t ldo, split_stride;
+  float* part_m;             // FWD: per-vocab-tile (max, sum) partials [M/BM][ldp]
+  float* part_s;
+  int64_t ldp;
+  float* ztgt;               // FWD: target logit per row
+  const int32_t* row_tgt;
+  const float* lse2;         // DZ
+  const float* row_scale;    // DZ
+  uint16_t* dZ;              // DZ: [rows][ldz]
+  int64_t ldz;
+  uint16_t* dZT;             // DZ: [V][ldzt]
+  int64_t ldzt;
+};
+
+template <int BM, int BN, int BK, int WM, int WN>
+struct Cfg {
+  static constexpr int NWM = BM / WM, NWN = BN / WN;
+  static constexpr int NWAVES = NWM * NWN;
+  static constexpr int NT = NWAVES * 64;
+  static constexpr int TM = WM / 32, TN = WN / 32;
+  static constexpr int KCH = BK / 8;                  // 16-byte chunks per LDS row
+  static constexpr int A_LD = BM * KCH / NT, B_LD = BN * KCH / NT;
+  static constexpr int ROWS_PER_128B = 8 / KCH;
+  static_assert(BM * KCH % NT == 0 && BN * KCH % NT == 0, "load split");
+  static_assert(KCH == 4 || KCH == 8, "BK must be 32 or 64");
+  __device__ static __forceinline__ int swz(int row) { return (row / ROWS_PER_128B) % KCH; }
+};
+
+// fp32 store (dX partials) or read-modify-write accumulate (dW), one 32-row
+// band of the wave tile at a time so the loads stay in flight without spills.
+template <bool ACCUM, bool FULL, int TM, int TN>
+__device__ __forceinline__ void epi_f32(const f32x16 (&acc)[TM][TN], float* outb, int64_t ldo,
+                                        int mw, int nw, int mlane, int lane, int M, int N) {
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    float old[TN][16];
+    if constexpr (ACCUM) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = nw + 32 * j + (lane & 31);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2);
+          old[j][e] = (FULL || (m < M && n < N)) ? outb[(int64_t)m * ldo + n] : 0.f;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = nw + 32 * j + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2);
+        if (FULL || (m < M && n < N))
+          outb[(int64_t)m * ldo + n] = ACCUM ? old[j][e] + acc[i][j][e] : acc[i][j][e];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Issue one K slab of both operand tiles into LDS stage `stage`.
+template <int BM, int BN, int KCH, int A_INS, int B_INS>
+__device__ __forceinline__ void issue_slab_loads(uint4* As, uint4* Bs, int stage, int wave,
+                                                 __amdgpu_buffer_rsrc_t a_rsrc,
+                                                 __amdgpu_buffer_rsrc_t b_rsrc,
+                                                 const uint32_t (&a_voff)[A_INS],
+                                                 const uint32_t (&b_voff)[B_INS], int soff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+  for (int q = 0; q < A_INS; ++q) {
+    uint4* dst = As + stage * BM * KCH + (wave * A_INS + q) * 64;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        a_rsrc, (__attribute__((address_space(3))) void*)dst, 16, a_voff[q], soff, 0, 0);
+  }
+#pragma unroll
+  for (int q = 0; q < B_INS; ++q) {
+    uint4* dst = Bs + stage * BN * KCH + (wave * B_INS + q) * 64;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        b_rsrc, (__attribute__((address_space(3))) void*)dst, 16, b_voff[q], soff, 0, 0);
+  }
+#endif
+}
+
+template <int EPI, int BM, int BN, int BK, int WM, int WN>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, 1) void k_gemm(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature
+  using C = Cfg<BM, BN, BK, WM, WN>;
+  constexpr int NT = C::NT, TM = C::TM, TN = C::TN, KCH = C::KCH;
+  __shared__ uint4 smem[2 * (BM + BN) * KCH];
+  uint4* As = smem;                      // [2][BM][KCH]
+  uint4* Bs = smem + 2 * BM * KCH;       // [2][BN][KCH]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / C::NWN, wn = wave % C::NWN;
+
+  int M = p.M, N = p.N, K = p.K, n_valid = p.N;
+  if (p.dyn_m) { M = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
+  if (p.dyn_n) { N = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
+  if (p.dyn_k) K = (p.meta->n_rows + BK - 1) / BK * BK;
+  if (EPI == EPI_F32_ACCUM && K == 0) return;   // nothing to add
+  const int tilesM = (M + BM - 1) / BM, tilesN = (N + BN - 1) / BN;
+  const int64_t total = (int64_t)tilesM * tilesN * p.n_split;
+  const int G = gridDim.x;
+  const int w = blockIdx.x;
+  const int xcd_slot = (G % 8 == 0) ? (w % 8) * (G / 8) + w / 8 : w;
+
+  for (int64_t base = 0; base < total; base += G) {
+    const int64_t t = base + xcd_slot;
+    if (t >= total) continue;
+    int mt, nt, split;
+    {
+      const int64_t per_split = (int64_t)tilesM * tilesN;
+      split = (int)(t / per_split);
+      const int64_t r = t - (int64_t)split * per_split;
+      if (p.m_fastest) { mt = (int)(r % tilesM); nt = (int)(r / tilesM); }
+      else { nt = (int)(r % tilesN); mt = (int)(r / tilesN); }
+    }
+    const int m0 = mt * BM, n0 = nt * BN;
+    const int64_t kb = (int64_t)split * p.k_split;
+    const int64_t ke = min((int64_t)K, kb + p.k_split);
+    const int nk = ke > kb ? (int)((ke - kb) / BK) : 0;
+
+    // accumulator element (i, j, e) sits at
+    //   m = mw + 32 i + 4 (lane >> 5) + (e & 3) + 8 (e >> 2),  n = nw + 32 j + (lane & 31)
+    const int mw = m0 + wm * WM, nw = n0 + wn * WN;
+    const int mlane = 4 * (lane >> 5);
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    // Operand panels as buffer resources (wave-uniform): rows [m0, m0 + BM) of A
+    // and [n0, n0 + BN) of B.  Each load instruction moves 64 lanes x 16 bytes
+    // straight into LDS (lane l lands at byte 16 l of the instruction's LDS
+    // block), so the XOR swizzle is applied on the global side: lane l of
+    // block g fetches logical chunk (l mod KCH) ^ swz(row) of row
+    // g * RPI + l / KCH.  Rows past the matrix are clamped to its last row.
+    const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.A + (int64_t)m0 * p.lda), (short)0, 0x7FFFFFFF, 0x00020000);
+    const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.B + (int64_t)n0 * p.ldb), (short)0, 0x7FFFFFFF, 0x00020000);
+    constexpr int RPI = 64 / KCH;                        // rows per load instruction
+    constexpr int A_INS = BM / RPI / C::NWAVES, B_INS = BN / RPI / C::NWAVES;
+    uint32_t a_voff[A_INS], b_voff[B_INS];
+#pragma unroll
+    for (int q = 0; q < A_INS; ++q) {
+      const int g = wave * A_INS + q, row = g * RPI + lane / KCH;
+      const int c = (lane % KCH) ^ C::swz(row);
+      const int rr = min(m0 + row, M - 1) - m0;
+      a_voff[q] = (uint32_t)(rr * p.lda * 2 + c * 16);
+    }
+#pragma unroll
+    for (int q = 0; q < B_INS; ++q) {
+      const int g = wave * B_INS + q, row = g * RPI + lane / KCH;
+      const int c = (lane % KCH) ^ C::swz(row);
+      const int rr = min(n0 + row, N - 1) - n0;
+      b_voff[q] = (uint32_t)(rr * p.ldb * 2 + c * 16);
+    }
+    if (nk > 0) {
+      issue_slab_loads<BM, BN, KCH, A_INS, B_INS>(As, Bs, 0, wave, a_rsrc, b_rsrc, a_voff, b_voff, (int)(kb * 2));
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+
+      for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        if (kt + 1 < nk)
+          issue_slab_loads<BM, BN, KCH, A_INS, B_INS>(As, Bs, cur ^ 1, wave, a_rsrc, b_rsrc, a_voff,
+                                                      b_voff, (int)((kb + (int64_t)(kt + 1) * BK) * 2));
+        const uint4* Ac = As + cur * BM * KCH;
+        const uint4* Bc = Bs + cur * BN * KCH;
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+          const int ch = ks * 2 + (lane >> 5);
+          bf16x8 af[TM], bfr[TN];
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const int row = wm * WM + i * 32 + (lane & 31);
+            af[i] = __builtin_bit_cast(bf16x8, Ac[row * KCH + (ch ^ C::swz(row))]);
+          }
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int row = wn * WN + j * 32 + (lane & 31);
+            bfr[j] = __builtin_bit_cast(bf16x8, Bc[row * KCH + (ch ^ C::swz(row))]);
+          }
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+      }
+    }
+
+    // ---------------- epilogues ----------------
+    if constexpr (EPI == EPI_FWD) {
+      // per (row, vocabulary tile): running max and sum of exponentials, in
+      // log2 units; the lanes l and l ^ 32 hold the two halves of a row's
+      // 64-entry slice, the waves along M hold the other slices.
+      float* red = reinterpret_cast<float*>(smem);   // [NWM][BN] max, then [NWM][BN] sum
+      const bool full_m = m0 + BM <= M;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        float mx = -INFINITY;
+        if (full_m) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[i][j][e]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int m = mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2);
+              if (m < M) mx = fmaxf(mx, acc[i][j][e]);
+            }
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mx2 = mx * kLog2e;
+        float s = 0.f;
+        if (mx2 > -INFINITY) {
+          if (full_m) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+              for (int e = 0; e < 16; ++e)
+                s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mx2));
+          } else {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+              for (int e = 0; e < 16; ++e) {
+                const int m = mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2);
+                if (m < M) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mx2));
+              }
+          }
+        }
+        s += __shfl_xor(s, 32, 64);
+        if (lane < 32) {
+          const int nl = wn * WN + 32 * j + lane;
+          red[wm * BN + nl] = mx2;
+          red[C::NWM * BN + wm * BN + nl] = s;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      __syncthreads();
+      const int vt = m0 / BM;
+      for (int q = tid; q < BN; q += NT) {
+        const int n = n0 + q;
+        if (n >= n_valid) continue;
+        float M2 = -INFINITY;
+#pragma unroll
+        for (int a = 0; a < C::NWM; ++a) M2 = fmaxf(M2, red[a * BN + q]);
+        float S = 0.f;
+#pragma unroll
+        for (int a = 0; a < C::NWM; ++a) {
+          const float sa = red[C::NWM * BN + a * BN + q];
+          if (sa > 0.f) S += sa * __builtin_amdgcn_exp2f(red[a * BN + q] - M2);
+        }
+        p.part_m[(int64_t)vt * p.ldp + n] = M2;
+        p.part_s[(int64_t)vt * p.ldp + n] = S;
+      }
+    } else if constexpr (EPI == EPI_DZ) {
+      // dZ = s * softmax (the -s at the target is applied afterwards by a
+      // separate one-element-per-row kernel); padded rows get zeros.
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = nw + 32 * j + (lane & 31);
+        const bool valid = n < n_valid;
+        const float L2 = valid ? p.lse2[n] : 0.f;
+        const float sc = valid ? p.row_scale[n] : 0.f;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            const int m = mw + 32 * i + mlane + 8 * e4;   // vocabulary ids m .. m+3
+            if (m < M && n < N) {
+              bf16_t h[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float pz = __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * e4 + e], kLog2e, -L2));
+                h[e] = f32_to_bf16(valid ? sc * pz : 0.f);
+                p.dZT[(int64_t)(m + e) * p.ldzt + n] = h[e];
+              }
+              uint2 pk;
+              pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+              pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+              *reinterpret_cast<uint2*>(p.dZ + (int64_t)n * p.ldz + m) = pk;
+            }
+          }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      // fp32 store (dX partials) or read-modify-write accumulate (dW); one
+      // 32-row band of the wave tile at a time keeps the loads in flight
+      // without spilling.
+      float* outb = p.out + (int64_t)split * p.split_stride;
+      if (m0 + BM <= M && n0 + BN <= N) epi_f32<EPI == EPI_F32_ACCUM, true, TM, TN>(acc, outb, p.ldo, mw, nw, mlane, lane, M, N);
+      else epi_f32<EPI == EPI_F32_ACCUM, false, TM, TN>(acc, outb, p.ldo, mw, nw, mlane, lane, M, N);
+    }
+    __syncthreads();
+  }
+#endif
+}
+
+// Tile configuration of the production kernels: 256x256 block tile, K slab
+// 64, four waves each owning a 128x128 sub-tile (4x4 MFMA 32x32 tiles).
+#define BGPO_TILE 256, 256, 64, 128, 128
+constexpr int kGemmThreads = 256;
+
+static GemmParams base_params() {
+  GemmParams p;
+  memset(&p, 0, sizeof(p));
+  p.n_split = 1;
+  p.k_split = INT64_MAX / 4;
+  return p;
+}
+
+hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, hipStream_t s) {
+  GemmParams p = base_params();
+  p.A = ws.WT; p.lda = d;
+  p.B = ws.Hc; p.ldb = d;
+  p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.meta;
+  p.k_split = d;
+  p.part_m = ws.part_m; p.part_s = ws.part_s; p.ldp = ws.NP;
+  p.ztgt = ws.ztgt; p.row_tgt = ws.row_tgt;
+  k_gemm<EPI_FWD, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_recompute(const Workspace& ws, int d, int V, int grid, hipStream_t s) {
+  GemmParams p = base_params();
+  p.A = ws.WT; p.lda = d;
+  p.B = ws.Hc; p.ldb = d;
+  p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.meta;
+  p.k_split = d;
+  p.row_tgt = ws.row_tgt; p.lse2 = ws.lse2; p.row_scale = ws.row_scale;
+  p.dZ = ws.dZ; p.ldz = V; p.dZT = ws.dZT; p.ldzt = ws.NP;
+  k_gemm<EPI_DZ, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
+                          hipStream_t s) {
+  GemmParams p = base_params();
+  p.A = ws.dZ; p.lda = V;
+  p.B = W; p.ldb = V;
+  p.N = d; p.K = V; p.dyn_m = 1; p.meta = ws.meta;
+  p.n_split = (int)ws.n_split; p.k_split = ws.k_split;
+  p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.NP * d;
+  k_gemm<EPI_F32_STORE, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s) {
+  GemmParams p = base_params();
+  p.A = ws.HcT; p.lda = ws.NP;
+  p.B = ws.dZT; p.ldb = ws.NP;
+  p.M = d; p.N = V; p.dyn_k = 1; p.meta = ws.meta;
+  p.m_fastest = 1;
+  p.out = dW; p.ldo = V;
+  k_gemm<EPI_F32_ACCUM, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+int gemm_grid(int device) {
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  return cus;  // one 256-thread workgroup per compute unit
+}
+
+}  // namespace bgpo
+
+// ---- test hook: the GEMM core alone, C[m][n] = sum_k A[m][k] B[n][k] in fp32 ----
+extern "C" int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
+                                 int32_t K, void* stream) {
+  using namespace bgpo;
+  if (!A || !B || !C || M <= 0 || N <= 0 || K <= 0 || K % 64) return -1;
+  GemmParams p = base_params();
+  p.A = A; p.lda = K; p.B = B; p.ldb = K;
+  p.M = M; p.N = N; p.K = K; p.k_split = K;
+  p.out = C; p.ldo = N;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -3;
+  k_gemm<EPI_F32_STORE, BGPO_TILE><<<gemm_grid(dev), kGemmThreads, 0, (hipStream_t)stream>>>(p);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}

@@ -1,0 +1,77 @@
+// Host-side declarations shared by the translation units of libbgpo.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bgpo {
+
+// Rows of the compacted masked-position list are padded to a multiple of
+// this (the row tile of the LM-head GEMMs); padded rows carry zeros.
+constexpr int kRowPad = 256;
+// Column tile of the LM-head GEMM over the vocabulary = one log-sum-exp partial.
+constexpr int kVocabTile = 256;
+
+constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
+
+// Device-resident per-sample bookkeeping written by the mask kernel.
+struct SampleMeta {
+  int32_t n_rows;      // N_j: masked positions in this sample (all responses)
+  int32_t n_rows_pad;  // N_j rounded up to kRowPad
+  int32_t pad[62];
+};
+
+// Views into the caller's workspace.
+struct Workspace {
+  SampleMeta* meta;
+  int32_t* idx;        // [P]          masked flat positions, ascending
+  int32_t* row_tgt;    // [NP]         target token of each compacted row
+  int32_t* row_seq;    // [NP]         response of each compacted row (B for padding)
+  int32_t* seg_off;    // [B+1]        first compacted row of each response
+  uint32_t* t24;       // [B]          integer timestep of each response
+  uint16_t* Hc;        // [NP, d]      gathered masked hidden rows (bf16)
+  uint16_t* HcT;       // [d, NP]      the same, transposed
+  uint16_t* WT;        // [V, d]       W_head transposed (bf16)
+  float* part_m;       // [nvt, NP]    per-vocab-tile running max (log2 units)
+  float* part_s;       // [nvt, NP]    per-vocab-tile sum of 2^(z*log2e - max)
+  float* ztgt;         // [NP]         target logit
+  float* lse2;         // [NP]         log2-sum-exp2 of each row (log2 units)
+  float* lp;           // [NP]         log p of the target
+  float* row_scale;    // [NP]         gradient scale s of each row (0 for padding)
+  uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16
+  uint16_t* dZT;       // [V, NP]      the same, transposed
+  float* dx_part;      // [S, NP, d]   split-vocabulary partial dX
+  int64_t P, NP, nvt, n_split, k_split;
+};
+
+struct Dims {
+  int B, L, d, V, n_t;
+};
+
+size_t workspace_layout(const Dims& dm, void* base, Workspace* ws);  // base may be NULL
+
+// ---- launchers (return hipSuccess or the launch error) ----
+hipError_t launch_transpose_w(const uint16_t* W, uint16_t* WT, int d, int V, hipStream_t s);
+hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int B, int L, int n_t, int j,
+                               int t_mode, uint64_t seed, uint32_t seq_base, int32_t* idx,
+                               int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
+                               SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
+                               float* t_out, int t_stride, int row_cap, int V, hipStream_t s);
+hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s);
+hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, hipStream_t s);
+hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s);
+hipError_t launch_onehot(const Workspace& ws, int V, hipStream_t s);
+hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s);
+hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const float* adv,
+                            const double* ell_old, double loss_scale, double* ell, double* g,
+                            double* loss, int32_t* flags, bool backward, hipStream_t s);
+hipError_t launch_gemm_recompute(const Workspace& ws, int d, int V, int grid, hipStream_t s);
+hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
+                          hipStream_t s);
+hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s);
+hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s);
+
+int gemm_grid(int device);  // persistent grid size of the GEMM kernels on `device`
+
+}  // namespace bgpo

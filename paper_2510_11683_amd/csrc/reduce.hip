@@ -1,0 +1,215 @@
+// Row and response reductions of the ELBO head:
+//   target logit      z[row, y_row] = Hc[row] . W[:, y_row]
+//   log-sum-exp       combine the per-vocabulary-tile (max, sum) partials
+//   per-response      l = (1/t) sum log p (Eq. per_step_loss), d, g (Eq. g),
+//                     loss (Algorithm 1, L_j = -g_j/G) and the gradient scale
+//   one-hot           dZ[row, y_row] = s (p_y - 1), the target term of the
+//                     softmax-minus-onehot backward
+//   dX                sum of the split-vocabulary partials, scattered to the
+//                     masked positions
+// Every reduction runs in a fixed order, so results are bit-reproducible.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace bgpo {
+
+// One wave per row: 64 lanes split the d-long dot product.
+__global__ __launch_bounds__(256) void k_target_logit(const uint16_t* __restrict__ Hc,
+                                                      const uint16_t* __restrict__ WT,
+                                                      const int32_t* __restrict__ row_tgt,
+                                                      const SampleMeta* __restrict__ meta,
+                                                      float* __restrict__ ztgt, int d) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= meta->n_rows) return;
+  const uint16_t* h = Hc + (int64_t)row * d;
+  const uint16_t* w = WT + (int64_t)row_tgt[row] * d;
+  float acc = 0.f;
+  for (int k = lane * 8; k < d; k += 64 * 8) {
+    const uint4 hv = *reinterpret_cast<const uint4*>(h + k);
+    const uint4 wv = *reinterpret_cast<const uint4*>(w + k);
+    const uint32_t ha[4] = {hv.x, hv.y, hv.z, hv.w}, wa[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc = fmaf(__uint_as_float(ha[e] << 16), __uint_as_float(wa[e] << 16), acc);
+      acc = fmaf(__uint_as_float(ha[e] & 0xFFFF0000u), __uint_as_float(wa[e] & 0xFFFF0000u), acc);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+  if (lane == 0) ztgt[row] = acc;
+}
+
+hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s) {
+  k_target_logit<<<(unsigned)(ws.NP / 4), 256, 0, s>>>(ws.Hc, ws.WT, ws.row_tgt, ws.meta, ws.ztgt, d);
+  return hipGetLastError();
+}
+
+// One wave per row: lanes stride over the vocabulary-tile partials.
+__global__ __launch_bounds__(256) void k_combine_rows(const float* __restrict__ part_m,
+                                                      const float* __restrict__ part_s,
+                                                      const float* __restrict__ ztgt,
+                                                      const SampleMeta* __restrict__ meta,
+                                                      float* __restrict__ lse2, float* __restrict__ lp,
+                                                      int nvt, int64_t ldp) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= meta->n_rows) return;
+  float m = -INFINITY, s = 0.f;
+  for (int t = lane; t < nvt; t += 64) {
+    const float mt = part_m[(int64_t)t * ldp + row], st = part_s[(int64_t)t * ldp + row];
+    if (st > 0.f) {
+      const float mn = fmaxf(m, mt);
+      s = s * exp2f(m - mn) + st * exp2f(mt - mn);
+      m = mn;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float mo = __shfl_xor(m, off, 64), so = __shfl_xor(s, off, 64);
+    const float mn = fmaxf(m, mo);
+    const float a = s > 0.f ? s * exp2f(m - mn) : 0.f;
+    const float b = so > 0.f ? so * exp2f(mo - mn) : 0.f;
+    s = a + b;
+    m = mn;
+  }
+  if (lane == 0) {
+    const float l2 = m + log2f(s);
+    lse2[row] = l2;
+    lp[row] = ztgt[row] - l2 * kLn2;
+  }
+}
+
+hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s) {
+  k_combine_rows<<<(unsigned)(ws.NP / 4), 256, 0, s>>>(ws.part_m, ws.part_s, ws.ztgt, ws.meta,
+                                                      ws.lse2, ws.lp, (int)ws.nvt, ws.NP);
+  return hipGetLastError();
+}
+
+// Per-response terms of sample j.  One workgroup; responses in order.
+constexpr int kSeqThreads = 1024;
+constexpr int kSeqMaxB = 4096;
+
+__global__ __launch_bounds__(kSeqThreads) void k_seq_terms(
+    const float* __restrict__ lp, const int32_t* __restrict__ seg_off,
+    const uint32_t* __restrict__ t24, const int32_t* __restrict__ row_seq,
+    const SampleMeta* __restrict__ meta, int B, int n_t, int j, const float* __restrict__ adv,
+    const double* __restrict__ ell_old, double loss_scale, double* __restrict__ ell,
+    double* __restrict__ g, double* __restrict__ loss, int32_t* __restrict__ flags,
+    float* __restrict__ row_scale, int backward) {
+  __shared__ double red[kSeqThreads / 64];
+  __shared__ float s_scale[kSeqMaxB];
+  __shared__ int s_bad;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) s_bad = 0;
+  double loss_acc = 0.0;
+  for (int b = 0; b < B; ++b) {
+    const int r0 = seg_off[b], r1 = seg_off[b + 1];
+    double acc = 0.0;
+    for (int r = r0 + tid; r < r1; r += kSeqThreads) acc += (double)lp[r];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) red[wave] = acc;
+    __syncthreads();
+    if (tid == 0) {
+      double sum = 0.0;
+      for (int w = 0; w < kSeqThreads / 64; ++w) sum += red[w];
+      const double t = (double)t24[b] * (1.0 / 16777216.0);
+      const double l = sum / t;                                      // Eq. per_step_loss
+      const int64_t o = (int64_t)b * n_t + j;
+      ell[o] = l;
+      if (backward) {
+        const double dj = ell_old ? l - ell_old[o] : 0.0;
+        const double A = (double)adv[b];
+        double gj, dg;
+        if (A >= 0.0) {                 // first-order Taylor bound (Lemma 1)
+          gj = (1.0 + dj) * A / n_t;
+          dg = A / n_t;
+        } else {                        // Jensen bound (Lemma 2)
+          const double e = exp(dj);
+          gj = e * A / n_t;
+          dg = gj;
+        }
+        g[o] = gj;
+        loss_acc += -loss_scale * gj;
+        const double sc = loss_scale * dg / t;
+        s_scale[b] = (float)sc;
+        if (!isfinite(l) || !isfinite(gj) || !isfinite(sc) || !isfinite((float)sc)) s_bad = 1;
+      } else if (!isfinite(l)) {
+        s_bad = 1;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    if (backward) loss[0] += loss_acc;
+    if (s_bad && flags) atomicOr(flags, kFlagNonfinite);
+  }
+  if (backward) {
+    const int N = meta->n_rows, NPr = meta->n_rows_pad;
+    for (int r = tid; r < NPr; r += kSeqThreads) row_scale[r] = r < N ? s_scale[row_seq[r]] : 0.f;
+  }
+}
+
+hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const float* adv,
+                            const double* ell_old, double loss_scale, double* ell, double* g,
+                            double* loss, int32_t* flags, bool backward, hipStream_t s) {
+  k_seq_terms<<<1, kSeqThreads, 0, s>>>(ws.lp, ws.seg_off, ws.t24, ws.row_seq, ws.meta, B, n_t, j,
+                                        adv, ell_old, loss_scale, ell, g, loss, flags,
+                                        ws.row_scale, backward ? 1 : 0);
+  return hipGetLastError();
+}
+
+// dZ[row, y] = bf16(s (p_y - 1)) in both layouts; the recompute epilogue wrote
+// bf16(s p_y) there.
+__global__ __launch_bounds__(256) void k_onehot(const int32_t* __restrict__ row_tgt,
+                                                const float* __restrict__ ztgt,
+                                                const float* __restrict__ lse2,
+                                                const float* __restrict__ row_scale,
+                                                const SampleMeta* __restrict__ meta,
+                                                uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT,
+                                                int V, int64_t ldzt) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= meta->n_rows) return;
+  const int y = row_tgt[r];
+  const float py = __builtin_amdgcn_exp2f(fmaf(ztgt[r], kLog2e, -lse2[r]));
+  const bf16_t h = f32_to_bf16(row_scale[r] * (py - 1.f));
+  dZ[(int64_t)r * V + y] = h;
+  dZT[(int64_t)y * ldzt + r] = h;
+}
+
+hipError_t launch_onehot(const Workspace& ws, int V, hipStream_t s) {
+  k_onehot<<<(unsigned)(ws.NP / 256), 256, 0, s>>>(ws.row_tgt, ws.ztgt, ws.lse2, ws.row_scale,
+                                                  ws.meta, ws.dZ, ws.dZT, V, ws.NP);
+  return hipGetLastError();
+}
+
+// dX[idx[r], :] += sum_s part[s][r][:], float4 per thread; rows are unique
+// within a sample, so there are no write conflicts.
+__global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ part,
+                                                   const int32_t* __restrict__ idx,
+                                                   const SampleMeta* __restrict__ meta,
+                                                   float* __restrict__ dX, int d, int n_split,
+                                                   int64_t split_stride) {
+  const int r = blockIdx.x;
+  if (r >= meta->n_rows) return;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (c >= d) return;
+  float4 acc = *reinterpret_cast<const float4*>(part + (int64_t)r * d + c);
+  for (int s = 1; s < n_split; ++s) {
+    const float4 v = *reinterpret_cast<const float4*>(part + s * split_stride + (int64_t)r * d + c);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  float4* dst = reinterpret_cast<float4*>(dX + (int64_t)idx[r] * d + c);
+  float4 o = *dst;
+  o.x += acc.x; o.y += acc.y; o.z += acc.z; o.w += acc.w;
+  *dst = o;
+}
+
+hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s) {
+  dim3 grid((unsigned)ws.NP, (unsigned)((d / 4 + 255) / 256));
+  k_dx_reduce<<<grid, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta, dX, d, (int)ws.n_split, ws.NP * d);
+  return hipGetLastError();
+}
+
+}  // namespace bgpo

@@ -1,0 +1,218 @@
+// Timestep draw, Bernoulli(t) masking, stable stream compaction of the masked
+// positions, gather of the masked hidden rows, and the one-off W_head
+// transpose.
+//
+// The forward masking process (Section 2.1) masks every response token
+// independently with probability t; the ELBO term (Eq. per_step_loss) only
+// touches masked positions, so the rows that reach the LM-head GEMMs are the
+// masked ones, compacted in ascending flat order b*L + i.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace bgpo {
+
+constexpr int kMaskThreads = 1024;
+constexpr int kMaxB = 4096;
+
+// Philox words for position p = b*L + i are taken from counter (i>>2, seq, j, 0);
+// consecutive positions of one response share a counter block, so a thread
+// caches the last block it computed.
+struct MaskWalker {
+  uint32_t k0, k1, seq_base;
+  int L, j;
+  int cached_b = -1, cached_blk = -1;
+  u32x4 w;
+  __device__ bool masked(const uint8_t* resp, const uint32_t* sT, int64_t p) {
+    const int b = (int)(p / L);
+    const int i = (int)(p - (int64_t)b * L);
+    if (!resp[p]) return false;
+    const int blk = i >> 2;
+    if (blk != cached_blk || b != cached_b) {
+      w = philox4x32_10(u32x4{(uint32_t)blk, seq_base + (uint32_t)b, (uint32_t)j, 0u}, k0, k1);
+      cached_blk = blk;
+      cached_b = b;
+    }
+    return (pick_word(w, i & 3) >> 8) < sT[b];
+  }
+};
+
+__global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
+    const uint8_t* __restrict__ resp, const int32_t* __restrict__ targets, int B, int L, int n_t,
+    int j, int t_mode, uint32_t k0, uint32_t k1, uint32_t seq_base, int32_t* __restrict__ idx,
+    int32_t* __restrict__ row_tgt, int32_t* __restrict__ row_seq, int32_t* __restrict__ seg_off,
+    uint32_t* __restrict__ t24_out, SampleMeta* __restrict__ meta, int32_t* __restrict__ nm_out,
+    int nm_stride, float* __restrict__ t_out, int t_stride, int row_cap, int V) {
+  __shared__ uint32_t sT[kMaxB];
+  __shared__ int32_t sSeg[kMaxB + 1];
+  __shared__ int32_t sWave[kMaskThreads / 64];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+
+  for (int b = tid; b < B; b += kMaskThreads)
+    sT[b] = timestep_t24(k0, k1, seq_base + (uint32_t)b, j, n_t, t_mode);
+  __syncthreads();
+
+  const int64_t P = (int64_t)B * L;
+  const int64_t chunk = (P + kMaskThreads - 1) / kMaskThreads;
+  const int64_t p0 = min(P, (int64_t)tid * chunk), p1 = min(P, p0 + chunk);
+
+  MaskWalker mw{k0, k1, seq_base, L, j};
+  int cnt = 0;
+  for (int64_t p = p0; p < p1; ++p) cnt += mw.masked(resp, sT, p) ? 1 : 0;
+
+  // block-wide exclusive scan of the per-thread counts
+  int incl = cnt;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  if (lane == 63) sWave[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    int wv = lane < kMaskThreads / 64 ? sWave[lane] : 0;
+    int wincl = wv;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(wincl, off, 64);
+      if (lane >= off) wincl += v;
+    }
+    if (lane < kMaskThreads / 64) sWave[lane] = wincl - wv;  // exclusive
+  }
+  __syncthreads();
+  int base = sWave[wave] + incl - cnt;
+
+  MaskWalker mw2{k0, k1, seq_base, L, j};
+  for (int64_t p = p0; p < p1; ++p) {
+    const int b = (int)(p / L);
+    if (p == (int64_t)b * L) sSeg[b] = base;
+    if (mw2.masked(resp, sT, p)) {
+      if (idx) idx[base] = (int32_t)p;
+      if (row_tgt) {
+        // ids outside [0, V) are clamped so that no kernel reads outside W
+        const int y = targets[p];
+        row_tgt[base] = y < 0 ? 0 : (y >= V ? V - 1 : y);
+      }
+      if (row_seq) row_seq[base] = b;
+      ++base;
+    }
+  }
+  if (tid == kMaskThreads - 1) sSeg[B] = base;  // the last thread ends at P
+  __syncthreads();
+
+  const int total = sSeg[B];
+  const int total_pad = (total + kRowPad - 1) / kRowPad * kRowPad;
+  for (int b = tid; b < B; b += kMaskThreads) {
+    const int nm = sSeg[b + 1] - sSeg[b];
+    if (nm_out) nm_out[(int64_t)b * nm_stride] = nm;
+    if (t_out) t_out[(int64_t)b * t_stride] = (float)sT[b] * (1.0f / 16777216.0f);
+    if (seg_off) seg_off[b] = sSeg[b];
+    if (t24_out) t24_out[b] = sT[b];
+  }
+  if (tid == 0) {
+    if (seg_off) seg_off[B] = total;
+    if (meta) {
+      meta->n_rows = total;
+      meta->n_rows_pad = total_pad;
+    }
+  }
+  if (row_cap > 0) {
+    const int pad_end = min(total_pad, row_cap);
+    for (int r = total + tid; r < pad_end; r += kMaskThreads) {
+      if (row_tgt) row_tgt[r] = 0;
+      if (row_seq) row_seq[r] = B;
+    }
+  }
+}
+
+hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int B, int L, int n_t,
+                               int j, int t_mode, uint64_t seed, uint32_t seq_base, int32_t* idx,
+                               int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
+                               SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
+                               float* t_out, int t_stride, int row_cap, int V, hipStream_t s) {
+  k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, t_mode,
+                                            (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
+                                            seq_base, idx, row_tgt, row_seq, seg_off, t24, meta,
+                                            n_masked_out, nm_stride, t_out, t_stride, row_cap, V);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Gather: Hc[r, :] = hidden[idx[r], :] and HcT[:, r] for r < N; zeros for
+// N <= r < N_pad.  64x64 tiles staged in LDS for the transposed copy.
+__global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hidden,
+                                                const int32_t* __restrict__ idx,
+                                                const SampleMeta* __restrict__ meta,
+                                                uint16_t* __restrict__ Hc,
+                                                uint16_t* __restrict__ HcT, int d, int64_t ldt) {
+  __shared__ uint16_t tile[64][72];
+  const int r0 = blockIdx.x * 64;
+  if (r0 >= meta->n_rows_pad) return;
+  const int N = meta->n_rows;
+  const int c0 = blockIdx.y * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int q = tid + it * 256;
+    const int row = q >> 3, ch = q & 7;
+    const int r = r0 + row;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (r < N) v = *reinterpret_cast<const uint4*>(hidden + (int64_t)idx[r] * d + c0 + ch * 8);
+    *reinterpret_cast<uint4*>(Hc + (int64_t)r * d + c0 + ch * 8) = v;
+    *reinterpret_cast<uint4*>(&tile[row][ch * 8]) = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int q = tid + it * 256;
+    const int c = q >> 3, rch = q & 7;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = (uint32_t)tile[rch * 8 + 2 * e][c] | ((uint32_t)tile[rch * 8 + 2 * e + 1][c] << 16);
+    *reinterpret_cast<uint4*>(HcT + (int64_t)(c0 + c) * ldt + r0 + rch * 8) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s) {
+  dim3 grid((unsigned)(ws.NP / 64), (unsigned)(d / 64));
+  k_gather<<<grid, 256, 0, s>>>(hidden, ws.idx, ws.meta, ws.Hc, ws.HcT, d, ws.NP);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// W_head [d, V] -> WT [V, d], 64x64 tiles through LDS.
+__global__ __launch_bounds__(256) void k_transpose_w(const uint16_t* __restrict__ W,
+                                                     uint16_t* __restrict__ WT, int d, int V) {
+  __shared__ uint16_t tile[64][72];
+  const int v0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int q = tid + it * 256;
+    const int kr = q >> 3, ch = q & 7;
+    *reinterpret_cast<uint4*>(&tile[kr][ch * 8]) =
+        *reinterpret_cast<const uint4*>(W + (int64_t)(k0 + kr) * V + v0 + ch * 8);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int q = tid + it * 256;
+    const int v = q >> 3, kch = q & 7;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = (uint32_t)tile[kch * 8 + 2 * e][v] | ((uint32_t)tile[kch * 8 + 2 * e + 1][v] << 16);
+    *reinterpret_cast<uint4*>(WT + (int64_t)(v0 + v) * d + k0 + kch * 8) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+hipError_t launch_transpose_w(const uint16_t* W, uint16_t* WT, int d, int V, hipStream_t s) {
+  dim3 grid((unsigned)(V / 64), (unsigned)(d / 64));
+  k_transpose_w<<<grid, 256, 0, s>>>(W, WT, d, V);
+  return hipGetLastError();
+}
+
+}  // namespace bgpo

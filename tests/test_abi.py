@@ -1,0 +1,110 @@
+"""The C-ABI library loads, exports every declared symbol and validates its
+arguments on the host before any HIP call (runs without a GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2510_11683_amd", "libbgpo.so")
+
+
+def _declared():
+    names = set()
+    for h in ("bgpo.h", "bgpo_testing.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names |= set(re.findall(r"\b(bgpo_\w+)\s*\(", src))
+    return names
+
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libbgpo.so not built")
+
+
+def test_exports_every_declared_symbol():
+    declared = _declared()
+    assert {"bgpo_elbo_fwd", "bgpo_elbo_bwd_accumulate", "bgpo_workspace_size",
+            "bgpo_sample_masks", "bgpo_status_string", "bgpo_version"} <= declared
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (bgpo_\w+)", out))
+    missing = declared - exported
+    assert not missing, missing
+    lib = ctypes.CDLL(LIB)
+    for n in declared:
+        assert hasattr(lib, n)
+
+
+@pytest.fixture(scope="module")
+def b():
+    from paper_2510_11683_amd import bgpo
+    return bgpo
+
+
+def _prob(b, **kw):
+    base = dict(B=8, L=512, d=4096, V=126464, n_t=64, j_begin=0, j_count=None, seed=1)
+    base.update(kw)
+    return b.Problem(**base)
+
+
+def test_status_strings(b):
+    for s in (0, -1, -2, -3, -4):
+        assert b._lib.bgpo_status_string(s)
+    assert b"unknown" in b._lib.bgpo_status_string(-99)
+
+
+def test_workspace_independent_of_n_t(b):
+    sizes = {b.bgpo_workspace_size(_prob(b, n_t=n)) for n in (1, 4, 16, 64, 1000)}
+    assert len(sizes) == 1
+    assert b.bgpo_workspace_size(_prob(b, B=16)) > b.bgpo_workspace_size(_prob(b))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=4000), -4), (dict(V=126000), -4), (dict(d=32), -4), (dict(B=5000, L=1), -4),
+    (dict(B=2048, L=1024), -4), (dict(B=0), -1), (dict(L=0), -1), (dict(n_t=0), -1),
+    (dict(j_begin=-1), -1), (dict(j_begin=60, j_count=5), -1), (dict(t_mode=2), -1),
+])
+def test_problem_validation(b, kw, status):
+    with pytest.raises(b.BgpoError) as e:
+        b.bgpo_workspace_size(_prob(b, **kw))
+    assert e.value.status == status
+
+
+def test_null_pointers_and_workspace_rejected_before_hip(b):
+    p = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
+    lib = b._lib
+    fake = ctypes.c_void_p(0x1000)        # never dereferenced: validation fails first
+    nbytes = ctypes.c_size_t(0)
+    assert lib.bgpo_workspace_size(ctypes.byref(p), ctypes.byref(nbytes)) == 0
+    # missing hidden
+    assert lib.bgpo_elbo_fwd(ctypes.byref(p), None, fake, fake, fake, fake, fake, None,
+                             fake, nbytes.value, None, None) == -1
+    # workspace too small / misaligned / missing
+    ws_small = ctypes.c_void_p(0x100000)
+    assert lib.bgpo_elbo_fwd(ctypes.byref(p), fake, fake, fake, fake, fake, fake, None,
+                             ws_small, nbytes.value - 1, None, None) == -2
+    assert lib.bgpo_elbo_fwd(ctypes.byref(p), fake, fake, fake, fake, fake, fake, None,
+                             ctypes.c_void_p(0x100010), nbytes.value, None, None) == -2
+    assert lib.bgpo_elbo_fwd(ctypes.byref(p), fake, fake, fake, fake, fake, fake, None,
+                             None, nbytes.value, None, None) == -2
+    # backward: missing dW, non-finite loss scale
+    assert lib.bgpo_elbo_bwd_accumulate(ctypes.byref(p), fake, fake, fake, fake, fake, None, 0.125,
+                                        fake, None, fake, fake, fake, fake, None, None,
+                                        ws_small, nbytes.value, None, None) == -1
+    assert lib.bgpo_elbo_bwd_accumulate(ctypes.byref(p), fake, fake, fake, fake, fake, None,
+                                        float("nan"), fake, fake, fake, fake, fake, fake, None,
+                                        None, ws_small, nbytes.value, None, None) == -1
+    # sample masks: j out of range
+    assert lib.bgpo_sample_masks(ctypes.byref(p), fake, 4, fake, fake, None, None) == -1
+    assert lib.bgpo_sample_masks(ctypes.byref(p), fake, -1, fake, fake, None, None) == -1
+    # bad reserved field
+    q = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
+    q.reserved = 1
+    assert lib.bgpo_workspace_size(ctypes.byref(q), ctypes.byref(nbytes)) == -1
+
+
+def test_problem_struct_layout(b):
+    # matches the C struct: 8 int32, uint64, 2 uint32 = 48 bytes
+    assert ctypes.sizeof(b._Problem) == 48
+    assert b._Problem.seed.offset == 32

@@ -1,0 +1,207 @@
+"""Parity of the HIP path (through the C ABI) with the float64 oracle.
+
+Bars: masks, compacted indices, counts and timesteps bit-exact; l_{b,j}
+within 1e-3 relative; accumulated dX and dW within 2e-2 relative max-norm
+(bf16 inputs, fp32 accumulation, bf16 dZ).
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import elbo
+from gpu_util import Runner, lib, problem, rel_maxnorm
+
+pytestmark = pytest.mark.gpu
+
+ELL_RTOL = 1e-3
+GRAD_RTOL = 2e-2
+
+# several 256-wide tiles in every GEMM dimension with ragged tails: rows
+# (masked positions), vocabulary (4288 = 16.75 tiles) and hidden size (576)
+MID = workloads.Workload("mid_B4_L200_d576_V4288_nt3", B=4, L=200, d=576, V=4288, n_t=3,
+                         lengths=(120, 200), group=4, data_seed=2001, philox_seed=0xB6B10001)
+
+
+def _oracle_problem(w, j_begin=0, j_count=None):
+    return elbo.Problem(w.B, w.L, w.d, w.V, w.n_t, j_begin=j_begin, j_count=j_count,
+                        seed=w.philox_seed, seq_id_base=w.seq_id_base, t_mode=w.t_mode)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lib()
+
+
+# ---------------------------------------------------------------- GEMM core
+
+@pytest.mark.parametrize("M,N,K", [(300, 200, 192), (512, 768, 1024), (257, 1000, 64)])
+def test_gemm_core_matches_fp32_reference(M, N, K):
+    g = torch.Generator().manual_seed(M * 7 + N)
+    A = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    Bm = torch.randn(N, K, generator=g).to(torch.bfloat16)
+    ref = A.double() @ Bm.double().T                      # exact products of bf16 values
+    C = torch.empty(M, N, dtype=torch.float32, device="cuda")
+    lib().bgpo_test_gemm_nt(A.cuda(), Bm.cuda(), C)
+    torch.cuda.synchronize()
+    err = (C.cpu().double() - ref).abs().max().item()
+    assert err <= 1e-5 * (K ** 0.5) * ref.abs().max().item() + 1e-5, err
+
+
+# ---------------------------------------------------------------- masks
+
+@pytest.mark.parametrize("w", workloads.CONFIGS + (MID,), ids=lambda w: w.name)
+def test_masks_bit_exact(w):
+    x = workloads.generate(w, with_weights=False, with_hidden=False)
+    resp = torch.from_numpy(x["resp_mask"]).cuda()
+    p = problem(w)
+    op = _oracle_problem(w)
+    idx = torch.full((w.B * w.L,), -7, dtype=torch.int32, device="cuda")
+    nm = torch.zeros(w.B, dtype=torch.int32, device="cuda")
+    t = torch.zeros(w.B, dtype=torch.float32, device="cuda")
+    for j in sorted({0, 1, w.n_t - 1}):
+        idx.fill_(-7)
+        lib().bgpo_sample_masks(p, resp, j, idx, nm, t)
+        T, tt, m, oidx = elbo.sample_masks(op, x["resp_mask"], j)
+        torch.cuda.synchronize()
+        n = int(nm.sum())
+        assert n == oidx.size
+        assert np.array_equal(idx[:n].cpu().numpy(), oidx)
+        assert np.array_equal(nm.cpu().numpy(), m.sum(axis=1))
+        assert np.array_equal(t.cpu().numpy().astype(np.float64), tt)   # exact multiples of 2^-24
+        assert (idx[n:].cpu().numpy() == -7).all()                       # untouched tail
+
+
+# ---------------------------------------------------------------- ELBO head
+
+def _check_against_oracle(w, out, ref, js):
+    for j in js:
+        assert np.array_equal(out["nm"][:, j], ref.n_masked[:, j])
+        assert np.array_equal(out["t"][:, j].astype(np.float64), ref.t[:, j])
+        np.testing.assert_allclose(out["ell"][:, j], ref.ell[:, j], rtol=ELL_RTOL, atol=0)
+        np.testing.assert_allclose(out["g"][:, j], ref.g[:, j], rtol=ELL_RTOL, atol=1e-12)
+    assert abs(out["loss"] - ref.loss) <= ELL_RTOL * max(abs(ref.loss), 1e-12)
+    assert rel_maxnorm(out["dX"], ref.dX) <= GRAD_RTOL
+    assert rel_maxnorm(out["dW"], ref.dW) <= GRAD_RTOL
+    assert out["flags"] == 0
+
+
+def test_tiny_parity_fwd_and_bwd():
+    w = workloads.TINY
+    x = workloads.generate(w)
+    r = Runner(w, x)
+    ref = elbo.elbo_literal(_oracle_problem(w), x["hidden"], x["W"], x["targets"],
+                            x["resp_mask"], x["adv"])
+    r.fwd()
+    f = r.out()
+    np.testing.assert_allclose(f["ell"], ref.ell, rtol=ELL_RTOL, atol=0)
+    assert np.array_equal(f["nm"], ref.n_masked)
+    r.bwd()
+    _check_against_oracle(w, r.out(), ref, range(w.n_t))
+
+
+def test_mid_parity_off_policy_both_branches():
+    w = MID
+    x = workloads.generate(w)
+    assert (x["adv"] > 0).any() and (x["adv"] < 0).any()
+    op = _oracle_problem(w)
+    ell_old = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                                backward=False).ell
+    ell_old = ell_old + np.random.default_rng(5).normal(0, 2.0, ell_old.shape)
+    ref = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                            ell_old=ell_old, loss_scale=0.25)
+    r = Runner(w, x)
+    r.bwd(ell_old=ell_old, loss_scale=0.25)
+    _check_against_oracle(w, r.out(), ref, range(w.n_t))
+
+
+def test_on_policy_d_is_exactly_zero():
+    """ell from the forward entry point fed back as ell_old gives d == 0 bit-exactly,
+    so g = A / n_t exactly (the equivalence case)."""
+    w = MID
+    x = workloads.generate(w)
+    r = Runner(w, x)
+    r.fwd()
+    ell_fwd = r.out()["ell"].copy()
+    r.bwd(ell_old=ell_fwd)
+    o = r.out()
+    assert np.array_equal(o["ell"], ell_fwd)
+    adv = x["adv"].astype(np.float64)
+    expect = np.repeat((adv / w.n_t)[:, None], w.n_t, axis=1)
+    assert np.array_equal(o["g"], expect)
+
+
+def test_linearity_and_determinism():
+    w = MID.replace(n_t=4)
+    x = workloads.generate(w)
+    r = Runner(w, x)
+    r.bwd()
+    full = r.out()
+    r.zero_grads()
+    r.bwd()
+    again = r.out()
+    assert np.array_equal(full["dX"], again["dX"]) and np.array_equal(full["dW"], again["dW"])
+    assert np.array_equal(full["ell"], again["ell"]) and full["loss"] == again["loss"]
+    r.zero_grads()
+    for jb, jc in ((0, 1), (1, 2), (3, 1)):
+        r.bwd(j_begin=jb, j_count=jc)
+    split = r.out()
+    assert np.array_equal(split["ell"], full["ell"])
+    assert abs(split["loss"] - full["loss"]) <= 1e-12 * abs(full["loss"])
+    assert rel_maxnorm(split["dX"], full["dX"]) <= 1e-5
+    assert rel_maxnorm(split["dW"], full["dW"]) <= 1e-5
+
+
+def test_empty_range_and_empty_masks():
+    w = MID
+    x = workloads.generate(w)
+    r = Runner(w, x)
+    r.bwd(j_begin=1, j_count=0)
+    o = r.out()
+    assert not o["dX"].any() and not o["dW"].any() and o["loss"] == 0.0
+    # a response-mask of all zeros: nothing is ever masked
+    x0 = dict(x)
+    x0["resp_mask"] = np.zeros_like(x["resp_mask"])
+    r0 = Runner(w, x0)
+    r0.bwd()
+    o0 = r0.out()
+    assert not o0["nm"].any() and not o0["ell"].any()
+    assert not o0["dX"].any() and not o0["dW"].any()
+    expect_g = np.where(x["adv"] >= 0, x["adv"].astype(np.float64), np.exp(0.0) * x["adv"]) / w.n_t
+    np.testing.assert_allclose(o0["g"], np.repeat(expect_g[:, None], w.n_t, 1), rtol=1e-15)
+
+
+def test_nonfinite_flag_raised_not_clamped():
+    w = MID
+    x = workloads.generate(w)
+    x = dict(x)
+    x["adv"] = -np.abs(x["adv"]) - 0.1            # Jensen branch everywhere
+    r = Runner(w, x)
+    ell_old = np.full((w.B, w.n_t), -1e6)         # d = l - l_old ~ +1e6 -> e^d overflows
+    r.bwd(ell_old=ell_old, j_count=1)
+    o = r.out()
+    assert o["flags"] & lib().BGPO_FLAG_NONFINITE
+    assert np.isinf(o["g"][:, 0]).all()
+
+
+def test_memory_constant_in_n_t():
+    """Peak device memory of a full bwd call is the same for n_t = 1, 4, 16 (the
+    [B, n_t] outputs round to the same 512-byte allocation blocks here)."""
+    w = MID
+    x = workloads.generate(w)
+    peaks = []
+    for nt in (1, 4, 16):
+        wn = w.replace(n_t=nt)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        free0 = torch.cuda.mem_get_info()[0]
+        r = Runner(wn, x)
+        r.bwd()
+        torch.cuda.synchronize()
+        peaks.append((torch.cuda.max_memory_allocated(), free0 - torch.cuda.mem_get_info()[0]))
+        del r
+    assert len({p[0] for p in peaks}) == 1, peaks
+    assert len({p[1] for p in peaks}) == 1, peaks

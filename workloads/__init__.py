@@ -96,8 +96,25 @@ def _zipf_tokens(rng: np.random.Generator, V: int, n: int, exponent: float = 1.1
     return perm[r].astype(np.int32)
 
 
-def generate(w: Workload, *, with_weights: bool = True) -> dict:
-    """Draw every input of workload ``w`` from numpy PCG64(w.data_seed).
+_CHUNK_ROWS = 1024
+
+
+def _chunked(seed_seq, n_rows, fill, rows=_CHUNK_ROWS):
+    """Fill rows [0, n_rows) in fixed chunks of ``rows``, chunk c drawing from
+    its own stream spawned from ``seed_seq``; threads only change the speed."""
+    import concurrent.futures as cf
+    import os
+    starts = list(range(0, n_rows, rows))
+    seqs = seed_seq.spawn(len(starts))
+    jobs = [(c, np.random.Generator(np.random.PCG64(q))) for c, q in zip(starts, seqs)]
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    with cf.ThreadPoolExecutor(workers) as ex:
+        list(ex.map(lambda a: fill(*a), jobs))
+
+
+def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True) -> dict:
+    """Draw every input of workload ``w`` from numpy PCG64 streams spawned from
+    ``w.data_seed`` (one stream per input, so W or hidden can be skipped).
 
     Returns a dict of numpy arrays:
       hidden    uint16 [B, L, d]  bf16 bits, row-major
@@ -107,44 +124,50 @@ def generate(w: Workload, *, with_weights: bool = True) -> dict:
       adv       float32 [B]       per-response advantage
     plus ``lengths`` (int32 [B]).
     """
-    rng = np.random.Generator(np.random.PCG64(w.data_seed))
+    # independent streams per input, so that any subset can be drawn alone
+    ss = np.random.SeedSequence(w.data_seed).spawn(5)
+    r_h, r_w, r_y, r_len, r_adv = (np.random.Generator(np.random.PCG64(s)) for s in ss)
     B, L, d, V = w.B, w.L, w.d, w.V
 
-    h = rng.standard_normal((B, L, d), dtype=np.float32)
-    if w.hidden == "rmsnorm":
-        rms = np.sqrt(np.mean(h.astype(np.float64) ** 2, axis=-1, keepdims=True) + 1e-6)
-        h = (h / rms).astype(np.float32)
-    hidden = f32_to_bf16_bits(h).reshape(B, L, d)
-    del h
+    hidden = None
+    if with_hidden:
+        hidden = np.empty((B * L, d), dtype=np.uint16)
+
+        def fill_h(c, rng):
+            h = rng.standard_normal((min(B * L, c + _CHUNK_ROWS) - c, d), dtype=np.float32)
+            if w.hidden == "rmsnorm":
+                rms = np.sqrt(np.mean(h.astype(np.float64) ** 2, axis=-1, keepdims=True) + 1e-6)
+                h = (h / rms).astype(np.float32)
+            hidden[c:c + h.shape[0]] = f32_to_bf16_bits(h).reshape(h.shape)
+
+        _chunked(ss[0], B * L, fill_h)
+        hidden = hidden.reshape(B, L, d)
 
     W = None
     if with_weights:
         W = np.empty((d, V), dtype=np.uint16)
-        rows_per_chunk = max(1, (1 << 24) // V)
-        for r0 in range(0, d, rows_per_chunk):
-            r1 = min(d, r0 + rows_per_chunk)
-            chunk = rng.standard_normal((r1 - r0, V), dtype=np.float32) * np.float32(w.w_std)
-            W[r0:r1] = f32_to_bf16_bits(chunk).reshape(r1 - r0, V)
-    else:
-        # keep the stream position identical to the with-weights draw
-        rows_per_chunk = max(1, (1 << 24) // V)
-        for r0 in range(0, d, rows_per_chunk):
-            r1 = min(d, r0 + rows_per_chunk)
-            rng.standard_normal((r1 - r0, V), dtype=np.float32)
+        rows = max(1, (_CHUNK_ROWS * 512) // V)
+
+        def fill_w(c, rng):
+            n = min(d, c + rows) - c
+            chunk = rng.standard_normal((n, V), dtype=np.float32) * np.float32(w.w_std)
+            W[c:c + n] = f32_to_bf16_bits(chunk).reshape(n, V)
+
+        _chunked(ss[1], d, fill_w, rows)
 
     if w.targets == "uniform":
-        targets = rng.integers(0, V, size=(B, L), dtype=np.int64).astype(np.int32)
+        targets = r_y.integers(0, V, size=(B, L), dtype=np.int64).astype(np.int32)
     else:
-        targets = _zipf_tokens(rng, V, B * L).reshape(B, L)
+        targets = _zipf_tokens(r_y, V, B * L).reshape(B, L)
 
     if w.lengths is None:
         lengths = np.full(B, L, dtype=np.int32)
     else:
         lo, hi = w.lengths
-        lengths = rng.integers(lo, hi + 1, size=B, dtype=np.int64).astype(np.int32)
+        lengths = r_len.integers(lo, hi + 1, size=B, dtype=np.int64).astype(np.int32)
     resp_mask = (np.arange(L)[None, :] < lengths[:, None]).astype(np.uint8)
 
-    r = rng.standard_normal(B)
+    r = r_adv.standard_normal(B)
     if w.adv == "group":
         G = w.group
         adv = np.empty(B, dtype=np.float64)
