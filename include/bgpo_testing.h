@@ -18,6 +18,20 @@ extern "C" {
 int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
                       int32_t K, void* stream);
 
+/* Tile-configuration variants of the same GEMM (fp32 store), for tuning:
+ * variant 0: 256x256 tile, K slab 32, 4-stage LDS ring (the production one)
+ *         1: 5 stages, 2: K slab 64 in 2 stages,
+ *         3: 256x128 tile, 3 stages, two workgroups per compute unit
+ *         4: 128x256 tile, 3 stages, two workgroups per compute unit
+ *         5: 256x256 tile, K slab 64, 2 stages, 8 waves of 128x64
+ *         6: as 5 with 8 waves of 64x128
+ *         7: as 2 with the 256-byte LDS swizzle; 8: as 5 with that swizzle
+ * flags bit 0: M tiles consecutive in the tile walk (else N tiles);
+ *       bit 1: plain workgroup order (no XCD grouping).
+ * Same shape rules and return codes as bgpo_test_gemm_nt. */
+int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
+                           int32_t K, int32_t variant, int32_t flags, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

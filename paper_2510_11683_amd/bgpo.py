@@ -61,8 +61,9 @@ def _load():
     lib.bgpo_elbo_bwd_accumulate.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, ctypes.c_double,
                                              vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, P(Timing)]
     lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
+    lib.bgpo_test_gemm_variant.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, vp]
     for f in ("bgpo_workspace_size", "bgpo_sample_masks", "bgpo_elbo_fwd",
-              "bgpo_elbo_bwd_accumulate", "bgpo_test_gemm_nt"):
+              "bgpo_elbo_bwd_accumulate", "bgpo_test_gemm_nt", "bgpo_test_gemm_variant"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -193,6 +194,16 @@ def bgpo_test_gemm_nt(A, B, C, stream=None):
     _check(_lib.bgpo_test_gemm_nt(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
                                   _ptr(C, "C", (torch.float32,), (M, N)), M, N, K, _stream(stream)),
            "bgpo_test_gemm_nt")
+
+
+def bgpo_test_gemm_variant(A, B, C, variant: int, flags: int = 0, stream=None):
+    """Test hook: tile-configuration variants of the GEMM core (see bgpo_testing.h)."""
+    M, K = A.shape
+    N = B.shape[0]
+    _check(_lib.bgpo_test_gemm_variant(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
+                                       _ptr(C, "C", (torch.float32,), (M, N)), M, N, K,
+                                       int(variant), int(flags), _stream(stream)),
+           "bgpo_test_gemm_variant")
 
 
 def device_inputs(x: dict, device="cuda") -> dict:

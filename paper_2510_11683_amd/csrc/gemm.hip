@@ -39,6 +39,7 @@ struct GemmParams {
   int n_split;               // K split count (dX)
   int64_t k_split;           // K per split (multiple of BK)
   int m_fastest;             // tile order: 1 = M tiles consecutive, 0 = N tiles consecutive
+  int plain_order;           // 1 = no XCD grouping of consecutive tiles (experiments)
   const SampleMeta* meta;
   // epilogue operands
   float* out;                // F32 store / accumulate target
@@ -56,7 +57,7 @@ struct GemmParams {
   int64_t ldzt;
 };
 
-template <int BM, int BN, int BK, int WM, int WN>
+template <int BM, int BN, int BK, int WM, int WN, int SWZ = 0>
 struct Cfg {
   static constexpr int NWM = BM / WM, NWN = BN / WN;
   static constexpr int NWAVES = NWM * NWN;
@@ -67,7 +68,13 @@ struct Cfg {
   static constexpr int ROWS_PER_128B = 8 / KCH;
   static_assert(BM * KCH % NT == 0 && BN * KCH % NT == 0, "load split");
   static_assert(KCH == 4 || KCH == 8, "BK must be 32 or 64");
-  __device__ static __forceinline__ int swz(int row) { return (row / ROWS_PER_128B) % KCH; }
+  // 16-byte chunk c of LDS row r is stored at chunk c ^ swz(r).  SWZ 0 makes 8
+  // consecutive rows hit 8 distinct 16-byte slots of a 128-byte bank line;
+  // SWZ 1 spreads 16 consecutive rows over 256 bytes (pairs of rows share a
+  // key, and consecutive rows already alternate 128-byte halves).
+  __device__ static __forceinline__ int swz(int row) {
+    return SWZ == 0 ? (row / ROWS_PER_128B) % KCH : ((row >> 1) / ROWS_PER_128B) % KCH;
+  }
 };
 
 // fp32 store (dX partials) or read-modify-write accumulate (dW), one 32-row
@@ -104,7 +111,37 @@ __device__ __forceinline__ void epi_f32(const f32x16 (&acc)[TM][TN], float* outb
 }
 
 // Issue one K slab of both operand tiles into LDS stage `stage`.
-template <int BM, int BN, int KCH, int A_INS, int B_INS>
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding: vmcnt
+// in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// MFMA operand fragments of K sub-step ks of LDS stage `stage`: lane l holds the
+// 8 consecutive K values 8 (2 ks + l / 32) .. +7 of row l % 32 of each 32-row
+// band of the wave's A and B sub-tiles.
+template <int BM, int BN, int KCH, int TM, int TN, int WM, int WN, class C>
+__device__ __forceinline__ void read_frags(bf16x8 (&fa)[TM], bf16x8 (&fb)[TN], const uint4* As,
+                                           const uint4* Bs, int stage, int ks, int wm, int wn,
+                                           int lane) {
+  const int ch = ks * 2 + (lane >> 5);
+  const uint4* Ac = As + stage * BM * KCH;
+  const uint4* Bc = Bs + stage * BN * KCH;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int row = wm * WM + i * 32 + (lane & 31);
+    fa[i] = __builtin_bit_cast(bf16x8, Ac[row * KCH + (ch ^ C::swz(row))]);
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int row = wn * WN + j * 32 + (lane & 31);
+    fb[j] = __builtin_bit_cast(bf16x8, Bc[row * KCH + (ch ^ C::swz(row))]);
+  }
+}
+
+template <int BM, int BN, int KCH, int A_INS, int B_INS, int STAGES>
 __device__ __forceinline__ void issue_slab_loads(uint4* As, uint4* Bs, int stage, int wave,
                                                  __amdgpu_buffer_rsrc_t a_rsrc,
                                                  __amdgpu_buffer_rsrc_t b_rsrc,
@@ -126,16 +163,36 @@ __device__ __forceinline__ void issue_slab_loads(uint4* As, uint4* Bs, int stage
 #endif
 }
 
-template <int EPI, int BM, int BN, int BK, int WM, int WN>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, 1) void k_gemm(GemmParams p) {
-#if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature
-  using C = Cfg<BM, BN, BK, WM, WN>;
-  constexpr int NT = C::NT, TM = C::TM, TN = C::TN, KCH = C::KCH;
-  __shared__ uint4 smem[2 * (BM + BN) * KCH];
-  uint4* As = smem;                      // [2][BM][KCH]
-  uint4* Bs = smem + 2 * BM * KCH;       // [2][BN][KCH]
+// Instruction-order template for one K sub-step: MF MFMAs with ND LDS
+// fragment reads and NV slab loads placed between them (one scheduling group
+// per instruction kind and position; requires ND <= MF).
+template <int I, int MF, int NV, int ND>
+__device__ __forceinline__ void sched_pattern() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  if constexpr (I < MF) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // MFMA
+    // fragment reads first (one per MFMA slot, so the next sub-step's operands
+    // land well before it starts), slab loads spread over the whole step
+    constexpr int v = (I + 1) * NV / MF - I * NV / MF;
+    constexpr int d = I < ND ? 1 : 0;
+    if constexpr (d > 0) __builtin_amdgcn_sched_group_barrier(0x100, d, 0);   // DS read
+    if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);   // VMEM read
+    sched_pattern<I + 1, MF, NV, ND>();
+  }
+#endif
+}
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+template <int EPI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC = 1, int SWZ = 0>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature
+  using C = Cfg<BM, BN, BK, WM, WN, SWZ>;
+  constexpr int NT = C::NT, TM = C::TM, TN = C::TN, KCH = C::KCH, KS = BK / 16;
+  __shared__ uint4 smem[STAGES * (BM + BN) * KCH];
+  uint4* As = smem;                           // [STAGES][BM][KCH]
+  uint4* Bs = smem + STAGES * BM * KCH;       // [STAGES][BN][KCH]
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, kept in an SGPR
   const int wm = wave / C::NWN, wn = wave % C::NWN;
 
   int M = p.M, N = p.N, K = p.K, n_valid = p.N;
@@ -147,7 +204,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, 1) void k_gemm(GemmPara
   const int64_t total = (int64_t)tilesM * tilesN * p.n_split;
   const int G = gridDim.x;
   const int w = blockIdx.x;
-  const int xcd_slot = (G % 8 == 0) ? (w % 8) * (G / 8) + w / 8 : w;
+  const int xcd_slot = (G % 8 == 0 && !p.plain_order) ? (w % 8) * (G / 8) + w / 8 : w;
 
   for (int64_t base = 0; base < total; base += G) {
     const int64_t t = base + xcd_slot;
@@ -205,40 +262,80 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, 1) void k_gemm(GemmPara
       b_voff[q] = (uint32_t)(rr * p.ldb * 2 + c * 16);
     }
     if (nk > 0) {
-      issue_slab_loads<BM, BN, KCH, A_INS, B_INS>(As, Bs, 0, wave, a_rsrc, b_rsrc, a_voff, b_voff, (int)(kb * 2));
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
+      // S-stage ring of K slabs: slab q lives in stage q % S.  The prologue
+      // fills all S stages; at the barrier that ends slab c every wave has
+      // read all of slab c's stage, so slab c + S is loaded into it right
+      // away and has S - 1 slabs of MFMA time to land.  Slabs past the end of
+      // this tile's K range re-load its last slab into a stage no later slab
+      // uses, so every wave always has the same number of load groups in
+      // flight and the vmcnt waits are compile-time constants.
+      constexpr int NINS = A_INS + B_INS;
+      constexpr int NFRAG = TM + TN;
+      auto issue = [&](int q) {
+        const int qc = min(q, nk - 1);
+        issue_slab_loads<BM, BN, KCH, A_INS, B_INS, STAGES>(As, Bs, q % STAGES, wave, a_rsrc,
+                                                            b_rsrc, a_voff, b_voff,
+                                                            (int)((kb + (int64_t)qc * BK) * 2));
+      };
+#pragma unroll
+      for (int q = 0; q < STAGES; ++q) issue(q);
+      wait_vmcnt<NINS * (STAGES - 1)>();
+      __builtin_amdgcn_s_barrier();
 
-      for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk)
-          issue_slab_loads<BM, BN, KCH, A_INS, B_INS>(As, Bs, cur ^ 1, wave, a_rsrc, b_rsrc, a_voff,
-                                                      b_voff, (int)((kb + (int64_t)(kt + 1) * BK) * 2));
-        const uint4* Ac = As + cur * BM * KCH;
-        const uint4* Bc = Bs + cur * BN * KCH;
+      bf16x8 fa[2][TM], fb[2][TN];
+      auto mfma_step = [&](int h) {
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-          const int ch = ks * 2 + (lane >> 5);
-          bf16x8 af[TM], bfr[TN];
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-          for (int i = 0; i < TM; ++i) {
-            const int row = wm * WM + i * 32 + (lane & 31);
-            af[i] = __builtin_bit_cast(bf16x8, Ac[row * KCH + (ch ^ C::swz(row))]);
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[h][i], fb[h][j], acc[i][j], 0, 0, 0);
+      };
+      read_frags<BM, BN, KCH, TM, TN, WM, WN, C>(fa[0], fb[0], As, Bs, 0, 0, wm, wn, lane);
+      for (int kt = 0; kt + 1 < nk; ++kt) {
+        const int cur = kt % STAGES;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          if (ks + 1 < KS) {
+            read_frags<BM, BN, KCH, TM, TN, WM, WN, C>(fa[(ks + 1) & 1], fb[(ks + 1) & 1], As, Bs,
+                                                        cur, ks + 1, wm, wn, lane);
+            mfma_step(ks & 1);
+            sched_pattern<0, TM * TN, 0, NFRAG>();
+          } else {
+            // slab kt+1 landed (own loads) and, after the barrier, every wave
+            // has finished reading stage `cur`: refill it with slab kt+S while
+            // the last MFMAs of slab kt run, and start reading slab kt+1.
+            wait_vmcnt<NINS * (STAGES - 2)>();
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            issue(kt + STAGES);
+            read_frags<BM, BN, KCH, TM, TN, WM, WN, C>(fa[(ks + 1) & 1], fb[(ks + 1) & 1], As, Bs,
+                                                        (kt + 1) % STAGES, 0, wm, wn, lane);
+            mfma_step(ks & 1);
+            sched_pattern<0, TM * TN, NINS, NFRAG>();
           }
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int row = wn * WN + j * 32 + (lane & 31);
-            bfr[j] = __builtin_bit_cast(bf16x8, Bc[row * KCH + (ch ^ C::swz(row))]);
-          }
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
       }
+      // the last slab
+      {
+        const int cur = (nk - 1) % STAGES;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          if (ks + 1 < KS) {
+            read_frags<BM, BN, KCH, TM, TN, WM, WN, C>(fa[(ks + 1) & 1], fb[(ks + 1) & 1], As, Bs,
+                                                        cur, ks + 1, wm, wn, lane);
+            mfma_step(ks & 1);
+            sched_pattern<0, TM * TN, 0, NFRAG>();
+          } else {
+            mfma_step(ks & 1);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      // drain the ring (outstanding re-loads) before the epilogue may reuse LDS
+      __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_s_barrier();
     }
 
     // ---------------- epilogues ----------------
@@ -354,9 +451,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, 1) void k_gemm(GemmPara
 }
 
 // Tile configuration of the production kernels: 256x256 block tile, K slab
-// 64, four waves each owning a 128x128 sub-tile (4x4 MFMA 32x32 tiles).
-#define BGPO_TILE 256, 256, 64, 128, 128
-constexpr int kGemmThreads = 256;
+// 64 in a 2-stage LDS ring, eight waves (two per SIMD, so one wave's memory
+// instructions issue while the other's MFMAs run), each owning a 128x64
+// sub-tile (4x2 MFMA 32x32 tiles), 256-byte LDS swizzle.
+#define BGPO_TILE 256, 256, 64, 128, 64, 2, 1, 1
+constexpr int kGemmThreads = 512;
 
 static GemmParams base_params() {
   GemmParams p;
@@ -435,5 +534,36 @@ extern "C" int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C,
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -3;
   k_gemm<EPI_F32_STORE, BGPO_TILE><<<gemm_grid(dev), kGemmThreads, 0, (hipStream_t)stream>>>(p);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// ---- test hook: tile-configuration variants of the GEMM core (fp32 store) ----
+extern "C" int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
+                                      int32_t N, int32_t K, int32_t variant, int32_t flags,
+                                      void* stream) {
+  using namespace bgpo;
+  if (!A || !B || !C || M <= 0 || N <= 0 || K <= 0 || K % 64) return -1;
+  GemmParams p = base_params();
+  p.A = A; p.lda = K; p.B = B; p.ldb = K;
+  p.M = M; p.N = N; p.K = K; p.k_split = K;
+  p.out = C; p.ldo = N;
+  p.m_fastest = flags & 1;
+  p.plain_order = (flags >> 1) & 1;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -3;
+  const int cus = gemm_grid(dev);
+  hipStream_t s = (hipStream_t)stream;
+  switch (variant) {
+    case 0: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 128, 4><<<cus, 256, 0, s>>>(p); break;
+    case 1: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 128, 5><<<cus, 256, 0, s>>>(p); break;
+    case 2: k_gemm<EPI_F32_STORE, 256, 256, 64, 128, 128, 2><<<cus, 256, 0, s>>>(p); break;
+    case 3: k_gemm<EPI_F32_STORE, 256, 128, 32, 128, 64, 3, 2><<<2 * cus, 256, 0, s>>>(p); break;
+    case 4: k_gemm<EPI_F32_STORE, 128, 256, 32, 64, 128, 3, 2><<<2 * cus, 256, 0, s>>>(p); break;
+    case 5: k_gemm<EPI_F32_STORE, 256, 256, 64, 128, 64, 2><<<cus, 512, 0, s>>>(p); break;
+    case 6: k_gemm<EPI_F32_STORE, 256, 256, 64, 64, 128, 2><<<cus, 512, 0, s>>>(p); break;
+    case 7: k_gemm<EPI_F32_STORE, 256, 256, 64, 128, 128, 2, 1, 1><<<cus, 256, 0, s>>>(p); break;
+    case 8: k_gemm<EPI_F32_STORE, 256, 256, 64, 128, 64, 2, 1, 1><<<cus, 512, 0, s>>>(p); break;
+    default: return -1;
+  }
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
