@@ -179,11 +179,22 @@ def elbo_collapsed(p: Problem, hidden_bits, W_bits, targets, resp_mask, adv,
     gradients to a subset, which is what makes full-size problems tractable:
     dX is returned as [len(dx_rows), d] and dW as [d, len(dw_cols)]."""
     H = bf16_to_f64(hidden_bits).reshape(p.B * p.L, p.d)
-    W = bf16_to_f64(W_bits).reshape(p.d, p.V)
     tg = targets.reshape(-1).astype(np.int64)
     resp = resp_mask.reshape(-1) != 0
-    pos = np.flatnonzero(resp)
 
+    # masks of every sample first: only positions masked in at least one sample
+    # of the range enter l or the gradients, so only those need a log-softmax
+    masks = {}
+    for j in p.js:
+        masks[j] = sample_masks(p, resp_mask, j)
+    used = np.zeros(p.B * p.L, dtype=bool)
+    for j in p.js:
+        used |= masks[j][2].reshape(-1)
+    if dx_rows is not None:
+        used[np.asarray(dx_rows, dtype=np.int64)] |= resp[np.asarray(dx_rows, dtype=np.int64)]
+    pos = np.flatnonzero(used)
+
+    W = bf16_to_f64(W_bits).reshape(p.d, p.V)
     lse = np.zeros(p.B * p.L)
     lp = np.zeros(p.B * p.L)
     for c0 in range(0, pos.size, row_chunk):
@@ -203,7 +214,7 @@ def elbo_collapsed(p: Problem, hidden_bits, W_bits, targets, resp_mask, adv,
     idx_all = {}
     lp2 = lp.reshape(p.B, p.L)
     for j in p.js:
-        T, t, m, idx = sample_masks(p, resp_mask, j)
+        T, t, m, idx = masks[j]
         idx_all[j] = idx
         for b in range(p.B):
             tt[b, j] = t[b]
@@ -217,7 +228,7 @@ def elbo_collapsed(p: Problem, hidden_bits, W_bits, targets, resp_mask, adv,
     dX = dW = None
     if backward:
         W = bf16_to_f64(W_bits).reshape(p.d, p.V)
-        xr = np.flatnonzero(resp) if dx_rows is None else np.asarray(dx_rows, dtype=np.int64)
+        xr = pos if dx_rows is None else np.asarray(dx_rows, dtype=np.int64)
         dX = np.zeros((xr.size, p.d))
         for c0 in range(0, xr.size, row_chunk):
             rows = xr[c0:c0 + row_chunk]
