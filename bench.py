@@ -33,6 +33,59 @@ DEFAULT = workloads.LLADA_L512_NT64.name
 GEMM_CLASSES = ("fwd", "recompute", "dx", "dw")
 
 
+class Telemetry:
+    """Samples the GPU engine clock (pp_dpm_sclk) and socket power (hwmon) from
+    sysfs in a background thread while the timed region runs."""
+
+    def __init__(self, period_s=0.02):
+        import glob
+        import threading
+        self.period = period_s
+        self.sclk_path = next(iter(sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))), None)
+        dev = os.path.dirname(self.sclk_path) if self.sclk_path else None
+        hw = sorted(glob.glob(os.path.join(dev, "hwmon", "hwmon*"))) if dev else []
+        self.power_path = os.path.join(hw[0], "power1_input") if hw else None
+        self.cap_path = os.path.join(hw[0], "power1_cap") if hw else None
+        self.sclk, self.power = [], []
+        self._stop = threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        try:
+            if self.sclk_path:
+                for line in open(self.sclk_path):
+                    if "*" in line:
+                        self.sclk.append(float(line.split(":")[1].strip().split("M")[0]))
+            if self.power_path and os.path.exists(self.power_path):
+                self.power.append(float(open(self.power_path).read()) / 1e6)
+        except (OSError, ValueError, IndexError):
+            pass
+
+    def _run(self):
+        while not self._stop.is_set():
+            self._read()
+            time.sleep(self.period)
+
+    def __enter__(self):
+        self._t.start()
+        return self
+
+    def __exit__(self, *a):
+        self._stop.set()
+        self._t.join()
+
+    def summary(self):
+        cap = None
+        try:
+            cap = float(open(self.cap_path).read()) / 1e6 if self.cap_path else None
+        except (OSError, ValueError):
+            pass
+        mean = lambda v: (sum(v) / len(v)) if v else None
+        return {"sclk_mhz_mean": mean(self.sclk), "sclk_mhz_min": min(self.sclk) if self.sclk else None,
+                "socket_power_w_mean": mean(self.power), "power_cap_w": cap,
+                "samples": len(self.sclk)}
+
+
 def cpu_baseline(w: workloads.Workload, x: dict, budget_s: float = 20.0) -> dict:
     """Time the float64 oracle's literal per-sample form (Algorithm 1 inner loop)
     on sample j = 0 for the first responses of the batch, adding responses until
@@ -118,13 +171,15 @@ def main():
     timing = bgpo.Timing()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
-        step(prob, timing)
-    end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    with Telemetry() as tel:
+        wall0 = time.perf_counter()
+        start.record()
+        for _ in range(args.steps):
+            step(prob, timing)
+        end.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+    telemetry = tel.summary()
     ms = start.elapsed_time(end) / args.steps
     peak_all = torch.cuda.max_memory_allocated()
     tokens = int(nm.sum().item())                        # masked tokens per step
@@ -175,6 +230,11 @@ def main():
         "mfma_frac_executed_8dV": exec_flops / (PEAK_BF16_TFLOPS * 1e12),
         "mfma_frac_useful_6dV": useful_flops / (PEAK_BF16_TFLOPS * 1e12),
         "kernels": per_kernel,
+        "telemetry": telemetry,
+        # the same MFMA fraction against the peak at the mean engine clock measured
+        "mfma_frac_executed_8dV_at_measured_clock": (
+            exec_flops / (PEAK_BF16_TFLOPS * 1e12 * telemetry["sclk_mhz_mean"] / 2400.0)
+            if telemetry.get("sclk_mhz_mean") else None),
         "wall_s_timed": wall,
         "peak_mem_bytes": {"n_t_1": peak_one, f"n_t_{nt}": peak_all,
                            "workspace": bgpo.bgpo_workspace_size(prob)},

@@ -26,6 +26,8 @@ int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
  *         5: 256x256 tile, K slab 64, 2 stages, 8 waves of 128x64
  *         6: as 5 with 8 waves of 64x128
  *         7: as 2 with the 256-byte LDS swizzle; 8: as 5 with that swizzle
+ *         9: 8 waves of 128x64, K slab 32, 4 stages; 10: as 9 with 5 stages
+ *         11: as 6 with the 256-byte swizzle
  * flags bit 0: M tiles consecutive in the tile walk (else N tiles);
  *       bit 1: plain workgroup order (no XCD grouping).
  * Same shape rules and return codes as bgpo_test_gemm_nt. */

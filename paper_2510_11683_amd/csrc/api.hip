@@ -20,6 +20,8 @@ namespace bgpo {
 
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+constexpr int64_t kMaxDwBatch = 4;
+
 size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   const int64_t P = (int64_t)dm.B * dm.L;
   const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
@@ -30,6 +32,11 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   int64_t n_split = std::min<int64_t>(16, std::max<int64_t>(1, (2048 + tiles_half - 1) / tiles_half));
   int64_t k_split = ((dm.V + n_split - 1) / n_split + 63) / 64 * 64;
   n_split = (dm.V + k_split - 1) / k_split;
+  // samples per dW GEMM: amortises the fp32 read-modify-write of dW over
+  // several samples while keeping H_c^T and dZ^T within about 16 GB
+  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2;
+  const int64_t dw_batch = std::max<int64_t>(1, std::min<int64_t>(kMaxDwBatch, (int64_t(16) << 30) / per_sample));
+  const int64_t KT = dw_batch * NP;
 
   size_t off = 0;
   char* b = static_cast<char*>(base);
@@ -52,16 +59,18 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   w.part_m = static_cast<float*>(take(nvt * NP * 4));
   w.part_s = static_cast<float*>(take(nvt * NP * 4));
   w.Hc = static_cast<uint16_t*>(take(NP * dm.d * 2));
-  w.HcT = static_cast<uint16_t*>(take(NP * dm.d * 2));
+  w.HcT = static_cast<uint16_t*>(take(KT * dm.d * 2));
   w.WT = static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2));
   w.dZ = static_cast<uint16_t*>(take(NP * dm.V * 2));
-  w.dZT = static_cast<uint16_t*>(take(NP * dm.V * 2));
+  w.dZT = static_cast<uint16_t*>(take(KT * dm.V * 2));
   w.dx_part = static_cast<float*>(take(n_split * NP * dm.d * 4));
   w.P = P;
   w.NP = NP;
   w.nvt = nvt;
   w.n_split = n_split;
   w.k_split = k_split;
+  w.dw_batch = dw_batch;
+  w.KT = KT;
   if (ws) *ws = w;
   return off;
 }
@@ -138,13 +147,13 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
                               const uint8_t* resp, const float* adv, const double* ell_old,
                               double loss_scale, double* ell, double* g, double* loss,
                               int32_t* n_masked, float* t_out, int32_t* flags, bool backward,
-                              hipStream_t s) {
+                              bool first_in_batch, hipStream_t s) {
   const Dims dm = dims_of(p);
   BGPO_TRY(tm.begin(BGPO_K_MASK));
   BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, p->t_mode, p->seed,
                                p->seq_id_base, ws.idx, ws.row_tgt, ws.row_seq, ws.seg_off, ws.t24,
                                ws.meta, n_masked + j, dm.n_t, t_out ? t_out + j : nullptr, dm.n_t,
-                               (int)ws.NP, dm.V, s));
+                               (int)ws.NP, dm.V, first_in_batch ? 1 : 0, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
   BGPO_TRY(launch_gather(hidden, ws, dm.d, s));
@@ -202,7 +211,7 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
   if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
   if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, prob->t_mode,
                           prob->seed, prob->seq_id_base, idx, nullptr, nullptr, nullptr, nullptr,
-                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, (hipStream_t)stream) != hipSuccess)
+                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, 1, (hipStream_t)stream) != hipSuccess)
     return BGPO_ERR_HIP;
   return BGPO_OK;
 }
@@ -236,7 +245,7 @@ int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16
   BGPO_TRY(tm.end());
   for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
     st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, nullptr, nullptr, 0.0,
-                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, s);
+                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, true, s);
     if (st != BGPO_OK) return st;
   }
   BGPO_TRY(tm.finish());
@@ -268,20 +277,26 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
   BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
-  for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
-    st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, adv, ell_old,
-                            loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, s);
-    if (st != BGPO_OK) return st;
-    BGPO_TRY(tm.begin(BGPO_K_RECOMPUTE));
-    BGPO_TRY(launch_gemm_recompute(ws, dm.d, dm.V, grid, s));
-    BGPO_TRY(launch_onehot(ws, dm.V, s));
-    BGPO_TRY(tm.end());
-    BGPO_TRY(tm.begin(BGPO_K_DX));
-    BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
-    BGPO_TRY(tm.end());
-    BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
-    BGPO_TRY(launch_dx_reduce(ws, dX, dm.d, s));
-    BGPO_TRY(tm.end());
+  const int j_end = prob->j_begin + prob->j_count;
+  for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.dw_batch) {
+    const int j1 = std::min<int>(j_end, j0 + (int)ws.dw_batch);
+    for (int j = j0; j < j1; ++j) {
+      st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, adv, ell_old,
+                              loss_scale, ell, g, loss, n_masked, t_out, status_flags, true,
+                              j == j0, s);
+      if (st != BGPO_OK) return st;
+      BGPO_TRY(tm.begin(BGPO_K_RECOMPUTE));
+      BGPO_TRY(launch_gemm_recompute(ws, dm.d, dm.V, grid, s));
+      BGPO_TRY(launch_onehot(ws, dm.V, s));
+      BGPO_TRY(tm.end());
+      BGPO_TRY(tm.begin(BGPO_K_DX));
+      BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
+      BGPO_TRY(tm.end());
+      BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
+      BGPO_TRY(launch_dx_reduce(ws, dX, dm.d, s));
+      BGPO_TRY(tm.end());
+    }
+    // one dW GEMM for the batch: K runs over the batch's samples side by side
     BGPO_TRY(tm.begin(BGPO_K_DW));
     BGPO_TRY(launch_gemm_dw(ws, dW, dm.d, dm.V, grid, s));
     BGPO_TRY(tm.end());

@@ -198,7 +198,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
   int M = p.M, N = p.N, K = p.K, n_valid = p.N;
   if (p.dyn_m) { M = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_n) { N = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
-  if (p.dyn_k) K = (p.meta->n_rows + BK - 1) / BK * BK;
+  if (p.dyn_k) K = p.meta->col_end;    // batched dW: all samples' columns (multiple of 64)
   if (EPI == EPI_F32_ACCUM && K == 0) return;   // nothing to add
   const int tilesM = (M + BM - 1) / BM, tilesN = (N + BN - 1) / BN;
   const int64_t total = (int64_t)tilesM * tilesN * p.n_split;
@@ -410,32 +410,75 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
     } else if constexpr (EPI == EPI_DZ) {
       // dZ = s * softmax (the -s at the target is applied afterwards by a
       // separate one-element-per-row kernel); padded rows get zeros.
+      // dZ[row][v]: each lane holds 4 consecutive vocabulary ids of a row ->
+      // 8-byte stores.  dZ^T[v][row] (columns start at this sample's offset in
+      // the dW batch) goes through LDS: neighbouring rows are paired with a
+      // lane swap into 4-byte LDS words, then written out as 16-byte chunks of
+      // 8 rows, i.e. 128-byte segments per vocabulary id.
+      uint16_t* dZT = p.dZT + p.meta->col_off;
+      constexpr int TROW = WN * 2 + 16;                      // bytes per staged vocabulary id
+      constexpr int HALF_M = WM / 2;                         // vocabulary ids per LDS pass
+      static_assert(C::NWAVES * HALF_M * TROW <= STAGES * (BM + BN) * KCH * 16, "dZ^T staging");
+      char* tls = reinterpret_cast<char*>(smem) + wave * HALF_M * TROW;
+      const bool odd = lane & 1;
+      float Lr[TN], Sr[TN];
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int n = nw + 32 * j + (lane & 31);
         const bool valid = n < n_valid;
-        const float L2 = valid ? p.lse2[n] : 0.f;
-        const float sc = valid ? p.row_scale[n] : 0.f;
+        Lr[j] = valid ? p.lse2[n] : 0.f;
+        Sr[j] = valid ? p.row_scale[n] : 0.f;
+      }
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+      for (int ih = 0; ih < 2; ++ih) {
 #pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4) {
-            const int m = mw + 32 * i + mlane + 8 * e4;   // vocabulary ids m .. m+3
-            if (m < M && n < N) {
-              bf16_t h[4];
+        for (int ii = 0; ii < TM / 2; ++ii) {
+          const int i = ih * (TM / 2) + ii;
 #pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const float pz = __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * e4 + e], kLog2e, -L2));
-                h[e] = f32_to_bf16(valid ? sc * pz : 0.f);
-                p.dZT[(int64_t)(m + e) * p.ldzt + n] = h[e];
-              }
-              uint2 pk;
-              pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-              pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-              *reinterpret_cast<uint2*>(p.dZ + (int64_t)n * p.ldz + m) = pk;
+          for (int j = 0; j < TN; ++j) {
+            const int n = nw + 32 * j + (lane & 31);
+            const bool valid = n < n_valid;
+            // packed pairs: pk[q] = (id 2q, id 2q+1) of this lane's row
+            uint32_t pk[8];
+            const float sc = valid ? Sr[j] : 0.f;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              const float p0 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][2 * q], kLog2e, -Lr[j]));
+              const float p1 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][2 * q + 1], kLog2e, -Lr[j]));
+              pk[q] = pack_bf16x2(sc * p0, sc * p1);
+            }
+#pragma unroll
+            for (int e4 = 0; e4 < 4; ++e4) {
+              const int m = mw + 32 * i + mlane + 8 * e4;   // vocabulary ids m .. m+3
+              if (m < M && n < N)
+                *reinterpret_cast<uint2*>(p.dZ + (int64_t)n * p.ldz + m) =
+                    make_uint2(pk[2 * e4], pk[2 * e4 + 1]);
+            }
+            // rows 2k and 2k+1 sit in lanes 2k and 2k+1: the even lane keeps id
+            // e, the odd lane id e+1, each with its neighbour's value
+#pragma unroll
+            for (int e = 0; e < 16; e += 2) {
+              const uint32_t lo = pk[e >> 1] & 0xFFFFu, hi = pk[e >> 1] >> 16;   // ids e, e+1
+              const uint32_t send = odd ? lo : hi;
+              const uint32_t recv = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)send, 0xB1, 0xF, 0xF, false);
+              const uint32_t word = odd ? (recv | (hi << 16)) : (lo | (recv << 16));
+              const int vl = 32 * ii + mlane + (e & 3) + 8 * (e >> 2) + (odd ? 1 : 0);
+              const int rl = 32 * j + ((lane & 31) & ~1);
+              *reinterpret_cast<uint32_t*>(tls + vl * TROW + rl * 2) = word;
             }
           }
-        __builtin_amdgcn_sched_barrier(0);
+        }
+        // write the staged half: 16-byte chunks (8 rows) of each vocabulary id
+        constexpr int CH = WN / 8;                           // chunks per vocabulary id
+#pragma unroll
+        for (int t = 0; t < HALF_M * CH / 64; ++t) {
+          const int q = lane + 64 * t;
+          const int vl = q / CH, r8 = q % CH;
+          const int m = mw + ih * HALF_M + vl;
+          const uint4 v = *reinterpret_cast<const uint4*>(tls + vl * TROW + r8 * 16);
+          if (m < M && nw + r8 * 8 < N)
+            *reinterpret_cast<uint4*>(dZT + (int64_t)m * p.ldzt + nw + r8 * 8) = v;
+        }
       }
     } else {
       // fp32 store (dX partials) or read-modify-write accumulate (dW); one
@@ -484,7 +527,7 @@ hipError_t launch_gemm_recompute(const Workspace& ws, int d, int V, int grid, hi
   p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.meta;
   p.k_split = d;
   p.row_tgt = ws.row_tgt; p.lse2 = ws.lse2; p.row_scale = ws.row_scale;
-  p.dZ = ws.dZ; p.ldz = V; p.dZT = ws.dZT; p.ldzt = ws.NP;
+  p.dZ = ws.dZ; p.ldz = V; p.dZT = ws.dZT; p.ldzt = ws.KT;
   k_gemm<EPI_DZ, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
   return hipGetLastError();
 }
@@ -503,8 +546,8 @@ hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, 
 
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s) {
   GemmParams p = base_params();
-  p.A = ws.HcT; p.lda = ws.NP;
-  p.B = ws.dZT; p.ldb = ws.NP;
+  p.A = ws.HcT; p.lda = ws.KT;
+  p.B = ws.dZT; p.ldb = ws.KT;
   p.M = d; p.N = V; p.dyn_k = 1; p.meta = ws.meta;
   p.m_fastest = 1;
   p.out = dW; p.ldo = V;
@@ -563,6 +606,9 @@ extern "C" int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, floa
     case 6: k_gemm<EPI_F32_STORE, 256, 256, 64, 64, 128, 2><<<cus, 512, 0, s>>>(p); break;
     case 7: k_gemm<EPI_F32_STORE, 256, 256, 64, 128, 128, 2, 1, 1><<<cus, 256, 0, s>>>(p); break;
     case 8: k_gemm<EPI_F32_STORE, 256, 256, 64, 128, 64, 2, 1, 1><<<cus, 512, 0, s>>>(p); break;
+    case 9: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 4><<<cus, 512, 0, s>>>(p); break;
+    case 10: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 5><<<cus, 512, 0, s>>>(p); break;
+    case 11: k_gemm<EPI_F32_STORE, 256, 256, 64, 64, 128, 2, 1, 1><<<cus, 512, 0, s>>>(p); break;
     default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -3;

@@ -19,7 +19,9 @@ constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
 struct SampleMeta {
   int32_t n_rows;      // N_j: masked positions in this sample (all responses)
   int32_t n_rows_pad;  // N_j rounded up to kRowPad
-  int32_t pad[62];
+  int32_t col_off;     // first column of this sample in H_c^T / dZ^T
+  int32_t col_end;     // col_off + N_j rounded up to 64: K of the batched dW GEMM
+  int32_t pad[60];
 };
 
 // Views into the caller's workspace.
@@ -31,7 +33,7 @@ struct Workspace {
   int32_t* seg_off;    // [B+1]        first compacted row of each response
   uint32_t* t24;       // [B]          integer timestep of each response
   uint16_t* Hc;        // [NP, d]      gathered masked hidden rows (bf16)
-  uint16_t* HcT;       // [d, NP]      the same, transposed
+  uint16_t* HcT;       // [d, KT]      the same, transposed; samples of a dW batch side by side
   uint16_t* WT;        // [V, d]       W_head transposed (bf16)
   float* part_m;       // [nvt, NP]    per-vocab-tile running max (log2 units)
   float* part_s;       // [nvt, NP]    per-vocab-tile sum of 2^(z*log2e - max)
@@ -40,9 +42,11 @@ struct Workspace {
   float* lp;           // [NP]         log p of the target
   float* row_scale;    // [NP]         gradient scale s of each row (0 for padding)
   uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16
-  uint16_t* dZT;       // [V, NP]      the same, transposed
+  uint16_t* dZT;       // [V, KT]      the same, transposed; samples of a dW batch side by side
   float* dx_part;      // [S, NP, d]   split-vocabulary partial dX
   int64_t P, NP, nvt, n_split, k_split;
+  int64_t dw_batch;    // samples whose dW contributions share one GEMM
+  int64_t KT;          // dw_batch * NP: leading dimension of H_c^T and dZ^T
 };
 
 struct Dims {
@@ -57,7 +61,8 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int t_mode, uint64_t seed, uint32_t seq_base, int32_t* idx,
                                int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
                                SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
-                               float* t_out, int t_stride, int row_cap, int V, hipStream_t s);
+                               float* t_out, int t_stride, int row_cap, int V,
+                               int first_in_batch, hipStream_t s);
 hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s);
 hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, hipStream_t s);
 hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s);

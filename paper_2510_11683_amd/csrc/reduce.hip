@@ -175,12 +175,12 @@ __global__ __launch_bounds__(256) void k_onehot(const int32_t* __restrict__ row_
   const float py = __builtin_amdgcn_exp2f(fmaf(ztgt[r], kLog2e, -lse2[r]));
   const bf16_t h = f32_to_bf16(row_scale[r] * (py - 1.f));
   dZ[(int64_t)r * V + y] = h;
-  dZT[(int64_t)y * ldzt + r] = h;
+  dZT[(int64_t)y * ldzt + meta->col_off + r] = h;
 }
 
 hipError_t launch_onehot(const Workspace& ws, int V, hipStream_t s) {
   k_onehot<<<(unsigned)(ws.NP / 256), 256, 0, s>>>(ws.row_tgt, ws.ztgt, ws.lse2, ws.row_scale,
-                                                  ws.meta, ws.dZ, ws.dZT, V, ws.NP);
+                                                  ws.meta, ws.dZ, ws.dZT, V, ws.KT);
   return hipGetLastError();
 }
 

@@ -41,7 +41,8 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     int j, int t_mode, uint32_t k0, uint32_t k1, uint32_t seq_base, int32_t* __restrict__ idx,
     int32_t* __restrict__ row_tgt, int32_t* __restrict__ row_seq, int32_t* __restrict__ seg_off,
     uint32_t* __restrict__ t24_out, SampleMeta* __restrict__ meta, int32_t* __restrict__ nm_out,
-    int nm_stride, float* __restrict__ t_out, int t_stride, int row_cap, int V) {
+    int nm_stride, float* __restrict__ t_out, int t_stride, int row_cap, int V,
+    int first_in_batch) {
   __shared__ uint32_t sT[kMaxB];
   __shared__ int32_t sSeg[kMaxB + 1];
   __shared__ int32_t sWave[kMaskThreads / 64];
@@ -114,6 +115,10 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     if (meta) {
       meta->n_rows = total;
       meta->n_rows_pad = total_pad;
+      // this sample's columns in H_c^T / dZ^T follow the previous sample's
+      const int off = first_in_batch ? 0 : meta->col_end;
+      meta->col_off = off;
+      meta->col_end = off + (total + 63) / 64 * 64;
     }
   }
   if (row_cap > 0) {
@@ -129,17 +134,19 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int j, int t_mode, uint64_t seed, uint32_t seq_base, int32_t* idx,
                                int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
                                SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
-                               float* t_out, int t_stride, int row_cap, int V, hipStream_t s) {
+                               float* t_out, int t_stride, int row_cap, int V,
+                               int first_in_batch, hipStream_t s) {
   k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, t_mode,
                                             (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
                                             seq_base, idx, row_tgt, row_seq, seg_off, t24, meta,
-                                            n_masked_out, nm_stride, t_out, t_stride, row_cap, V);
+                                            n_masked_out, nm_stride, t_out, t_stride, row_cap, V,
+                                            first_in_batch);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Gather: Hc[r, :] = hidden[idx[r], :] and HcT[:, r] for r < N; zeros for
-// N <= r < N_pad.  64x64 tiles staged in LDS for the transposed copy.
+// Gather: Hc[r, :] = hidden[idx[r], :] and HcT[:, col_off + r] for r < N; zeros
+// for N <= r < N_pad.  64x64 tiles staged in LDS for the transposed copy.
 __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hidden,
                                                 const int32_t* __restrict__ idx,
                                                 const SampleMeta* __restrict__ meta,
@@ -149,6 +156,7 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
   const int r0 = blockIdx.x * 64;
   if (r0 >= meta->n_rows_pad) return;
   const int N = meta->n_rows;
+  const int coff = meta->col_off;
   const int c0 = blockIdx.y * 64;
   const int tid = threadIdx.x;
 #pragma unroll
@@ -170,14 +178,14 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
 #pragma unroll
     for (int e = 0; e < 4; ++e)
       w[e] = (uint32_t)tile[rch * 8 + 2 * e][c] | ((uint32_t)tile[rch * 8 + 2 * e + 1][c] << 16);
-    *reinterpret_cast<uint4*>(HcT + (int64_t)(c0 + c) * ldt + r0 + rch * 8) =
+    *reinterpret_cast<uint4*>(HcT + (int64_t)(c0 + c) * ldt + coff + r0 + rch * 8) =
         make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
 
 hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s) {
   dim3 grid((unsigned)(ws.NP / 64), (unsigned)(d / 64));
-  k_gather<<<grid, 256, 0, s>>>(hidden, ws.idx, ws.meta, ws.Hc, ws.HcT, d, ws.NP);
+  k_gather<<<grid, 256, 0, s>>>(hidden, ws.idx, ws.meta, ws.Hc, ws.HcT, d, ws.KT);
   return hipGetLastError();
 }
 
