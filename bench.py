@@ -31,6 +31,31 @@ PEAK_HBM_GBS = 8000.0
 WORKLOADS = {w.name: w for w in workloads.CONFIGS}
 DEFAULT = workloads.LLADA_L512_NT64.name
 GEMM_CLASSES = ("fwd", "recompute", "dx", "dw")
+TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "hbm_traffic_llada_head_B8_L512_nt64.json")
+
+
+def kernel_source_hash() -> str:
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2510_11683_amd", "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
+def hbm_traffic(kernel: str, workload: str):
+    """Calibrated FETCH + WRITE bytes per launch of `kernel` from the committed
+    rocprofv3 counter table, or None if the table is for other kernel sources
+    or another workload."""
+    try:
+        t = json.load(open(TRAFFIC_TABLE))
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    k = t["kernels"].get(kernel)
+    return None if k is None else k["fetch_bytes"] + k["write_bytes"]
 
 
 class Telemetry:
@@ -226,7 +251,7 @@ def main():
                    "masked_tokens_per_step": tokens, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": None},
+                     "traffic": hbm_traffic(dom, w.name)},
         "mfma_frac_executed_8dV": exec_flops / (PEAK_BF16_TFLOPS * 1e12),
         "mfma_frac_useful_6dV": useful_flops / (PEAK_BF16_TFLOPS * 1e12),
         "kernels": per_kernel,
