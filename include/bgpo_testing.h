@@ -29,7 +29,10 @@ int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
  *         9: 8 waves of 128x64, K slab 32, 4 stages; 10: as 9 with 5 stages
  *         11: as 6 with the 256-byte swizzle
  * flags bit 0: M tiles consecutive in the tile walk (else N tiles);
- *       bit 1: plain workgroup order (no XCD grouping).
+ *       bit 1: plain workgroup order (no XCD grouping);
+ *       bits 8-15: if nonzero, band height (M tiles) of the tile walk;
+ *       bits 16-23: if > 1, split K into that many slices, slice s written to
+ *                   C + s * M * N (C then holds that many M x N blocks).
  * Same shape rules and return codes as bgpo_test_gemm_nt. */
 int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
                            int32_t K, int32_t variant, int32_t flags, void* stream);

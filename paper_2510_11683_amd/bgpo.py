@@ -200,8 +200,11 @@ def bgpo_test_gemm_variant(A, B, C, variant: int, flags: int = 0, stream=None):
     """Test hook: tile-configuration variants of the GEMM core (see bgpo_testing.h)."""
     M, K = A.shape
     N = B.shape[0]
+    nsplit = max(1, (flags >> 16) & 0xFF)
+    if C.numel() < nsplit * M * N:
+        raise ValueError("C too small for the requested K split")
     _check(_lib.bgpo_test_gemm_variant(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
-                                       _ptr(C, "C", (torch.float32,), (M, N)), M, N, K,
+                                       _ptr(C, "C", (torch.float32,)), M, N, K,
                                        int(variant), int(flags), _stream(stream)),
            "bgpo_test_gemm_variant")
 

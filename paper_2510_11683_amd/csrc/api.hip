@@ -26,10 +26,11 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   const int64_t P = (int64_t)dm.B * dm.L;
   const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
   const int64_t nvt = (dm.V + kVocabTile - 1) / kVocabTile;
-  // split of the vocabulary (the K of the dX GEMM) so that a sample with half
-  // of the positions masked still yields about 2048 work tiles
+  // split of the vocabulary (the K of the dX GEMM): about 512 work tiles for a
+  // sample with half of the positions masked (two rounds of the persistent
+  // grid); more splits cost more fp32 partial traffic than they gain
   const int64_t tiles_half = std::max<int64_t>(1, (NP / 2 + 255) / 256) * ((dm.d + 255) / 256);
-  int64_t n_split = std::min<int64_t>(16, std::max<int64_t>(1, (2048 + tiles_half - 1) / tiles_half));
+  int64_t n_split = std::min<int64_t>(16, std::max<int64_t>(1, (512 + tiles_half - 1) / tiles_half));
   int64_t k_split = ((dm.V + n_split - 1) / n_split + 63) / 64 * 64;
   n_split = (dm.V + k_split - 1) / k_split;
   // samples per dW GEMM: amortises the fp32 read-modify-write of dW over

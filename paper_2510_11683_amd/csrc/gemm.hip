@@ -38,7 +38,8 @@ struct GemmParams {
   int dyn_m, dyn_n, dyn_k;   // extents taken from the device sample metadata
   int n_split;               // K split count (dX)
   int64_t k_split;           // K per split (multiple of BK)
-  int m_fastest;             // tile order: 1 = M tiles consecutive, 0 = N tiles consecutive
+  int group_m;              // tile order: bands of group_m M tiles, walking along N
+                             // (1 = N tiles consecutive, tilesM = M tiles consecutive)
   int plain_order;           // 1 = no XCD grouping of consecutive tiles (experiments)
   const SampleMeta* meta;
   // epilogue operands
@@ -129,15 +130,20 @@ __device__ __forceinline__ void read_frags(bf16x8 (&fa)[TM], bf16x8 (&fb)[TN], c
   const int ch = ks * 2 + (lane >> 5);
   const uint4* Ac = As + stage * BM * KCH;
   const uint4* Bc = Bs + stage * BN * KCH;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
+  // issue order = order of first use by the next sub-step's MFMAs (i outer,
+  // j inner): B0, A0, B1, A1, then the remaining fragments
+  auto ra = [&](int i) {
     const int row = wm * WM + i * 32 + (lane & 31);
     fa[i] = __builtin_bit_cast(bf16x8, Ac[row * KCH + (ch ^ C::swz(row))]);
-  }
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
+  };
+  auto rb = [&](int j) {
     const int row = wn * WN + j * 32 + (lane & 31);
     fb[j] = __builtin_bit_cast(bf16x8, Bc[row * KCH + (ch ^ C::swz(row))]);
+  };
+#pragma unroll
+  for (int q = 0; q < (TM > TN ? TM : TN); ++q) {
+    if (q < TN) rb(q);
+    if (q < TM) ra(q);
   }
 }
 
@@ -211,11 +217,18 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
     if (t >= total) continue;
     int mt, nt, split;
     {
+      // bands of GM M tiles walk along N, so a run of consecutive tiles (the
+      // ones an XCD holds at once) covers about GM x (run / GM) tiles and
+      // touches GM + run / GM operand panels
       const int64_t per_split = (int64_t)tilesM * tilesN;
       split = (int)(t / per_split);
       const int64_t r = t - (int64_t)split * per_split;
-      if (p.m_fastest) { mt = (int)(r % tilesM); nt = (int)(r / tilesM); }
-      else { nt = (int)(r % tilesN); mt = (int)(r / tilesN); }
+      const int GM = max(1, min(p.group_m, tilesM));
+      const int64_t band = r / ((int64_t)GM * tilesN);
+      const int gm = min(GM, tilesM - (int)band * GM);   // the last band may be shorter
+      const int64_t idx = r - band * GM * tilesN;
+      mt = (int)band * GM + (int)(idx % gm);
+      nt = (int)(idx / gm);
     }
     const int m0 = mt * BM, n0 = nt * BN;
     const int64_t kb = (int64_t)split * p.k_split;
@@ -499,12 +512,19 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
 // sub-tile (4x2 MFMA 32x32 tiles), 256-byte LDS swizzle.
 #define BGPO_TILE 256, 256, 64, 128, 64, 2, 1, 1
 constexpr int kGemmThreads = 512;
+// band heights of the tile walk (see the tile-order comment in k_gemm),
+// measured at the LLaDA head shape: dW and dX fastest with bands of 8, the
+// forward GEMM insensitive between 1 and 8
+constexpr int kGroupMdW = 8;
+constexpr int kGroupMdX = 8;
+constexpr int kGroupMFwd = 4;
 
 static GemmParams base_params() {
   GemmParams p;
   memset(&p, 0, sizeof(p));
   p.n_split = 1;
   p.k_split = INT64_MAX / 4;
+  p.group_m = 1;
   return p;
 }
 
@@ -516,6 +536,7 @@ hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, hipStrea
   p.k_split = d;
   p.part_m = ws.part_m; p.part_s = ws.part_s; p.ldp = ws.NP;
   p.ztgt = ws.ztgt; p.row_tgt = ws.row_tgt;
+  p.group_m = kGroupMFwd;
   k_gemm<EPI_FWD, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
   return hipGetLastError();
 }
@@ -528,6 +549,7 @@ hipError_t launch_gemm_recompute(const Workspace& ws, int d, int V, int grid, hi
   p.k_split = d;
   p.row_tgt = ws.row_tgt; p.lse2 = ws.lse2; p.row_scale = ws.row_scale;
   p.dZ = ws.dZ; p.ldz = V; p.dZT = ws.dZT; p.ldzt = ws.KT;
+  p.group_m = kGroupMFwd;
   k_gemm<EPI_DZ, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
   return hipGetLastError();
 }
@@ -539,6 +561,7 @@ hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, 
   p.B = W; p.ldb = V;
   p.N = d; p.K = V; p.dyn_m = 1; p.meta = ws.meta;
   p.n_split = (int)ws.n_split; p.k_split = ws.k_split;
+  p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.NP * d;
   k_gemm<EPI_F32_STORE, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
   return hipGetLastError();
@@ -549,7 +572,7 @@ hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid
   p.A = ws.HcT; p.lda = ws.KT;
   p.B = ws.dZT; p.ldb = ws.KT;
   p.M = d; p.N = V; p.dyn_k = 1; p.meta = ws.meta;
-  p.m_fastest = 1;
+  p.group_m = kGroupMdW;
   p.out = dW; p.ldo = V;
   k_gemm<EPI_F32_ACCUM, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
   return hipGetLastError();
@@ -590,8 +613,15 @@ extern "C" int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, floa
   p.A = A; p.lda = K; p.B = B; p.ldb = K;
   p.M = M; p.N = N; p.K = K; p.k_split = K;
   p.out = C; p.ldo = N;
-  p.m_fastest = flags & 1;
+  p.group_m = (flags & 1) ? M : 1;
   p.plain_order = (flags >> 1) & 1;
+  if ((flags >> 8) & 0xFF) p.group_m = (flags >> 8) & 0xFF;
+  const int nsplit = (flags >> 16) & 0xFF;
+  if (nsplit > 1) {
+    p.n_split = nsplit;
+    p.k_split = ((K + nsplit - 1) / nsplit + 63) / 64 * 64;
+    p.split_stride = (int64_t)M * N;   // C must hold nsplit x M x N floats
+  }
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -3;
   const int cus = gemm_grid(dev);
