@@ -16,6 +16,8 @@ loops; Section 2.2 and Section 3):
   d_{b,j}      = l_theta - l_old on the same masked sample      (Section 3.1)
   g_{b,j}      = (1 + d) A / n_t  if A >= 0  (first-order Taylor, Lemma 1)
                = e^d A / n_t      if A <  0  (Jensen, Lemma 2)  (Eq. g)
+               (also: Taylor-only / Jensen-only ablations of Table 3, and the
+               exact objective exp(mean_j d_j) A of Eq. elbo_ratio)
   loss        += -loss_scale * g_{b,j}    (Algorithm 1 sets L_j = -g_j / G)
   gradients    of the loss w.r.t. the hidden states and the head weights,
                accumulated over every (b, j) (Algorithm 1, gradient
@@ -51,10 +53,24 @@ def log_softmax_rows(z: np.ndarray) -> np.ndarray:
     return z - (m + np.log(np.exp(z - m).sum(axis=1, keepdims=True)))
 
 
-def bound_term(d: float, A: float, n_t: int):
-    """Eq. g: returns (g_j, dg_j/dl_j).  A >= 0 (including -0.0) takes the
-    Taylor branch, A < 0 the Jensen branch."""
-    if A >= 0:
+BOUND_PAPER, BOUND_TAYLOR, BOUND_JENSEN, BOUND_EXACT = 0, 1, 2, 3
+
+
+def bound_term(d: float, A: float, n_t: int, mode: int = BOUND_PAPER, dbar: float = 0.0):
+    """Per-sample objective term and its derivative w.r.t. l_j: (g_j, dg_j/dl_j).
+
+    BOUND_PAPER  Eq. g: A >= 0 (including -0.0) takes the first-order Taylor
+                 term (1 + d) A / n_t (Lemma 1), A < 0 the Jensen term
+                 e^d A / n_t (Lemma 2)
+    BOUND_TAYLOR the Taylor term for every A (ablation of Table 3)
+    BOUND_JENSEN the Jensen term for every A (ablation of Table 3)
+    BOUND_EXACT  the exact objective R = exp(dbar) A of Eq. elbo_ratio, dbar =
+                 mean_j d_j over all n_t samples; g_j = R / n_t is sample j's
+                 share of its value and dR/dl_j = exp(dbar) A / n_t"""
+    if mode == BOUND_EXACT:
+        e = np.exp(dbar)
+        return e * A / n_t, e * A / n_t
+    if mode == BOUND_TAYLOR or (mode == BOUND_PAPER and A >= 0):
         return (1.0 + d) * A / n_t, A / n_t
     e = np.exp(d)
     return e * A / n_t, e * A / n_t
@@ -73,6 +89,7 @@ class Problem:
     seed: int = 0
     seq_id_base: int = 0
     t_mode: int = 0                 # 0 = i.i.d. U(0,1), 1 = stratified
+    bound: int = 0                  # BOUND_PAPER / _TAYLOR / _JENSEN / _EXACT
 
     @property
     def js(self):
@@ -149,6 +166,16 @@ def elbo_literal_f64(p: Problem, H, W, targets, resp_mask, adv,
     dW = np.zeros((p.d, p.V)) if backward else None
     loss = 0.0
     idx_all = {}
+    dbar = np.zeros(p.B)
+    if p.bound == BOUND_EXACT:
+        # the exact objective couples the samples through mean_j d_j: a first
+        # pass over all n_t samples gives it (Eq. elbo_ratio)
+        if list(p.js) != list(range(p.n_t)):
+            raise ValueError("the exact objective needs the full sample range")
+        first = elbo_literal_f64(dataclasses.replace(p, bound=BOUND_PAPER), H, W, targets,
+                                 resp_mask, adv, ell_old=ell_old, backward=False)
+        d_all = first.ell - (0.0 if ell_old is None else np.asarray(ell_old, dtype=np.float64))
+        dbar = d_all.mean(axis=1)
     for j in p.js:
         T, t, m, idx = sample_masks(p, resp_mask, j)
         idx_all[j] = idx
@@ -157,7 +184,7 @@ def elbo_literal_f64(p: Problem, H, W, targets, resp_mask, adv,
             ell[b, j], rows, lsm = ell_of_mask(H[b], W, targets[b], m[b], t[b])
             nm[b, j] = rows.size
             dj = 0.0 if ell_old is None else ell[b, j] - float(ell_old[b, j])
-            g[b, j], dg = bound_term(dj, float(adv[b]), p.n_t)
+            g[b, j], dg = bound_term(dj, float(adv[b]), p.n_t, p.bound, float(dbar[b]))
             loss += -loss_scale * g[b, j]
             if backward and rows.size:
                 s = loss_scale * dg / t[b]
@@ -220,8 +247,16 @@ def elbo_collapsed(p: Problem, hidden_bits, W_bits, targets, resp_mask, adv,
             tt[b, j] = t[b]
             nm[b, j] = int(m[b].sum())
             ell[b, j] = lp2[b][m[b]].sum() / t[b]
+    dbar = np.zeros(p.B)
+    if p.bound == BOUND_EXACT:
+        if list(p.js) != list(range(p.n_t)):
+            raise ValueError("the exact objective needs the full sample range")
+        dbar = (ell - (0.0 if ell_old is None else np.asarray(ell_old, dtype=np.float64))).mean(axis=1)
+    for j in p.js:
+        T, t, m, idx = masks[j]
+        for b in range(p.B):
             dj = 0.0 if ell_old is None else ell[b, j] - float(ell_old[b, j])
-            g[b, j], dg = bound_term(dj, float(adv[b]), p.n_t)
+            g[b, j], dg = bound_term(dj, float(adv[b]), p.n_t, p.bound, float(dbar[b]))
             loss += -loss_scale * g[b, j]
             wpos[b * p.L:(b + 1) * p.L] += (loss_scale * dg / t[b]) * m[b]
 

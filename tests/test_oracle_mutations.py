@@ -52,24 +52,24 @@ def mut_no_normaliser(z):
     return z - z.max(axis=1, keepdims=True)
 
 
-def mut_swap_branches(d, A, n_t):
+def mut_swap_branches(d, A, n_t, *rest):
     if A < 0:
         return (1.0 + d) * A / n_t, A / n_t
     e = np.exp(d)
     return e * A / n_t, e * A / n_t
 
 
-def mut_taylor_everywhere(d, A, n_t):
+def mut_taylor_everywhere(d, A, n_t, *rest):
     return (1.0 + d) * A / n_t, A / n_t
 
 
-def mut_bound_derivative_missing_nt(d, A, n_t, _f=_orig("bound_term")):
-    g, dg = _f(d, A, n_t)
+def mut_bound_derivative_missing_nt(d, A, n_t, *rest, _f=_orig("bound_term")):
+    g, dg = _f(d, A, n_t, *rest)
     return g, dg * n_t
 
 
-def mut_jensen_derivative_missing_exp(d, A, n_t, _f=_orig("bound_term")):
-    g, dg = _f(d, A, n_t)
+def mut_jensen_derivative_missing_exp(d, A, n_t, *rest, _f=_orig("bound_term")):
+    g, dg = _f(d, A, n_t, *rest)
     return g, (A / n_t if A < 0 else dg)
 
 
