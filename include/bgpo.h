@@ -13,7 +13,8 @@
  *   l_{b,j}      (1/t) * sum over masked positions of log softmax(h W)[target]
  *                (Eq. per_step_loss)
  *   d_{b,j}      l_{b,j} - l_old_{b,j} on the same masked sample (Section 3.1)
- *   g_{b,j}      (1+d) A_b / n_t if A_b >= 0, e^d A_b / n_t if A_b < 0 (Eq. g)
+ *   g_{b,j}      (1+d) A_b / n_t if A_b >= 0, e^d A_b / n_t if A_b < 0 (Eq. g);
+ *                prob->bound selects the variants below
  *   loss        += -loss_scale * g_{b,j}   (Algorithm 1: L_j = -g_j / G)
  *   dX, dW      += gradient of that loss term w.r.t. hidden states and head
  *                weights, accumulated sample by sample (Algorithm 1, gradient
@@ -46,7 +47,7 @@
  *     crosses the ABI.  Entry points keep no mutable global state; calls on
  *     different streams must not share a workspace.
  *   - hidden and W_head are bfloat16 bit patterns (uint16), row-major.
- *   - Supported shapes: B >= 1, L >= 1, B*L <= 2^24, d % 64 == 0,
+ *   - Supported shapes: 1 <= B <= 4096, L >= 1, B*L <= 2^20, d % 64 == 0,
  *     V % 64 == 0, 64 <= d <= 65536, 64 <= V <= 2^20, n_t >= 1,
  *     0 <= j_begin, j_count >= 0, j_begin + j_count <= n_t.  Targets must lie
  *     in [0, V) on every response position.  Other shapes return
@@ -73,6 +74,24 @@ typedef enum bgpo_status {
 /* Timestep modes. */
 enum { BGPO_T_IID = 0, BGPO_T_STRATIFIED = 1 };
 
+/* Objective modes (bgpo_problem.bound), per response b with d_j = l_j - l_old_j:
+ *   BGPO_BOUND_PAPER   Eq. g: the first-order Taylor bound (1 + d_j) A / n_t
+ *                      (Lemma 1) for A >= 0, the Jensen bound e^{d_j} A / n_t
+ *                      (Lemma 2) for A < 0; the tighter lower bound of the two
+ *                      for each sign
+ *   BGPO_BOUND_TAYLOR  the Taylor term for every sign (ablation of Table 3)
+ *   BGPO_BOUND_JENSEN  the Jensen term for every sign (ablation of Table 3)
+ *   BGPO_BOUND_EXACT   the ratio objective exp(B_theta - B_old) A itself
+ *                      (Eq. elbo_ratio) with B the n_t-sample ELBO estimates:
+ *                      g_j = exp(dbar) A / n_t, dbar = mean_j d_j.  Its
+ *                      gradient couples all samples, so bgpo_elbo_bwd_accumulate
+ *                      requires the full range (j_begin 0, j_count n_t; else
+ *                      BGPO_ERR_INVALID_ARG) and, off-policy, first runs a
+ *                      forward pass over every sample to form dbar (memory
+ *                      stays constant in n_t; the forward work doubles).
+ * On-policy (d == 0) all four give g_j = A / n_t and the same gradient. */
+enum { BGPO_BOUND_PAPER = 0, BGPO_BOUND_TAYLOR = 1, BGPO_BOUND_JENSEN = 2, BGPO_BOUND_EXACT = 3 };
+
 /* Bits of *status_flags (device int32, OR-ed in, never cleared by the library). */
 enum { BGPO_FLAG_NONFINITE = 1 };
 
@@ -87,7 +106,7 @@ typedef struct bgpo_problem {
   int32_t t_mode;       /* BGPO_T_IID or BGPO_T_STRATIFIED */
   uint64_t seed;        /* Philox key */
   uint32_t seq_id_base; /* global id of response b = 0 (seq = seq_id_base + b) */
-  uint32_t reserved;    /* must be 0 */
+  int32_t bound;        /* BGPO_BOUND_*; 0 (the paper's objective) for plain callers */
 } bgpo_problem;
 
 /* Kernel classes reported by the optional timing record. */

@@ -26,6 +26,7 @@ BGPO_ERR_UNSUPPORTED = -4
 BGPO_T_IID = 0
 BGPO_T_STRATIFIED = 1
 BGPO_FLAG_NONFINITE = 1
+BGPO_BOUND_PAPER, BGPO_BOUND_TAYLOR, BGPO_BOUND_JENSEN, BGPO_BOUND_EXACT = 0, 1, 2, 3
 KERNEL_CLASSES = ("transpose_w", "mask", "gather", "fwd", "ell", "recompute", "dx", "dx_reduce", "dw")
 
 
@@ -34,7 +35,7 @@ class _Problem(ctypes.Structure):
                 ("V", ctypes.c_int32), ("n_t", ctypes.c_int32), ("j_begin", ctypes.c_int32),
                 ("j_count", ctypes.c_int32), ("t_mode", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("seq_id_base", ctypes.c_uint32),
-                ("reserved", ctypes.c_uint32)]
+                ("bound", ctypes.c_int32)]
 
 
 class Timing(ctypes.Structure):
@@ -95,11 +96,12 @@ class Problem:
     seed: int = 0
     seq_id_base: int = 0
     t_mode: int = BGPO_T_IID
+    bound: int = BGPO_BOUND_PAPER
 
     def c(self) -> _Problem:
         jc = self.n_t - self.j_begin if self.j_count is None else self.j_count
         return _Problem(self.B, self.L, self.d, self.V, self.n_t, self.j_begin, jc, self.t_mode,
-                        self.seed & 0xFFFFFFFFFFFFFFFF, self.seq_id_base & 0xFFFFFFFF, 0)
+                        self.seed & 0xFFFFFFFFFFFFFFFF, self.seq_id_base & 0xFFFFFFFF, self.bound)
 
 
 def _ptr(t: Optional[torch.Tensor], name: str, dtypes=None, shape=None, allow_none=False):

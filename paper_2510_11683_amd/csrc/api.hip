@@ -57,6 +57,7 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   w.lse2 = static_cast<float*>(take(NP * 4));
   w.lp = static_cast<float*>(take(NP * 4));
   w.row_scale = static_cast<float*>(take(NP * 4));
+  w.dbar = static_cast<double*>(take(dm.B * 8));
   w.part_m = static_cast<float*>(take(nvt * NP * 4));
   w.part_s = static_cast<float*>(take(nvt * NP * 4));
   w.Hc = static_cast<uint16_t*>(take(NP * dm.d * 2));
@@ -127,7 +128,7 @@ static int check_problem(const bgpo_problem* p) {
   if (!p) return BGPO_ERR_INVALID_ARG;
   if (p->B < 1 || p->L < 1 || p->n_t < 1 || p->j_begin < 0 || p->j_count < 0 ||
       (int64_t)p->j_begin + p->j_count > p->n_t || (p->t_mode != BGPO_T_IID && p->t_mode != BGPO_T_STRATIFIED) ||
-      p->reserved != 0 || p->d < 1 || p->V < 1)
+      p->bound < BGPO_BOUND_PAPER || p->bound > BGPO_BOUND_EXACT || p->d < 1 || p->V < 1)
     return BGPO_ERR_INVALID_ARG;
   if (p->B > 4096 || (int64_t)p->B * p->L > (1 << 20) || p->d % 64 || p->V % 64 || p->d < 64 ||
       p->d > 65536 || p->V < 64 || p->V > (1 << 20))
@@ -148,7 +149,7 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
                               const uint8_t* resp, const float* adv, const double* ell_old,
                               double loss_scale, double* ell, double* g, double* loss,
                               int32_t* n_masked, float* t_out, int32_t* flags, bool backward,
-                              bool first_in_batch, hipStream_t s) {
+                              bool first_in_batch, const double* dbar, hipStream_t s) {
   const Dims dm = dims_of(p);
   BGPO_TRY(tm.begin(BGPO_K_MASK));
   BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, p->t_mode, p->seed,
@@ -166,7 +167,7 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
   BGPO_TRY(launch_target_logit(ws, dm.d, s));
   BGPO_TRY(launch_combine_rows(ws, dm.V, s));
   BGPO_TRY(launch_seq_terms(ws, dm.B, dm.n_t, j, adv, ell_old, loss_scale, ell, g, loss, flags,
-                            backward, s));
+                            backward, p->bound, dbar, s));
   BGPO_TRY(tm.end());
   return BGPO_OK;
 }
@@ -246,7 +247,8 @@ int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16
   BGPO_TRY(tm.end());
   for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
     st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, nullptr, nullptr, 0.0,
-                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, true, s);
+                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, true, nullptr,
+                            s);
     if (st != BGPO_OK) return st;
   }
   BGPO_TRY(tm.finish());
@@ -267,6 +269,8 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
   if (!aligned16(hidden) || !aligned16(W_head) || !aligned16(dX) || !aligned16(dW))
     return BGPO_ERR_INVALID_ARG;
   if ((st = check_workspace(prob, workspace, ws_bytes)) != BGPO_OK) return st;
+  const bool exact = prob->bound == BGPO_BOUND_EXACT;
+  if (exact && (prob->j_begin != 0 || prob->j_count != prob->n_t)) return BGPO_ERR_INVALID_ARG;
   if (prob->j_count == 0) return BGPO_OK;
   hipStream_t s = (hipStream_t)stream;
   const Dims dm = dims_of(prob);
@@ -278,13 +282,28 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
   BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
+  // exact objective off-policy: a forward pass over every sample gives the
+  // mean log-ratio, which scales every sample's gradient (on-policy it is 0)
+  const double* dbar = nullptr;
+  if (exact && ell_old) {
+    for (int j = 0; j < prob->n_t; ++j) {
+      st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, nullptr, nullptr,
+                              0.0, ell, nullptr, nullptr, n_masked, t_out, status_flags, false,
+                              true, nullptr, s);
+      if (st != BGPO_OK) return st;
+    }
+    BGPO_TRY(tm.begin(BGPO_K_ELL));
+    BGPO_TRY(launch_mean_ratio(ell, ell_old, dm.B, dm.n_t, ws.dbar, s));
+    BGPO_TRY(tm.end());
+    dbar = ws.dbar;
+  }
   const int j_end = prob->j_begin + prob->j_count;
   for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.dw_batch) {
     const int j1 = std::min<int>(j_end, j0 + (int)ws.dw_batch);
     for (int j = j0; j < j1; ++j) {
       st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, adv, ell_old,
                               loss_scale, ell, g, loss, n_masked, t_out, status_flags, true,
-                              j == j0, s);
+                              j == j0, dbar, s);
       if (st != BGPO_OK) return st;
       BGPO_TRY(tm.begin(BGPO_K_RECOMPUTE));
       BGPO_TRY(launch_gemm_recompute(ws, dm.d, dm.V, grid, s));

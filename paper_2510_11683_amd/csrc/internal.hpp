@@ -41,6 +41,7 @@ struct Workspace {
   float* lse2;         // [NP]         log2-sum-exp2 of each row (log2 units)
   float* lp;           // [NP]         log p of the target
   float* row_scale;    // [NP]         gradient scale s of each row (0 for padding)
+  double* dbar;        // [B]          mean log-ratio over all samples (exact objective)
   uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16
   uint16_t* dZT;       // [V, KT]      the same, transposed; samples of a dW batch side by side
   float* dx_part;      // [S, NP, d]   split-vocabulary partial dX
@@ -70,7 +71,10 @@ hipError_t launch_onehot(const Workspace& ws, int V, hipStream_t s);
 hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s);
 hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const float* adv,
                             const double* ell_old, double loss_scale, double* ell, double* g,
-                            double* loss, int32_t* flags, bool backward, hipStream_t s);
+                            double* loss, int32_t* flags, bool backward, int bound,
+                            const double* dbar, hipStream_t s);
+hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, int n_t,
+                             double* dbar, hipStream_t s);
 hipError_t launch_gemm_recompute(const Workspace& ws, int d, int V, int grid, hipStream_t s);
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s);

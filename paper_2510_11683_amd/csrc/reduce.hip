@@ -90,13 +90,36 @@ hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s) {
 constexpr int kSeqThreads = 1024;
 constexpr int kSeqMaxB = 4096;
 
+// The objective's per-sample term g and its derivative dg/dl for
+// d = l - l_old:
+//   paper (Eq. g):  first-order Taylor bound (1 + d) A / n_t for A >= 0
+//                   (Lemma 1), Jensen bound e^d A / n_t for A < 0 (Lemma 2)
+//   Taylor only / Jensen only: one of the two for every sign (the ablation of
+//                   Table 3)
+//   exact:          exp(dbar) A / n_t with dbar the mean of d over all n_t
+//                   samples, whose sum is exp(B_theta - B_old) A
+//                   (Eq. elbo_ratio); dg/dl_j = exp(dbar) A / n_t
+__device__ __forceinline__ void bound_term(double dj, double A, int n_t, int bound, double dbar,
+                                           double* gj, double* dg) {
+  if (bound == 3) {
+    *gj = exp(dbar) * A / n_t;
+    *dg = *gj;
+  } else if (bound == 1 || (bound == 0 && A >= 0.0)) {
+    *gj = (1.0 + dj) * A / n_t;
+    *dg = A / n_t;
+  } else {
+    *gj = exp(dj) * A / n_t;
+    *dg = *gj;
+  }
+}
+
 __global__ __launch_bounds__(kSeqThreads) void k_seq_terms(
     const float* __restrict__ lp, const int32_t* __restrict__ seg_off,
     const uint32_t* __restrict__ t24, const int32_t* __restrict__ row_seq,
     const SampleMeta* __restrict__ meta, int B, int n_t, int j, const float* __restrict__ adv,
     const double* __restrict__ ell_old, double loss_scale, double* __restrict__ ell,
     double* __restrict__ g, double* __restrict__ loss, int32_t* __restrict__ flags,
-    float* __restrict__ row_scale, int backward) {
+    float* __restrict__ row_scale, int backward, int bound, const double* __restrict__ dbar) {
   __shared__ double red[kSeqThreads / 64];
   __shared__ float s_scale[kSeqMaxB];
   __shared__ int s_bad;
@@ -120,16 +143,8 @@ __global__ __launch_bounds__(kSeqThreads) void k_seq_terms(
       ell[o] = l;
       if (backward) {
         const double dj = ell_old ? l - ell_old[o] : 0.0;
-        const double A = (double)adv[b];
         double gj, dg;
-        if (A >= 0.0) {                 // first-order Taylor bound (Lemma 1)
-          gj = (1.0 + dj) * A / n_t;
-          dg = A / n_t;
-        } else {                        // Jensen bound (Lemma 2)
-          const double e = exp(dj);
-          gj = e * A / n_t;
-          dg = gj;
-        }
+        bound_term(dj, (double)adv[b], n_t, bound, dbar ? dbar[b] : 0.0, &gj, &dg);
         g[o] = gj;
         loss_acc += -loss_scale * gj;
         const double sc = loss_scale * dg / t;
@@ -153,10 +168,30 @@ __global__ __launch_bounds__(kSeqThreads) void k_seq_terms(
 
 hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const float* adv,
                             const double* ell_old, double loss_scale, double* ell, double* g,
-                            double* loss, int32_t* flags, bool backward, hipStream_t s) {
+                            double* loss, int32_t* flags, bool backward, int bound,
+                            const double* dbar, hipStream_t s) {
   k_seq_terms<<<1, kSeqThreads, 0, s>>>(ws.lp, ws.seg_off, ws.t24, ws.row_seq, ws.meta, B, n_t, j,
                                         adv, ell_old, loss_scale, ell, g, loss, flags,
-                                        ws.row_scale, backward ? 1 : 0);
+                                        ws.row_scale, backward ? 1 : 0, bound, dbar);
+  return hipGetLastError();
+}
+
+// dbar[b] = (1/n_t) sum_j (l[b][j] - l_old[b][j]), samples in order: the
+// log-ratio B_theta - B_old of Eq. elbo_ratio with both ELBOs estimated on the
+// same n_t masked samples.
+__global__ __launch_bounds__(256) void k_mean_ratio(const double* __restrict__ ell,
+                                                    const double* __restrict__ ell_old, int B,
+                                                    int n_t, double* __restrict__ dbar) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= B) return;
+  double acc = 0.0;
+  for (int j = 0; j < n_t; ++j) acc += ell[(int64_t)b * n_t + j] - ell_old[(int64_t)b * n_t + j];
+  dbar[b] = acc / n_t;
+}
+
+hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, int n_t,
+                             double* dbar, hipStream_t s) {
+  k_mean_ratio<<<(unsigned)((B + 255) / 256), 256, 0, s>>>(ell, ell_old, B, n_t, dbar);
   return hipGetLastError();
 }
 

@@ -11,11 +11,11 @@ def lib():
     return bgpo
 
 
-def problem(w: workloads.Workload, j_begin=0, j_count=None, n_t=None):
+def problem(w: workloads.Workload, j_begin=0, j_count=None, n_t=None, bound=0):
     b = lib()
     return b.Problem(w.B, w.L, w.d, w.V, w.n_t if n_t is None else n_t, j_begin=j_begin,
                      j_count=j_count, seed=w.philox_seed, seq_id_base=w.seq_id_base,
-                     t_mode=w.t_mode)
+                     t_mode=w.t_mode, bound=bound)
 
 
 class Runner:
@@ -47,11 +47,11 @@ class Runner:
         b.bgpo_elbo_fwd(problem(self.w, j_begin, j_count), d["hidden"], d["W"], d["targets"],
                         d["resp_mask"], self.ell, self.nm, self.t, self.ws, timing=timing)
 
-    def bwd(self, j_begin=0, j_count=None, ell_old=None, loss_scale=1.0 / 8, timing=None):
+    def bwd(self, j_begin=0, j_count=None, ell_old=None, loss_scale=1.0 / 8, timing=None, bound=0):
         b = lib()
         d = self.dev
         eo = None if ell_old is None else torch.as_tensor(ell_old, dtype=torch.float64).cuda().contiguous()
-        b.bgpo_elbo_bwd_accumulate(problem(self.w, j_begin, j_count), d["hidden"], d["W"],
+        b.bgpo_elbo_bwd_accumulate(problem(self.w, j_begin, j_count, bound=bound), d["hidden"], d["W"],
                                    d["targets"], d["resp_mask"], d["adv"], eo, loss_scale,
                                    self.dX, self.dW, self.ell, self.g, self.loss, self.nm, self.t,
                                    self.flags, self.ws, timing=timing)

@@ -98,13 +98,21 @@ def test_null_pointers_and_workspace_rejected_before_hip(b):
     # sample masks: j out of range
     assert lib.bgpo_sample_masks(ctypes.byref(p), fake, 4, fake, fake, None, None) == -1
     assert lib.bgpo_sample_masks(ctypes.byref(p), fake, -1, fake, fake, None, None) == -1
-    # bad reserved field
-    q = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
-    q.reserved = 1
-    assert lib.bgpo_workspace_size(ctypes.byref(q), ctypes.byref(nbytes)) == -1
+    # objective mode outside BGPO_BOUND_*
+    for bad in (-1, 4):
+        q = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
+        q.bound = bad
+        assert lib.bgpo_workspace_size(ctypes.byref(q), ctypes.byref(nbytes)) == -1
+    # the exact objective couples all samples: a partial range is refused
+    # before anything is enqueued
+    q = _prob(b, B=2, L=64, d=128, V=1024, n_t=4, j_begin=1, j_count=2).c()
+    q.bound = b.BGPO_BOUND_EXACT
+    assert lib.bgpo_elbo_bwd_accumulate(ctypes.byref(q), fake, fake, fake, fake, fake, None, 0.125,
+                                        fake, fake, fake, fake, fake, fake, None, None,
+                                        ws_small, nbytes.value, None, None) == -1
 
 
 def test_problem_struct_layout(b):
-    # matches the C struct: 8 int32, uint64, 2 uint32 = 48 bytes
+    # matches the C struct: 8 int32, uint64, uint32, int32 = 48 bytes
     assert ctypes.sizeof(b._Problem) == 48
     assert b._Problem.seed.offset == 32
