@@ -114,9 +114,10 @@ enum {
   BGPO_K_TRANSPOSE_W = 0,  /* W[d,V] -> W^T[V,d] staging, once per call */
   BGPO_K_MASK = 1,         /* Philox t and masks + stable compaction */
   BGPO_K_GATHER = 2,       /* masked hidden rows -> H_c and H_c^T */
-  BGPO_K_FWD = 3,          /* fused LM-head GEMM + online log-sum-exp partials */
+  BGPO_K_FWD = 3,          /* fused LM-head GEMM + online log-sum-exp partials (in the
+                              backward it also stores the exponentials) */
   BGPO_K_ELL = 4,          /* partial combine, log p, l, d, g, loss, gradient scale */
-  BGPO_K_RECOMPUTE = 5,    /* logits recompute + softmax-minus-onehot -> dZ */
+  BGPO_K_SOFTMAX_GRAD = 5, /* stored exponentials -> dZ = s (softmax - onehot), both layouts */
   BGPO_K_DX = 6,           /* dZ W^T split over the vocabulary */
   BGPO_K_DX_REDUCE = 7,    /* split reduction + scatter-add into dX */
   BGPO_K_DW = 8,           /* H_c^T dZ accumulated into dW */

@@ -27,7 +27,7 @@ BGPO_T_IID = 0
 BGPO_T_STRATIFIED = 1
 BGPO_FLAG_NONFINITE = 1
 BGPO_BOUND_PAPER, BGPO_BOUND_TAYLOR, BGPO_BOUND_JENSEN, BGPO_BOUND_EXACT = 0, 1, 2, 3
-KERNEL_CLASSES = ("transpose_w", "mask", "gather", "fwd", "ell", "recompute", "dx", "dx_reduce", "dw")
+KERNEL_CLASSES = ("transpose_w", "mask", "gather", "fwd", "ell", "softmax_grad", "dx", "dx_reduce", "dw")
 
 
 class _Problem(ctypes.Structure):

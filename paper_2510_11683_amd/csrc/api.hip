@@ -2,8 +2,9 @@
 //
 // One call walks the Monte-Carlo samples j of its range in order (Algorithm 1,
 // inner loop): draw t and the mask, compact and gather the masked rows, run the
-// fused LM-head forward, form l, d, g and the gradient scale, then recompute
-// the logits into dZ = s (softmax - onehot) and accumulate dX and dW before the
+// fused LM-head forward (which, with backward, also keeps the exponentials of
+// the logits), form l, d, g and the gradient scale, turn the exponentials into
+// dZ = s (softmax - onehot) and accumulate dX and dW before the
 // next sample starts.  All buffers are views into the caller's workspace,
 // sized by B, L, d and V; nothing depends on n_t, so device memory is the same
 // for any number of samples.
@@ -161,7 +162,7 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
   BGPO_TRY(launch_gather(hidden, ws, dm.d, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_FWD));
-  BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, s));
+  BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, backward, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_ELL));
   BGPO_TRY(launch_target_logit(ws, dm.d, s));
@@ -305,9 +306,8 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
                               loss_scale, ell, g, loss, n_masked, t_out, status_flags, true,
                               j == j0, dbar, s);
       if (st != BGPO_OK) return st;
-      BGPO_TRY(tm.begin(BGPO_K_RECOMPUTE));
-      BGPO_TRY(launch_gemm_recompute(ws, dm.d, dm.V, grid, s));
-      BGPO_TRY(launch_onehot(ws, dm.V, s));
+      BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
+      BGPO_TRY(launch_softmax_grad(ws, dm.V, s));
       BGPO_TRY(tm.end());
       BGPO_TRY(tm.begin(BGPO_K_DX));
       BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));

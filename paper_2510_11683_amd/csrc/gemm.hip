@@ -27,7 +27,7 @@
 
 namespace bgpo {
 
-enum EpiKind { EPI_FWD = 0, EPI_DZ = 1, EPI_F32_STORE = 2, EPI_F32_ACCUM = 3 };
+enum EpiKind { EPI_FWD = 0, EPI_FWDU = 1, EPI_F32_STORE = 2, EPI_F32_ACCUM = 3 };
 
 struct GemmParams {
   const uint16_t* A;
@@ -45,17 +45,11 @@ struct GemmParams {
   // epilogue operands
   float* out;                // F32 store / accumulate target
   int64_t ldo, split_stride;
-  float* part_m;             // FWD: per-vocab-tile (max, sum) partials [M/BM][ldp]
+  float* part_m;             // FWD: per-128-vocabulary-slice (max, sum) partials [M/WM][ldp]
   float* part_s;
   int64_t ldp;
-  float* ztgt;               // FWD: target logit per row
-  const int32_t* row_tgt;
-  const float* lse2;         // DZ
-  const float* row_scale;    // DZ
-  uint16_t* dZ;              // DZ: [rows][ldz]
+  uint16_t* dZ;              // FWDU: exponentials u, [rows][ldz]
   int64_t ldz;
-  uint16_t* dZT;             // DZ: [V][ldzt]
-  int64_t ldzt;
 };
 
 template <int BM, int BN, int BK, int WM, int WN, int SWZ = 0>
@@ -352,114 +346,56 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
     }
 
     // ---------------- epilogues ----------------
-    if constexpr (EPI == EPI_FWD) {
-      // per (row, vocabulary tile): running max and sum of exponentials, in
-      // log2 units; the lanes l and l ^ 32 hold the two halves of a row's
-      // 64-entry slice, the waves along M hold the other slices.
-      float* red = reinterpret_cast<float*>(smem);   // [NWM][BN] max, then [NWM][BN] sum
-      const bool full_m = m0 + BM <= M;
+    if constexpr (EPI == EPI_FWD || EPI == EPI_FWDU) {
+      // Per (row, 128-entry vocabulary slice of this wave): max m and sum of
+      // 2^(z log2e - m), in log2 units, written straight to the partials (the
+      // slice of wave row wm is partial index mw / 128).  Lanes l and l ^ 32
+      // hold the two halves of a row's slice.  EPI_FWDU also stores the
+      // exponentials u = 2^(z log2e - m) as fp16 into dZ[row][v] (each lane
+      // holds 4 consecutive vocabulary ids of a row: 8-byte stores); the
+      // softmax-gradient kernel later turns them into s (p - onehot) with
+      // p = u 2^(m - lse) and writes the transposed copy.  Both variants sum
+      // in the same order, so l is bit-identical between them.  No LDS is
+      // used here.
+      static_assert(WM == kVocabTile, "one partial per wave slice");
+      constexpr bool kStore = EPI == EPI_FWDU;
+      if (mw + WM > M) {
+        // the wave slice crosses the end of the vocabulary: entries past it
+        // become -inf, i.e. exponentials 0 (wave-uniform branch)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              if (mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2) >= M) acc[i][j][e] = -INFINITY;
+      }
+      float mref[TN], ssum[TN];
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         float mx = -INFINITY;
-        if (full_m) {
 #pragma unroll
-          for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[i][j][e]);
-        } else {
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int m = mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2);
-              if (m < M) mx = fmaxf(mx, acc[i][j][e]);
-            }
-        }
+          for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[i][j][e]);
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float mx2 = mx * kLog2e;
-        float s = 0.f;
-        if (mx2 > -INFINITY) {
-          if (full_m) {
+        mref[j] = mx > -INFINITY ? mx * kLog2e : 0.f;        // a slice past V has no entries
+        ssum[j] = 0.f;
+      }
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i) {
 #pragma unroll
-              for (int e = 0; e < 16; ++e)
-                s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mx2));
-          } else {
+        for (int j = 0; j < TN; ++j) {
+          const int n = nw + 32 * j + (lane & 31);
+          uint32_t pk[8];   // pk[q] = (id 2q, id 2q+1) of this lane's row
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-              for (int e = 0; e < 16; ++e) {
-                const int m = mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2);
-                if (m < M) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mx2));
-              }
+          for (int q = 0; q < 8; ++q) {
+            const float u0 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][2 * q], kLog2e, -mref[j]));
+            const float u1 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][2 * q + 1], kLog2e, -mref[j]));
+            ssum[j] += u0 + u1;
+            if constexpr (kStore) pk[q] = pack_f16x2(u0, u1);
           }
-        }
-        s += __shfl_xor(s, 32, 64);
-        if (lane < 32) {
-          const int nl = wn * WN + 32 * j + lane;
-          red[wm * BN + nl] = mx2;
-          red[C::NWM * BN + wm * BN + nl] = s;
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      __syncthreads();
-      const int vt = m0 / BM;
-      for (int q = tid; q < BN; q += NT) {
-        const int n = n0 + q;
-        if (n >= n_valid) continue;
-        float M2 = -INFINITY;
-#pragma unroll
-        for (int a = 0; a < C::NWM; ++a) M2 = fmaxf(M2, red[a * BN + q]);
-        float S = 0.f;
-#pragma unroll
-        for (int a = 0; a < C::NWM; ++a) {
-          const float sa = red[C::NWM * BN + a * BN + q];
-          if (sa > 0.f) S += sa * __builtin_amdgcn_exp2f(red[a * BN + q] - M2);
-        }
-        p.part_m[(int64_t)vt * p.ldp + n] = M2;
-        p.part_s[(int64_t)vt * p.ldp + n] = S;
-      }
-    } else if constexpr (EPI == EPI_DZ) {
-      // dZ = s * softmax (the -s at the target is applied afterwards by a
-      // separate one-element-per-row kernel); padded rows get zeros.
-      // dZ[row][v]: each lane holds 4 consecutive vocabulary ids of a row ->
-      // 8-byte stores.  dZ^T[v][row] (columns start at this sample's offset in
-      // the dW batch) goes through LDS: neighbouring rows are paired with a
-      // lane swap into 4-byte LDS words, then written out as 16-byte chunks of
-      // 8 rows, i.e. 128-byte segments per vocabulary id.
-      uint16_t* dZT = p.dZT + p.meta->col_off;
-      constexpr int TROW = WN * 2 + 16;                      // bytes per staged vocabulary id
-      constexpr int HALF_M = WM / 2;                         // vocabulary ids per LDS pass
-      static_assert(C::NWAVES * HALF_M * TROW <= STAGES * (BM + BN) * KCH * 16, "dZ^T staging");
-      char* tls = reinterpret_cast<char*>(smem) + wave * HALF_M * TROW;
-      const bool odd = lane & 1;
-      float Lr[TN], Sr[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = nw + 32 * j + (lane & 31);
-        const bool valid = n < n_valid;
-        Lr[j] = valid ? p.lse2[n] : 0.f;
-        Sr[j] = valid ? p.row_scale[n] : 0.f;
-      }
-#pragma unroll
-      for (int ih = 0; ih < 2; ++ih) {
-#pragma unroll
-        for (int ii = 0; ii < TM / 2; ++ii) {
-          const int i = ih * (TM / 2) + ii;
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int n = nw + 32 * j + (lane & 31);
-            const bool valid = n < n_valid;
-            // packed pairs: pk[q] = (id 2q, id 2q+1) of this lane's row
-            uint32_t pk[8];
-            const float sc = valid ? Sr[j] : 0.f;
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              const float p0 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][2 * q], kLog2e, -Lr[j]));
-              const float p1 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][2 * q + 1], kLog2e, -Lr[j]));
-              pk[q] = pack_bf16x2(sc * p0, sc * p1);
-            }
+          if constexpr (kStore) {
 #pragma unroll
             for (int e4 = 0; e4 < 4; ++e4) {
               const int m = mw + 32 * i + mlane + 8 * e4;   // vocabulary ids m .. m+3
@@ -467,30 +403,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
                 *reinterpret_cast<uint2*>(p.dZ + (int64_t)n * p.ldz + m) =
                     make_uint2(pk[2 * e4], pk[2 * e4 + 1]);
             }
-            // rows 2k and 2k+1 sit in lanes 2k and 2k+1: the even lane keeps id
-            // e, the odd lane id e+1, each with its neighbour's value
-#pragma unroll
-            for (int e = 0; e < 16; e += 2) {
-              const uint32_t lo = pk[e >> 1] & 0xFFFFu, hi = pk[e >> 1] >> 16;   // ids e, e+1
-              const uint32_t send = odd ? lo : hi;
-              const uint32_t recv = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)send, 0xB1, 0xF, 0xF, false);
-              const uint32_t word = odd ? (recv | (hi << 16)) : (lo | (recv << 16));
-              const int vl = 32 * ii + mlane + (e & 3) + 8 * (e >> 2) + (odd ? 1 : 0);
-              const int rl = 32 * j + ((lane & 31) & ~1);
-              *reinterpret_cast<uint32_t*>(tls + vl * TROW + rl * 2) = word;
-            }
           }
         }
-        // write the staged half: 16-byte chunks (8 rows) of each vocabulary id
-        constexpr int CH = WN / 8;                           // chunks per vocabulary id
+      }
+      const int vt = mw / WM;
 #pragma unroll
-        for (int t = 0; t < HALF_M * CH / 64; ++t) {
-          const int q = lane + 64 * t;
-          const int vl = q / CH, r8 = q % CH;
-          const int m = mw + ih * HALF_M + vl;
-          const uint4 v = *reinterpret_cast<const uint4*>(tls + vl * TROW + r8 * 16);
-          if (m < M && nw + r8 * 8 < N)
-            *reinterpret_cast<uint4*>(dZT + (int64_t)m * p.ldzt + nw + r8 * 8) = v;
+      for (int j = 0; j < TN; ++j) {
+        const float st = ssum[j] + __shfl_xor(ssum[j], 32, 64);
+        const int n = nw + 32 * j + lane;
+        if (lane < 32 && mw < M && n < n_valid) {
+          p.part_m[(int64_t)vt * p.ldp + n] = mref[j];
+          p.part_s[(int64_t)vt * p.ldp + n] = st;
         }
       }
     } else {
@@ -528,29 +451,21 @@ static GemmParams base_params() {
   return p;
 }
 
-hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, hipStream_t s) {
+hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool store_u,
+                           hipStream_t s) {
   GemmParams p = base_params();
   p.A = ws.WT; p.lda = d;
   p.B = ws.Hc; p.ldb = d;
   p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.meta;
   p.k_split = d;
   p.part_m = ws.part_m; p.part_s = ws.part_s; p.ldp = ws.NP;
-  p.ztgt = ws.ztgt; p.row_tgt = ws.row_tgt;
   p.group_m = kGroupMFwd;
-  k_gemm<EPI_FWD, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
-  return hipGetLastError();
-}
-
-hipError_t launch_gemm_recompute(const Workspace& ws, int d, int V, int grid, hipStream_t s) {
-  GemmParams p = base_params();
-  p.A = ws.WT; p.lda = d;
-  p.B = ws.Hc; p.ldb = d;
-  p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.meta;
-  p.k_split = d;
-  p.row_tgt = ws.row_tgt; p.lse2 = ws.lse2; p.row_scale = ws.row_scale;
-  p.dZ = ws.dZ; p.ldz = V; p.dZT = ws.dZT; p.ldzt = ws.KT;
-  p.group_m = kGroupMFwd;
-  k_gemm<EPI_DZ, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  if (store_u) {
+    p.dZ = ws.dZ; p.ldz = V;
+    k_gemm<EPI_FWDU, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  } else {
+    k_gemm<EPI_FWD, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  }
   return hipGetLastError();
 }
 

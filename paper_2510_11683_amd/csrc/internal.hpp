@@ -10,8 +10,9 @@ namespace bgpo {
 // Rows of the compacted masked-position list are padded to a multiple of
 // this (the row tile of the LM-head GEMMs); padded rows carry zeros.
 constexpr int kRowPad = 256;
-// Column tile of the LM-head GEMM over the vocabulary = one log-sum-exp partial.
-constexpr int kVocabTile = 256;
+// Vocabulary slice of one log-sum-exp partial (the M extent of one wave of the
+// LM-head GEMM).
+constexpr int kVocabTile = 128;
 
 constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
 
@@ -35,14 +36,14 @@ struct Workspace {
   uint16_t* Hc;        // [NP, d]      gathered masked hidden rows (bf16)
   uint16_t* HcT;       // [d, KT]      the same, transposed; samples of a dW batch side by side
   uint16_t* WT;        // [V, d]       W_head transposed (bf16)
-  float* part_m;       // [nvt, NP]    per-vocab-tile running max (log2 units)
-  float* part_s;       // [nvt, NP]    per-vocab-tile sum of 2^(z*log2e - max)
+  float* part_m;       // [nvt, NP]    per-vocabulary-slice max (log2 units)
+  float* part_s;       // [nvt, NP]    per-vocabulary-slice sum of 2^(z*log2e - max)
   float* ztgt;         // [NP]         target logit
   float* lse2;         // [NP]         log2-sum-exp2 of each row (log2 units)
   float* lp;           // [NP]         log p of the target
   float* row_scale;    // [NP]         gradient scale s of each row (0 for padding)
   double* dbar;        // [B]          mean log-ratio over all samples (exact objective)
-  uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16
+  uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16 (first the fp16 exponentials)
   uint16_t* dZT;       // [V, KT]      the same, transposed; samples of a dW batch side by side
   float* dx_part;      // [S, NP, d]   split-vocabulary partial dX
   int64_t P, NP, nvt, n_split, k_split;
@@ -65,9 +66,9 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                float* t_out, int t_stride, int row_cap, int V,
                                int first_in_batch, hipStream_t s);
 hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s);
-hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, hipStream_t s);
+hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool store_u,
+                           hipStream_t s);
 hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s);
-hipError_t launch_onehot(const Workspace& ws, int V, hipStream_t s);
 hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s);
 hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const float* adv,
                             const double* ell_old, double loss_scale, double* ell, double* g,
@@ -75,7 +76,7 @@ hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const fl
                             const double* dbar, hipStream_t s);
 hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, int n_t,
                              double* dbar, hipStream_t s);
-hipError_t launch_gemm_recompute(const Workspace& ws, int d, int V, int grid, hipStream_t s);
+hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s);
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s);
 hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s);

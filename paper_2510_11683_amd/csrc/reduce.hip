@@ -195,27 +195,95 @@ hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, in
   return hipGetLastError();
 }
 
-// dZ[row, y] = bf16(s (p_y - 1)) in both layouts; the recompute epilogue wrote
-// bf16(s p_y) there.
-__global__ __launch_bounds__(256) void k_onehot(const int32_t* __restrict__ row_tgt,
-                                                const float* __restrict__ ztgt,
-                                                const float* __restrict__ lse2,
-                                                const float* __restrict__ row_scale,
-                                                const SampleMeta* __restrict__ meta,
-                                                uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT,
-                                                int V, int64_t ldzt) {
-  const int r = blockIdx.x * 256 + threadIdx.x;
-  if (r >= meta->n_rows) return;
-  const int y = row_tgt[r];
-  const float py = __builtin_amdgcn_exp2f(fmaf(ztgt[r], kLog2e, -lse2[r]));
-  const bf16_t h = f32_to_bf16(row_scale[r] * (py - 1.f));
-  dZ[(int64_t)r * V + y] = h;
-  dZT[(int64_t)y * ldzt + meta->col_off + r] = h;
+// dZ = s (p - onehot) in bf16, in place over the fp16 exponentials
+// u = 2^(z log2e - m_h) stored by the forward GEMM, with m_h the row's max over
+// the 128-entry vocabulary slice h: p = u 2^(m_h - lse2).  (Differentiating
+// Eq. per_step_loss, d l / d z = (onehot - p) / t; s carries -loss_scale dg/dl
+// and the 1/t.)  At the target the value comes from the fp32 target logit,
+// s (2^(z_y log2e - lse2) - 1), not from the rounded u.  Padded rows become
+// zeros.  One workgroup per (64-row chunk, slice): the rows are read and
+// rewritten in 256-byte runs, and the transposed copy dZ^T[v][col_off + row]
+// is assembled in LDS and written as 128-byte runs of 64 rows.
+__global__ __launch_bounds__(256) void k_softmax_grad(
+    const float* __restrict__ part_m, const float* __restrict__ lse2,
+    const float* __restrict__ row_scale, const float* __restrict__ ztgt,
+    const int32_t* __restrict__ row_tgt, const SampleMeta* __restrict__ meta,
+    uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT, int V, int64_t ldp, int64_t ldzt) {
+  constexpr int kTS = 33;                                // words per vocabulary id in the tile
+  __shared__ float s_c[64], s_oh[64];
+  __shared__ int s_y[64];
+  __shared__ uint32_t tile[kVocabTile * kTS];            // [v][row pair], (row 2k, row 2k+1)
+  const int h = blockIdx.x, r0 = blockIdx.y * 64;
+  if (r0 >= meta->n_rows_pad) return;   // n_rows_pad is a multiple of 64: chunks are whole
+  const int N = meta->n_rows;
+  const int tid = threadIdx.x;
+  if (tid < 64) {
+    const int r = r0 + tid;
+    float c = 0.f, oh = 0.f;
+    int y = -1;
+    if (r < N) {
+      const float l2 = lse2[r], sr = row_scale[r];
+      c = sr * __builtin_amdgcn_exp2f(part_m[(int64_t)h * ldp + r] - l2);
+      y = row_tgt[r];
+      oh = sr * (__builtin_amdgcn_exp2f(fmaf(ztgt[r], kLog2e, -l2)) - 1.f);
+    }
+    s_c[tid] = c;
+    s_oh[tid] = oh;
+    s_y[tid] = y;
+  }
+  __syncthreads();
+  const int v_lo = h * kVocabTile;
+  const int nv = min(kVocabTile, V - v_lo);   // 128, or 64 in a last half slice
+  const int cpr = nv / 8;                     // 16-byte chunks per row
+  // rows 2 rp and 2 rp + 1, vocabulary ids v0 .. v0 + 7
+  for (int q = tid; q < 32 * cpr; q += 256) {
+    const int vc = q % cpr, rp = q / cpr;
+    const int ra = 2 * rp, v0 = v_lo + vc * 8;
+    uint4* pa = reinterpret_cast<uint4*>(dZ + (int64_t)(r0 + ra) * V + v0);
+    uint4* pb = reinterpret_cast<uint4*>(dZ + (int64_t)(r0 + ra + 1) * V + v0);
+    uint32_t oa[4] = {0, 0, 0, 0}, ob[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int rl = ra + half;
+      if (r0 + rl >= N) continue;
+      const uint4 u = half ? *pb : *pa;
+      const uint32_t uw[4] = {u.x, u.y, u.z, u.w};
+      const float c = s_c[rl], oh = s_oh[rl];
+      const int yo = s_y[rl] - v0;
+      uint32_t* o = half ? ob : oa;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        float x0 = c * f16_to_f32((uint16_t)(uw[k] & 0xFFFFu));
+        float x1 = c * f16_to_f32((uint16_t)(uw[k] >> 16));
+        if (yo == 2 * k) x0 = oh;
+        if (yo == 2 * k + 1) x1 = oh;
+        o[k] = pack_bf16x2(x0, x1);
+      }
+    }
+    *pa = make_uint4(oa[0], oa[1], oa[2], oa[3]);
+    *pb = make_uint4(ob[0], ob[1], ob[2], ob[3]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int vl = vc * 8 + 2 * k;
+      tile[vl * kTS + rp] = (oa[k] & 0xFFFFu) | (ob[k] << 16);
+      tile[(vl + 1) * kTS + rp] = (oa[k] >> 16) | (ob[k] & 0xFFFF0000u);
+    }
+  }
+  __syncthreads();
+  // dZ^T: 8 lanes (64 rows, 128 bytes) per vocabulary id
+  uint16_t* zt = dZT + meta->col_off;
+  for (int q = tid; q < nv * 8; q += 256) {
+    const int vl = q >> 3, c = q & 7;
+    const uint32_t* src = tile + vl * kTS + 4 * c;
+    *reinterpret_cast<uint4*>(zt + (int64_t)(v_lo + vl) * ldzt + r0 + 8 * c) =
+        make_uint4(src[0], src[1], src[2], src[3]);
+  }
 }
 
-hipError_t launch_onehot(const Workspace& ws, int V, hipStream_t s) {
-  k_onehot<<<(unsigned)(ws.NP / 256), 256, 0, s>>>(ws.row_tgt, ws.ztgt, ws.lse2, ws.row_scale,
-                                                  ws.meta, ws.dZ, ws.dZT, V, ws.KT);
+hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s) {
+  dim3 grid((unsigned)ws.nvt, (unsigned)(ws.NP / 64));
+  k_softmax_grad<<<grid, 256, 0, s>>>(ws.part_m, ws.lse2, ws.row_scale, ws.ztgt, ws.row_tgt,
+                                      ws.meta, ws.dZ, ws.dZT, V, ws.NP, ws.KT);
   return hipGetLastError();
 }
 
