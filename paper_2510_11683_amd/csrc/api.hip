@@ -27,13 +27,10 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   const int64_t P = (int64_t)dm.B * dm.L;
   const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
   const int64_t nvt = (dm.V + kVocabTile - 1) / kVocabTile;
-  // split of the vocabulary (the K of the dX GEMM): about 512 work tiles for a
-  // sample with half of the positions masked (two rounds of the persistent
-  // grid); more splits cost more fp32 partial traffic than they gain
-  const int64_t tiles_half = std::max<int64_t>(1, (NP / 2 + 255) / 256) * ((dm.d + 255) / 256);
-  int64_t n_split = std::min<int64_t>(16, std::max<int64_t>(1, (512 + tiles_half - 1) / tiles_half));
-  int64_t k_split = ((dm.V + n_split - 1) / n_split + 63) / 64 * 64;
-  n_split = (dm.V + k_split - 1) / k_split;
+  // capacity of the split-vocabulary dX partials: up to 16 splits (the mask
+  // kernel picks each sample's count), within about 4 GB
+  const int64_t per_split = NP * dm.d * 4;
+  const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t(4) << 30) / per_split));
   // samples per dW GEMM: amortises the fp32 read-modify-write of dW over
   // several samples while keeping H_c^T and dZ^T within about 16 GB
   const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2;
@@ -71,7 +68,6 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   w.NP = NP;
   w.nvt = nvt;
   w.n_split = n_split;
-  w.k_split = k_split;
   w.dw_batch = dw_batch;
   w.KT = KT;
   if (ws) *ws = w;
@@ -144,6 +140,10 @@ static Dims dims_of(const bgpo_problem* p) { return Dims{p->B, p->L, p->d, p->V,
     if ((expr) != hipSuccess) return BGPO_ERR_HIP; \
   } while (0)
 
+static DxPlan dx_plan(const Dims& dm, const Workspace& ws, int grid) {
+  return DxPlan{dm.V / 64, (dm.d + 255) / 256, grid, (int)ws.n_split};
+}
+
 // forward part of one sample: mask .. l (and, with backward, g / loss / scale)
 static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer& tm, int grid,
                               int j, const uint16_t* hidden, const int32_t* targets,
@@ -156,7 +156,7 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
   BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, p->t_mode, p->seed,
                                p->seq_id_base, ws.idx, ws.row_tgt, ws.row_seq, ws.seg_off, ws.t24,
                                ws.meta, n_masked + j, dm.n_t, t_out ? t_out + j : nullptr, dm.n_t,
-                               (int)ws.NP, dm.V, first_in_batch ? 1 : 0, s));
+                               (int)ws.NP, dm.V, first_in_batch ? 1 : 0, dx_plan(dm, ws, grid), s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
   BGPO_TRY(launch_gather(hidden, ws, dm.d, s));
@@ -214,7 +214,8 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
   if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
   if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, prob->t_mode,
                           prob->seed, prob->seq_id_base, idx, nullptr, nullptr, nullptr, nullptr,
-                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, 1, (hipStream_t)stream) != hipSuccess)
+                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, 1, DxPlan{1, 1, 1, 1},
+                          (hipStream_t)stream) != hipSuccess)
     return BGPO_ERR_HIP;
   return BGPO_OK;
 }

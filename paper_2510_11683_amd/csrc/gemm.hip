@@ -36,7 +36,8 @@ struct GemmParams {
   int64_t ldb;
   int M, N, K;               // static extents
   int dyn_m, dyn_n, dyn_k;   // extents taken from the device sample metadata
-  int n_split;               // K split count (dX)
+  int dyn_split;             // K split taken from the metadata (dX)
+  int n_split;               // K split count
   int64_t k_split;           // K per split (multiple of BK)
   int group_m;              // tile order: bands of group_m M tiles, walking along N
                              // (1 = N tiles consecutive, tilesM = M tiles consecutive)
@@ -199,9 +200,15 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
   if (p.dyn_m) { M = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_n) { N = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_k) K = p.meta->col_end;    // batched dW: all samples' columns (multiple of 64)
+  int n_split = p.n_split;
+  int64_t k_split = p.k_split;
+  if (p.dyn_split) {
+    n_split = p.meta->dx_split;
+    k_split = (int64_t)p.meta->dx_kslab * BK;
+  }
   if (EPI == EPI_F32_ACCUM && K == 0) return;   // nothing to add
   const int tilesM = (M + BM - 1) / BM, tilesN = (N + BN - 1) / BN;
-  const int64_t total = (int64_t)tilesM * tilesN * p.n_split;
+  const int64_t total = (int64_t)tilesM * tilesN * n_split;
   const int G = gridDim.x;
   const int w = blockIdx.x;
   const int xcd_slot = (G % 8 == 0 && !p.plain_order) ? (w % 8) * (G / 8) + w / 8 : w;
@@ -225,8 +232,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
       nt = (int)(idx / gm);
     }
     const int m0 = mt * BM, n0 = nt * BN;
-    const int64_t kb = (int64_t)split * p.k_split;
-    const int64_t ke = min((int64_t)K, kb + p.k_split);
+    const int64_t kb = (int64_t)split * k_split;
+    const int64_t ke = min((int64_t)K, kb + k_split);
     const int nk = ke > kb ? (int)((ke - kb) / BK) : 0;
 
     // accumulator element (i, j, e) sits at
@@ -475,7 +482,7 @@ hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, 
   p.A = ws.dZ; p.lda = V;
   p.B = W; p.ldb = V;
   p.N = d; p.K = V; p.dyn_m = 1; p.meta = ws.meta;
-  p.n_split = (int)ws.n_split; p.k_split = ws.k_split;
+  p.dyn_split = 1;
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.NP * d;
   k_gemm<EPI_F32_STORE, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);

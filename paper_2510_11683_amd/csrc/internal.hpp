@@ -22,7 +22,18 @@ struct SampleMeta {
   int32_t n_rows_pad;  // N_j rounded up to kRowPad
   int32_t col_off;     // first column of this sample in H_c^T / dZ^T
   int32_t col_end;     // col_off + N_j rounded up to 64: K of the batched dW GEMM
-  int32_t pad[60];
+  int32_t dx_split;    // vocabulary splits of this sample's dX GEMM
+  int32_t dx_kslab;    // 64-wide vocabulary slabs per split
+  int32_t pad[58];
+};
+
+// What the mask kernel needs to choose the dX split of a sample (the split
+// count that best fills the persistent grid for the sample's row count).
+struct DxPlan {
+  int kslabs;      // V / 64
+  int col_tiles;   // d / 256
+  int grid;        // workgroups of the persistent GEMM grid
+  int s_max;       // splits the partial buffer holds
 };
 
 // Views into the caller's workspace.
@@ -46,7 +57,8 @@ struct Workspace {
   uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16 (first the fp16 exponentials)
   uint16_t* dZT;       // [V, KT]      the same, transposed; samples of a dW batch side by side
   float* dx_part;      // [S, NP, d]   split-vocabulary partial dX
-  int64_t P, NP, nvt, n_split, k_split;
+  int64_t P, NP, nvt;
+  int64_t n_split;     // capacity of dx_part in splits (the per-sample count is in meta)
   int64_t dw_batch;    // samples whose dW contributions share one GEMM
   int64_t KT;          // dw_batch * NP: leading dimension of H_c^T and dZ^T
 };
@@ -64,7 +76,7 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
                                SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
                                float* t_out, int t_stride, int row_cap, int V,
-                               int first_in_batch, hipStream_t s);
+                               int first_in_batch, const DxPlan& plan, hipStream_t s);
 hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s);
 hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool store_u,
                            hipStream_t s);

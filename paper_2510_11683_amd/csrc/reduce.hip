@@ -292,10 +292,11 @@ hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s) {
 __global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ part,
                                                    const int32_t* __restrict__ idx,
                                                    const SampleMeta* __restrict__ meta,
-                                                   float* __restrict__ dX, int d, int n_split,
+                                                   float* __restrict__ dX, int d,
                                                    int64_t split_stride) {
   const int r = blockIdx.x;
   if (r >= meta->n_rows) return;
+  const int n_split = meta->dx_split;
   const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
   if (c >= d) return;
   float4 acc = *reinterpret_cast<const float4*>(part + (int64_t)r * d + c);
@@ -311,7 +312,7 @@ __global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ par
 
 hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s) {
   dim3 grid((unsigned)ws.NP, (unsigned)((d / 4 + 255) / 256));
-  k_dx_reduce<<<grid, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta, dX, d, (int)ws.n_split, ws.NP * d);
+  k_dx_reduce<<<grid, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta, dX, d, ws.NP * d);
   return hipGetLastError();
 }
 

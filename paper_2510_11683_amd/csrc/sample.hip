@@ -36,13 +36,41 @@ struct MaskWalker {
   }
 };
 
+// Vocabulary split of the dX GEMM for a sample with row_tiles 256-row tiles:
+// the split count s minimising an estimate of the GEMM's time on the
+// persistent grid, in units of one 256x256x64 slab on one workgroup:
+//   ceil(tiles / grid) rounds x (slabs per split + ~10 for the tile's
+//   prologue and fp32 partial store) + ~0.65 per (split, row tile) for the
+//   reduction of the partials.
+// A fixed split leaves most of the last round idle for some row counts
+// (576 tiles on 256 workgroups use 2.25 of 3 rounds).
+__device__ void choose_dx_split(int row_tiles, const DxPlan& pl, int* split, int* kslab) {
+  // 32-bit divisions (tiles <= 4096 x 1024 x 16), 64-bit cost
+  int best_s = 1, best_ks = pl.kslabs;
+  uint64_t best = ~0ull;
+  for (int sp = 1; sp <= pl.s_max && row_tiles > 0; ++sp) {
+    const uint32_t ks = ((uint32_t)pl.kslabs + sp - 1) / sp;
+    const uint32_t se = ((uint32_t)pl.kslabs + ks - 1) / ks;   // splits actually used
+    const uint32_t tiles = (uint32_t)row_tiles * pl.col_tiles * se;
+    const uint32_t rounds = (tiles + pl.grid - 1) / pl.grid;
+    const uint64_t cost = (uint64_t)rounds * (ks + 10) * 20 + 13ull * se * row_tiles;
+    if (cost < best) {
+      best = cost;
+      best_s = (int)se;
+      best_ks = (int)ks;
+    }
+  }
+  *split = best_s;
+  *kslab = best_ks;
+}
+
 __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     const uint8_t* __restrict__ resp, const int32_t* __restrict__ targets, int B, int L, int n_t,
     int j, int t_mode, uint32_t k0, uint32_t k1, uint32_t seq_base, int32_t* __restrict__ idx,
     int32_t* __restrict__ row_tgt, int32_t* __restrict__ row_seq, int32_t* __restrict__ seg_off,
     uint32_t* __restrict__ t24_out, SampleMeta* __restrict__ meta, int32_t* __restrict__ nm_out,
     int nm_stride, float* __restrict__ t_out, int t_stride, int row_cap, int V,
-    int first_in_batch) {
+    int first_in_batch, DxPlan plan) {
   __shared__ uint32_t sT[kMaxB];
   __shared__ int32_t sSeg[kMaxB + 1];
   __shared__ int32_t sWave[kMaskThreads / 64];
@@ -119,6 +147,7 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
       const int off = first_in_batch ? 0 : meta->col_end;
       meta->col_off = off;
       meta->col_end = off + (total + 63) / 64 * 64;
+      choose_dx_split(total_pad / kRowPad, plan, &meta->dx_split, &meta->dx_kslab);
     }
   }
   if (row_cap > 0) {
@@ -135,12 +164,12 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
                                SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
                                float* t_out, int t_stride, int row_cap, int V,
-                               int first_in_batch, hipStream_t s) {
+                               int first_in_batch, const DxPlan& plan, hipStream_t s) {
   k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, t_mode,
                                             (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
                                             seq_base, idx, row_tgt, row_seq, seg_off, t24, meta,
                                             n_masked_out, nm_stride, t_out, t_stride, row_cap, V,
-                                            first_in_batch);
+                                            first_in_batch, plan);
   return hipGetLastError();
 }
 
