@@ -21,7 +21,7 @@ namespace bgpo {
 
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-constexpr int64_t kMaxDwBatch = 4;
+constexpr int64_t kMaxDwBatch = 8;
 
 size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   const int64_t P = (int64_t)dm.B * dm.L;
