@@ -39,6 +39,7 @@ from typing import Optional
 import numpy as np
 
 from . import philox
+from . import rmsnorm as _rms
 
 
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
@@ -192,6 +193,73 @@ def elbo_literal_f64(p: Problem, H, W, targets, resp_mask, adv,
                 dX[b, rows] += gx
                 dW += gw
     return Result(ell, g, nm, tt, loss, dX, dW, idx_all)
+
+
+@dataclasses.dataclass
+class SampleResult(Result):
+    dgamma: Optional[np.ndarray] = None   # [d] float64 (with the final norm)
+
+
+def elbo_per_sample(p: Problem, X, W, targets, resp_mask, adv, ell_old=None,
+                    loss_scale=1.0 / 8, backward=True, gamma=None, eps=1e-6,
+                    per_sample=True) -> SampleResult:
+    """Algorithm 1's inner step with the mask predictor's output taken per
+    sample: sample j (q = j - j_begin) has its own activations X[q] [B, L, d]
+    (per_sample) or all samples share X [B, L, d].  With ``gamma`` the head
+    input is the final RMSNorm of X (see ``oracle.rmsnorm``) and the gradients
+    are those w.r.t. the norm's input and weight.  dX has the layout of X.
+    Float64 inputs; literal loops, small sizes only."""
+    js = list(p.js)
+    X = np.asarray(X, dtype=np.float64)
+    Xq = (lambda q: X[q]) if per_sample else (lambda q: X)
+    Hq = (lambda q: _rms.rmsnorm(Xq(q), gamma, eps)[0]) if gamma is not None else Xq
+    ell = np.zeros((p.B, p.n_t))
+    g = np.zeros((p.B, p.n_t))
+    nm = np.zeros((p.B, p.n_t), dtype=np.int64)
+    tt = np.zeros((p.B, p.n_t))
+    dX = np.zeros_like(X) if backward else None
+    dW = np.zeros((p.d, p.V)) if backward else None
+    dgamma = np.zeros(p.d) if (backward and gamma is not None) else None
+    loss = 0.0
+    idx_all = {}
+    dbar = np.zeros(p.B)
+    masks = {j: sample_masks(p, resp_mask, j) for j in js}
+    if p.bound == BOUND_EXACT:
+        # mean_j d_j over all samples first (Eq. elbo_ratio)
+        if js != list(range(p.n_t)):
+            raise ValueError("the exact objective needs the full sample range")
+        for q, j in enumerate(js):
+            for b in range(p.B):
+                ell[b, j] = ell_of_mask(Hq(q)[b], W, targets[b], masks[j][2][b], masks[j][1][b])[0]
+        dbar = (ell - (0.0 if ell_old is None else np.asarray(ell_old, dtype=np.float64))).mean(axis=1)
+    for q, j in enumerate(js):
+        T, t, m, idx = masks[j]
+        idx_all[j] = idx
+        H = Hq(q)
+        dH = np.zeros_like(H) if backward else None
+        for b in range(p.B):
+            tt[b, j] = t[b]
+            ell[b, j], rows, lsm = ell_of_mask(H[b], W, targets[b], m[b], t[b])
+            nm[b, j] = rows.size
+            dj = 0.0 if ell_old is None else ell[b, j] - float(ell_old[b, j])
+            g[b, j], dg = bound_term(dj, float(adv[b]), p.n_t, p.bound, float(dbar[b]))
+            loss += -loss_scale * g[b, j]
+            if backward and rows.size:
+                s = loss_scale * dg / t[b]
+                gx, gw = backprop_rows(H[b, rows], W, np.asarray(targets[b])[rows], lsm, s)
+                dH[b, rows] += gx
+                dW += gw
+        if backward:
+            if gamma is not None:
+                gx, gg = _rms.rmsnorm_backward(Xq(q), gamma, eps, dH)
+                dgamma += gg
+            else:
+                gx = dH
+            if per_sample:
+                dX[q] += gx
+            else:
+                dX += gx
+    return SampleResult(ell, g, nm, tt, loss, dX, dW, idx_all, dgamma)
 
 
 def elbo_collapsed(p: Problem, hidden_bits, W_bits, targets, resp_mask, adv,

@@ -127,3 +127,73 @@ def test_pins_pass_unmutated():
 def test_mutation_is_caught(monkeypatch, name, fn):
     monkeypatch.setattr(elbo, name, fn)
     assert _any_pin_fails(), f"planted mistake {fn.__name__} in {name} passed every pin"
+
+
+# ---------------------------------------------------------------- final RMSNorm
+
+import test_oracle_rmsnorm as norm_pins
+from oracle import rmsnorm as _rmsnorm
+
+NORM_PINS = [
+    norm_pins.check_rmsnorm_forward,
+    norm_pins.check_rmsnorm_backward,
+    lambda: norm_pins.test_per_sample_gradients_match_autograd(True),
+]
+
+
+def mut_norm_no_eps(x, gamma, eps):
+    x = np.asarray(x, dtype=np.float64)
+    r = 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True))
+    return x * r * gamma, r
+
+
+def mut_norm_sum_not_mean(x, gamma, eps):
+    x = np.asarray(x, dtype=np.float64)
+    r = 1.0 / np.sqrt(np.sum(x * x, axis=-1, keepdims=True) + eps)
+    return x * r * gamma, r
+
+
+def mut_norm_bwd_no_projection(x, gamma, eps, dh):
+    _, r = _rmsnorm.rmsnorm(x, gamma, eps)
+    return r * gamma * dh, np.sum((dh * x * r).reshape(-1, x.shape[-1]), axis=0)
+
+
+def mut_norm_bwd_r_squared(x, gamma, eps, dh):
+    d = x.shape[-1]
+    _, r = _rmsnorm.rmsnorm(x, gamma, eps)
+    proj = np.sum(gamma * dh * x, axis=-1, keepdims=True)
+    return r * gamma * dh - (r ** 2 / d) * x * proj, np.sum((dh * x * r).reshape(-1, d), axis=0)
+
+
+def mut_norm_dgamma_without_r(x, gamma, eps, dh, _f=_rmsnorm.rmsnorm_backward):
+    dx, _ = _f(x, gamma, eps, dh)
+    return dx, np.sum((dh * x).reshape(-1, x.shape[-1]), axis=0)
+
+
+NORM_MUTATIONS = [
+    ("rmsnorm", mut_norm_no_eps),
+    ("rmsnorm", mut_norm_sum_not_mean),
+    ("rmsnorm_backward", mut_norm_bwd_no_projection),
+    ("rmsnorm_backward", mut_norm_bwd_r_squared),
+    ("rmsnorm_backward", mut_norm_dgamma_without_r),
+]
+
+
+def _any_norm_pin_fails():
+    for pin in NORM_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin()
+        except (AssertionError, ValueError, IndexError, FloatingPointError):
+            return True
+    return False
+
+
+def test_norm_pins_pass_unmutated():
+    assert not _any_norm_pin_fails()
+
+
+@pytest.mark.parametrize("name,fn", NORM_MUTATIONS, ids=[f.__name__ for _, f in NORM_MUTATIONS])
+def test_norm_mutation_is_caught(monkeypatch, name, fn):
+    monkeypatch.setattr(_rmsnorm, name, fn)
+    assert _any_norm_pin_fails(), f"planted mistake {fn.__name__} in {name} passed every pin"
