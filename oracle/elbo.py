@@ -202,17 +202,24 @@ class SampleResult(Result):
 
 def elbo_per_sample(p: Problem, X, W, targets, resp_mask, adv, ell_old=None,
                     loss_scale=1.0 / 8, backward=True, gamma=None, eps=1e-6,
-                    per_sample=True) -> SampleResult:
+                    per_sample=True, head_bf16=False) -> SampleResult:
     """Algorithm 1's inner step with the mask predictor's output taken per
     sample: sample j (q = j - j_begin) has its own activations X[q] [B, L, d]
     (per_sample) or all samples share X [B, L, d].  With ``gamma`` the head
     input is the final RMSNorm of X (see ``oracle.rmsnorm``) and the gradients
-    are those w.r.t. the norm's input and weight.  dX has the layout of X.
-    Float64 inputs; literal loops, small sizes only."""
+    are those w.r.t. the norm's input and weight; ``head_bf16`` rounds the
+    norm's output to bfloat16 before the head (the head's operand precision),
+    the rounding passed through unchanged in the backward.  dX has the layout
+    of X.  Float64 inputs; literal loops, small sizes only."""
     js = list(p.js)
     X = np.asarray(X, dtype=np.float64)
     Xq = (lambda q: X[q]) if per_sample else (lambda q: X)
-    Hq = (lambda q: _rms.rmsnorm(Xq(q), gamma, eps)[0]) if gamma is not None else Xq
+    if gamma is None:
+        Hq = Xq
+    elif head_bf16:
+        Hq = lambda q: _rms.round_to_bf16(_rms.rmsnorm(Xq(q), gamma, eps)[0])
+    else:
+        Hq = lambda q: _rms.rmsnorm(Xq(q), gamma, eps)[0]
     ell = np.zeros((p.B, p.n_t))
     g = np.zeros((p.B, p.n_t))
     nm = np.zeros((p.B, p.n_t), dtype=np.int64)
@@ -264,7 +271,7 @@ def elbo_per_sample(p: Problem, X, W, targets, resp_mask, adv, ell_old=None,
 
 def elbo_collapsed(p: Problem, hidden_bits, W_bits, targets, resp_mask, adv,
                    ell_old=None, loss_scale=1.0 / 8, backward=True,
-                   dx_rows=None, dw_cols=None, row_chunk=256) -> Result:
+                   dx_rows=None, dw_cols=None, row_chunk=256, hidden_f64=None) -> Result:
     """Same result for hidden states shared by all samples (the head-only slice).
 
     The log-softmax is computed once per response position; l_{b,j} is then the
@@ -272,8 +279,11 @@ def elbo_collapsed(p: Problem, hidden_bits, W_bits, targets, resp_mask, adv,
     backward is one pass with per-position weight w_{b,i} = sum_j s_{b,j} m_{b,j,i}.
     ``dx_rows`` (flat positions) and ``dw_cols`` (vocabulary ids) restrict the
     gradients to a subset, which is what makes full-size problems tractable:
-    dX is returned as [len(dx_rows), d] and dW as [d, len(dw_cols)]."""
-    H = bf16_to_f64(hidden_bits).reshape(p.B * p.L, p.d)
+    dX is returned as [len(dx_rows), d] and dW as [d, len(dw_cols)].
+    ``hidden_f64`` [B, L, d] replaces the bf16 hidden states (e.g. the float64
+    output of the final RMSNorm); dX is then the gradient w.r.t. it."""
+    H = (bf16_to_f64(hidden_bits) if hidden_f64 is None else np.asarray(hidden_f64, dtype=np.float64)
+         ).reshape(p.B * p.L, p.d)
     tg = targets.reshape(-1).astype(np.int64)
     resp = resp_mask.reshape(-1) != 0
 

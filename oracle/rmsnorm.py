@@ -7,6 +7,10 @@ TEST INFRASTRUCTURE: part of the oracle; see ``oracle/__init__.py``.
   r      = (mean_i x_i^2 + eps)^(-1/2)          per row
   h_i    = gamma_i x_i r
 
+The LM head is a bf16 product, so its input is the norm's output rounded to
+bfloat16 (``round_to_bf16``: 8 significant bits, round to nearest, ties to
+even); the rounding is passed through unchanged in the backward.
+
 Backward, from the definition (dr/dx_k = -r^3 x_k / d):
 
   dx_k     = r gamma_k dh_k - (r^3 / d) x_k sum_i gamma_i dh_i x_i
@@ -35,3 +39,11 @@ def rmsnorm_backward(x: np.ndarray, gamma: np.ndarray, eps: float, dh: np.ndarra
     dx = r * gamma * dh - (r ** 3 / d) * x * proj
     dgamma = np.sum((dh * x * r).reshape(-1, d), axis=0)
     return dx, dgamma
+
+
+def round_to_bf16(v: np.ndarray) -> np.ndarray:
+    """Nearest bfloat16 value (8 significant bits, ties to even) of float64 v,
+    returned as float64 (normal range; the values here never leave it)."""
+    v = np.asarray(v, dtype=np.float64)
+    m, e = np.frexp(v)                       # v = m 2^e, |m| in [0.5, 1)
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)

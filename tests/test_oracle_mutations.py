@@ -135,6 +135,7 @@ import test_oracle_rmsnorm as norm_pins
 from oracle import rmsnorm as _rmsnorm
 
 NORM_PINS = [
+    norm_pins.check_round_to_bf16,
     norm_pins.check_rmsnorm_forward,
     norm_pins.check_rmsnorm_backward,
     lambda: norm_pins.test_per_sample_gradients_match_autograd(True),
@@ -170,7 +171,21 @@ def mut_norm_dgamma_without_r(x, gamma, eps, dh, _f=_rmsnorm.rmsnorm_backward):
     return dx, np.sum((dh * x).reshape(-1, x.shape[-1]), axis=0)
 
 
+def mut_round_truncates(v):
+    v = np.asarray(v, dtype=np.float64)
+    m, e = np.frexp(v)
+    return np.ldexp(np.trunc(m * 256.0) / 256.0, e)
+
+
+def mut_round_half_away(v):
+    v = np.asarray(v, dtype=np.float64)
+    m, e = np.frexp(v)
+    return np.ldexp(np.sign(m) * np.floor(np.abs(m) * 256.0 + 0.5) / 256.0, e)
+
+
 NORM_MUTATIONS = [
+    ("round_to_bf16", mut_round_truncates),
+    ("round_to_bf16", mut_round_half_away),
     ("rmsnorm", mut_norm_no_eps),
     ("rmsnorm", mut_norm_sum_not_mean),
     ("rmsnorm_backward", mut_norm_bwd_no_projection),

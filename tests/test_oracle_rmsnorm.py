@@ -53,6 +53,23 @@ def check_rmsnorm_backward(fn=None):
         assert abs(fd - dx[r, c]) <= 1e-6 * max(1.0, abs(fd))
 
 
+def check_round_to_bf16(fn=None):
+    """Against torch's float32 -> bfloat16 conversion (round to nearest even) on
+    float32-representable values, plus exact ties."""
+    fn = fn or rmsnorm.round_to_bf16
+    rng = np.random.default_rng(13)
+    v = (rng.standard_normal(20000) * np.exp(rng.uniform(-20, 20, 20000))).astype(np.float32)
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(fn(v.astype(np.float64)), ref)
+    # ties: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7 -> even (1); 1 + 3 * 2^-8 -> 1 + 2^-6
+    t = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(1 + 2.0 ** -8), 3 * 2.0 ** -9])
+    assert np.array_equal(fn(t), [1.0, 1 + 2.0 ** -6, -1.0, 3 * 2.0 ** -9])
+
+
+def test_round_to_bf16_matches_torch_and_ties():
+    check_round_to_bf16()
+
+
 def test_rmsnorm_forward_matches_torch():
     check_rmsnorm_forward()
 
