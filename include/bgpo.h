@@ -47,6 +47,10 @@
  *     crosses the ABI.  Entry points keep no mutable global state; calls on
  *     different streams must not share a workspace.
  *   - hidden and W_head are bfloat16 bit patterns (uint16), row-major.
+ *   - The head input of sample j may be its own tensor (sample_stride > 0):
+ *     the mask predictor's output depends on the noised sequence y_t of each
+ *     sample (p_theta(y | y_t, x), Eq. per_step_loss), and the dX of sample j
+ *     is then the gradient that its own backward pass consumes.
  *   - Supported shapes: 1 <= B <= 4096, L >= 1, B*L <= 2^20, d % 64 == 0,
  *     V % 64 == 0, 64 <= d <= 65536, 64 <= V <= 2^20, n_t >= 1,
  *     0 <= j_begin, j_count >= 0, j_begin + j_count <= n_t.  Targets must lie
@@ -107,19 +111,26 @@ typedef struct bgpo_problem {
   uint64_t seed;        /* Philox key */
   uint32_t seq_id_base; /* global id of response b = 0 (seq = seq_id_base + b) */
   int32_t bound;        /* BGPO_BOUND_*; 0 (the paper's objective) for plain callers */
+  int64_t sample_stride;/* elements between the head inputs (and the dX outputs) of
+                           consecutive samples of the call's range: sample j reads
+                           hidden + (j - j_begin) * sample_stride and accumulates into
+                           dX + (j - j_begin) * sample_stride.  0 = one hidden[B, L, d]
+                           shared by every sample and one dX.  A multiple of 8, >= 0. */
+  float norm_eps;       /* epsilon of the final RMSNorm (the _rmsnorm entry points) */
+  int32_t reserved;     /* must be 0 */
 } bgpo_problem;
 
 /* Kernel classes reported by the optional timing record. */
 enum {
   BGPO_K_TRANSPOSE_W = 0,  /* W[d,V] -> W^T[V,d] staging, once per call */
   BGPO_K_MASK = 1,         /* Philox t and masks + stable compaction */
-  BGPO_K_GATHER = 2,       /* masked hidden rows -> H_c and H_c^T */
+  BGPO_K_GATHER = 2,       /* masked hidden rows (RMSNorm applied) -> H_c and H_c^T */
   BGPO_K_FWD = 3,          /* fused LM-head GEMM + online log-sum-exp partials (in the
                               backward it also stores the exponentials) */
   BGPO_K_ELL = 4,          /* partial combine, log p, l, d, g, loss, gradient scale */
   BGPO_K_SOFTMAX_GRAD = 5, /* stored exponentials -> dZ = s (softmax - onehot), both layouts */
   BGPO_K_DX = 6,           /* dZ W^T split over the vocabulary */
-  BGPO_K_DX_REDUCE = 7,    /* split reduction + scatter-add into dX */
+  BGPO_K_DX_REDUCE = 7,    /* split reduction + scatter-add into dX (+ RMSNorm backward) */
   BGPO_K_DW = 8,           /* H_c^T dZ accumulated into dW */
   BGPO_K_COUNT = 9
 };
@@ -197,6 +208,33 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
                              int32_t* n_masked, float* t_out, int32_t* status_flags,
                              void* workspace, size_t ws_bytes, void* stream,
                              bgpo_timing* prof);
+
+/* The same two calls with the final RMSNorm of the mask predictor fused in
+ * front of the LM head: the head input of a position is
+ *     h = norm_weight * x / sqrt(mean_i x_i^2 + norm_eps)
+ * with x the pre-norm activations (bf16 [B, L, d] per sample, laid out as
+ * `hidden` above, sample_stride included) and norm_weight fp32 [d]
+ * (16-byte aligned).  h is formed in fp32 for the masked positions only and
+ * rounded once to bf16 before the head GEMMs.  The backward returns the
+ * gradients w.r.t. the norm's input and weight:
+ *     dx            float [B, L, d] (+ sample_stride)  += d loss / d x
+ *     d_norm_weight float [d]                          += d loss / d norm_weight
+ * (dgamma summed over positions in a fixed order: deterministic).  Other
+ * arguments, outputs and errors as in bgpo_elbo_fwd / bgpo_elbo_bwd_accumulate;
+ * NULL norm_weight or d_norm_weight returns BGPO_ERR_INVALID_ARG. */
+int bgpo_elbo_fwd_rmsnorm(const bgpo_problem* prob, const uint16_t* x, const float* norm_weight,
+                          const uint16_t* W_head, const int32_t* targets,
+                          const uint8_t* resp_mask, double* ell, int32_t* n_masked, float* t_out,
+                          void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof);
+
+int bgpo_elbo_bwd_accumulate_rmsnorm(const bgpo_problem* prob, const uint16_t* x,
+                                     const float* norm_weight, const uint16_t* W_head,
+                                     const int32_t* targets, const uint8_t* resp_mask,
+                                     const float* adv, const double* ell_old, double loss_scale,
+                                     float* dx, float* d_norm_weight, float* dW, double* ell,
+                                     double* g, double* loss, int32_t* n_masked, float* t_out,
+                                     int32_t* status_flags, void* workspace, size_t ws_bytes,
+                                     void* stream, bgpo_timing* prof);
 
 #ifdef __cplusplus
 }

@@ -35,7 +35,8 @@ class _Problem(ctypes.Structure):
                 ("V", ctypes.c_int32), ("n_t", ctypes.c_int32), ("j_begin", ctypes.c_int32),
                 ("j_count", ctypes.c_int32), ("t_mode", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("seq_id_base", ctypes.c_uint32),
-                ("bound", ctypes.c_int32)]
+                ("bound", ctypes.c_int32), ("sample_stride", ctypes.c_int64),
+                ("norm_eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
 
 
 class Timing(ctypes.Structure):
@@ -61,10 +62,16 @@ def _load():
     lib.bgpo_elbo_fwd.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, P(Timing)]
     lib.bgpo_elbo_bwd_accumulate.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, ctypes.c_double,
                                              vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, P(Timing)]
+    lib.bgpo_elbo_fwd_rmsnorm.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp,
+                                          P(Timing)]
+    lib.bgpo_elbo_bwd_accumulate_rmsnorm.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, vp,
+                                                     ctypes.c_double, vp, vp, vp, vp, vp, vp, vp,
+                                                     vp, vp, vp, sz, vp, P(Timing)]
     lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
     lib.bgpo_test_gemm_variant.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, vp]
     for f in ("bgpo_workspace_size", "bgpo_sample_masks", "bgpo_elbo_fwd",
-              "bgpo_elbo_bwd_accumulate", "bgpo_test_gemm_nt", "bgpo_test_gemm_variant"):
+              "bgpo_elbo_bwd_accumulate", "bgpo_elbo_fwd_rmsnorm",
+              "bgpo_elbo_bwd_accumulate_rmsnorm", "bgpo_test_gemm_nt", "bgpo_test_gemm_variant"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -97,11 +104,17 @@ class Problem:
     seq_id_base: int = 0
     t_mode: int = BGPO_T_IID
     bound: int = BGPO_BOUND_PAPER
+    sample_stride: int = 0        # elements between per-sample head inputs / dX; 0 = shared
+    norm_eps: float = 1e-6        # final RMSNorm epsilon (the _rmsnorm calls)
+
+    @property
+    def jc(self) -> int:
+        return self.n_t - self.j_begin if self.j_count is None else self.j_count
 
     def c(self) -> _Problem:
-        jc = self.n_t - self.j_begin if self.j_count is None else self.j_count
-        return _Problem(self.B, self.L, self.d, self.V, self.n_t, self.j_begin, jc, self.t_mode,
-                        self.seed & 0xFFFFFFFFFFFFFFFF, self.seq_id_base & 0xFFFFFFFF, self.bound)
+        return _Problem(self.B, self.L, self.d, self.V, self.n_t, self.j_begin, self.jc, self.t_mode,
+                        self.seed & 0xFFFFFFFFFFFFFFFF, self.seq_id_base & 0xFFFFFFFF, self.bound,
+                        self.sample_stride, self.norm_eps, 0)
 
 
 def _ptr(t: Optional[torch.Tensor], name: str, dtypes=None, shape=None, allow_none=False):
@@ -153,11 +166,23 @@ def bgpo_sample_masks(prob: Problem, resp_mask, j: int, idx, n_masked, t_out=Non
                                   _stream(stream)), "bgpo_sample_masks")
 
 
+def _act_shape(prob: Problem):
+    """Shape of the head input (and dX): [B, L, d], or [j_count, B, L, d] with a
+    sample stride of exactly B*L*d elements (other strides: pass a flat tensor
+    through the C ABI directly)."""
+    B, L, d = prob.B, prob.L, prob.d
+    if prob.sample_stride == 0:
+        return (B, L, d)
+    if prob.sample_stride != B * L * d:
+        raise ValueError("the binding supports sample_stride 0 or B*L*d")
+    return (prob.jc, B, L, d)
+
+
 def bgpo_elbo_fwd(prob: Problem, hidden, W_head, targets, resp_mask, ell, n_masked, t_out,
                   workspace, stream=None, timing: Optional[Timing] = None):
     B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
     _check(_lib.bgpo_elbo_fwd(
-        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, (B, L, d)),
+        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, _act_shape(prob)),
         _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
         _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
         _ptr(ell, "ell", (torch.float64,), (B, nt)),
@@ -173,13 +198,13 @@ def bgpo_elbo_bwd_accumulate(prob: Problem, hidden, W_head, targets, resp_mask, 
                              timing: Optional[Timing] = None):
     B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
     _check(_lib.bgpo_elbo_bwd_accumulate(
-        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, (B, L, d)),
+        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, _act_shape(prob)),
         _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
         _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
         _ptr(adv, "adv", (torch.float32,), (B,)),
         _ptr(ell_old, "ell_old", (torch.float64,), (B, nt), allow_none=True),
         float(loss_scale),
-        _ptr(dX, "dX", (torch.float32,), (B, L, d)), _ptr(dW, "dW", (torch.float32,), (d, V)),
+        _ptr(dX, "dX", (torch.float32,), _act_shape(prob)), _ptr(dW, "dW", (torch.float32,), (d, V)),
         _ptr(ell, "ell", (torch.float64,), (B, nt)), _ptr(g, "g", (torch.float64,), (B, nt)),
         _ptr(loss, "loss", (torch.float64,), (1,)),
         _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
@@ -187,6 +212,47 @@ def bgpo_elbo_bwd_accumulate(prob: Problem, hidden, W_head, targets, resp_mask, 
         _ptr(status_flags, "status_flags", (torch.int32,), (1,), allow_none=True),
         _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(), _stream(stream),
         ctypes.byref(timing) if timing is not None else None), "bgpo_elbo_bwd_accumulate")
+
+
+def bgpo_elbo_fwd_rmsnorm(prob: Problem, x, norm_weight, W_head, targets, resp_mask, ell,
+                          n_masked, t_out, workspace, stream=None,
+                          timing: Optional[Timing] = None):
+    B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
+    _check(_lib.bgpo_elbo_fwd_rmsnorm(
+        ctypes.byref(prob.c()), _ptr(x, "x", _BF16, _act_shape(prob)),
+        _ptr(norm_weight, "norm_weight", (torch.float32,), (d,)),
+        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
+        _ptr(ell, "ell", (torch.float64,), (B, nt)),
+        _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
+        _ptr(t_out, "t_out", (torch.float32,), (B, nt), allow_none=True),
+        _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(), _stream(stream),
+        ctypes.byref(timing) if timing is not None else None), "bgpo_elbo_fwd_rmsnorm")
+
+
+def bgpo_elbo_bwd_accumulate_rmsnorm(prob: Problem, x, norm_weight, W_head, targets, resp_mask,
+                                     adv, ell_old, loss_scale: float, dx, d_norm_weight, dW, ell,
+                                     g, loss, n_masked, t_out, status_flags, workspace,
+                                     stream=None, timing: Optional[Timing] = None):
+    B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
+    _check(_lib.bgpo_elbo_bwd_accumulate_rmsnorm(
+        ctypes.byref(prob.c()), _ptr(x, "x", _BF16, _act_shape(prob)),
+        _ptr(norm_weight, "norm_weight", (torch.float32,), (d,)),
+        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
+        _ptr(adv, "adv", (torch.float32,), (B,)),
+        _ptr(ell_old, "ell_old", (torch.float64,), (B, nt), allow_none=True),
+        float(loss_scale),
+        _ptr(dx, "dx", (torch.float32,), _act_shape(prob)),
+        _ptr(d_norm_weight, "d_norm_weight", (torch.float32,), (d,)),
+        _ptr(dW, "dW", (torch.float32,), (d, V)),
+        _ptr(ell, "ell", (torch.float64,), (B, nt)), _ptr(g, "g", (torch.float64,), (B, nt)),
+        _ptr(loss, "loss", (torch.float64,), (1,)),
+        _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
+        _ptr(t_out, "t_out", (torch.float32,), (B, nt), allow_none=True),
+        _ptr(status_flags, "status_flags", (torch.int32,), (1,), allow_none=True),
+        _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(), _stream(stream),
+        ctypes.byref(timing) if timing is not None else None), "bgpo_elbo_bwd_accumulate_rmsnorm")
 
 
 def bgpo_test_gemm_nt(A, B, C, stream=None):

@@ -56,6 +56,8 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   w.lp = static_cast<float*>(take(NP * 4));
   w.row_scale = static_cast<float*>(take(NP * 4));
   w.dbar = static_cast<double*>(take(dm.B * 8));
+  w.inv_rms = static_cast<float*>(take(NP * 4));
+  w.gpart = static_cast<float*>(take((NP / 256) * dm.d * 4));
   w.part_m = static_cast<float*>(take(nvt * NP * 4));
   w.part_s = static_cast<float*>(take(nvt * NP * 4));
   w.Hc = static_cast<uint16_t*>(take(NP * dm.d * 2));
@@ -125,7 +127,9 @@ static int check_problem(const bgpo_problem* p) {
   if (!p) return BGPO_ERR_INVALID_ARG;
   if (p->B < 1 || p->L < 1 || p->n_t < 1 || p->j_begin < 0 || p->j_count < 0 ||
       (int64_t)p->j_begin + p->j_count > p->n_t || (p->t_mode != BGPO_T_IID && p->t_mode != BGPO_T_STRATIFIED) ||
-      p->bound < BGPO_BOUND_PAPER || p->bound > BGPO_BOUND_EXACT || p->d < 1 || p->V < 1)
+      p->bound < BGPO_BOUND_PAPER || p->bound > BGPO_BOUND_EXACT || p->d < 1 || p->V < 1 ||
+      p->sample_stride < 0 || p->sample_stride % 8 || !isfinite(p->norm_eps) || p->norm_eps < 0.f ||
+      p->reserved != 0)
     return BGPO_ERR_INVALID_ARG;
   if (p->B > 4096 || (int64_t)p->B * p->L > (1 << 20) || p->d % 64 || p->V % 64 || p->d < 64 ||
       p->d > 65536 || p->V < 64 || p->V > (1 << 20))
@@ -144,9 +148,21 @@ static DxPlan dx_plan(const Dims& dm, const Workspace& ws, int grid) {
   return DxPlan{dm.V / 64, (dm.d + 255) / 256, grid, (int)ws.n_split};
 }
 
+// The head input of the samples of a call: sample j reads x + (j - j_begin) *
+// stride (stride 0: one tensor shared by all samples), normalised by the
+// final RMSNorm when gamma is given.
+struct Act {
+  const uint16_t* x;
+  const float* gamma;
+  float eps;
+  int64_t stride;
+  int j0;
+  const uint16_t* at(int j) const { return x + (int64_t)(j - j0) * stride; }
+};
+
 // forward part of one sample: mask .. l (and, with backward, g / loss / scale)
 static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer& tm, int grid,
-                              int j, const uint16_t* hidden, const int32_t* targets,
+                              int j, const Act& act, const int32_t* targets,
                               const uint8_t* resp, const float* adv, const double* ell_old,
                               double loss_scale, double* ell, double* g, double* loss,
                               int32_t* n_masked, float* t_out, int32_t* flags, bool backward,
@@ -159,7 +175,8 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
                                (int)ws.NP, dm.V, first_in_batch ? 1 : 0, dx_plan(dm, ws, grid), s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
-  BGPO_TRY(launch_gather(hidden, ws, dm.d, s));
+  if (act.gamma) BGPO_TRY(launch_row_rms(act.at(j), ws, dm.d, act.eps, s));
+  BGPO_TRY(launch_gather(act.at(j), act.gamma, ws, dm.d, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_FWD));
   BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, backward, s));
@@ -186,7 +203,7 @@ using namespace bgpo;
 
 extern "C" {
 
-int bgpo_version(void) { return (1 << 16) | 0; }
+int bgpo_version(void) { return (2 << 16) | 0; }
 
 const char* bgpo_status_string(int status) {
   switch (status) {
@@ -228,14 +245,19 @@ static int check_workspace(const bgpo_problem* prob, void* workspace, size_t ws_
   return BGPO_OK;
 }
 
-int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16_t* W_head,
-                  const int32_t* targets, const uint8_t* resp_mask, double* ell,
-                  int32_t* n_masked, float* t_out, void* workspace, size_t ws_bytes, void* stream,
-                  bgpo_timing* prof) {
+}  // extern "C"
+
+namespace bgpo {
+
+static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
+                         const int32_t* targets, const uint8_t* resp_mask, double* ell,
+                         int32_t* n_masked, float* t_out, void* workspace, size_t ws_bytes,
+                         void* stream, bgpo_timing* prof) {
   int st = check_problem(prob);
   if (st != BGPO_OK) return st;
-  if (!hidden || !W_head || !targets || !resp_mask || !ell || !n_masked) return BGPO_ERR_INVALID_ARG;
-  if (!aligned16(hidden) || !aligned16(W_head)) return BGPO_ERR_INVALID_ARG;
+  if (!act.x || !W_head || !targets || !resp_mask || !ell || !n_masked) return BGPO_ERR_INVALID_ARG;
+  if (!aligned16(act.x) || !aligned16(W_head) || (act.gamma && !aligned16(act.gamma)))
+    return BGPO_ERR_INVALID_ARG;
   if ((st = check_workspace(prob, workspace, ws_bytes)) != BGPO_OK) return st;
   if (prob->j_count == 0) return BGPO_OK;
   hipStream_t s = (hipStream_t)stream;
@@ -248,7 +270,7 @@ int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16
   BGPO_TRY(launch_transpose_w(W_head, ws.WT, prob->d, prob->V, s));
   BGPO_TRY(tm.end());
   for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
-    st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, nullptr, nullptr, 0.0,
+    st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, nullptr, nullptr, 0.0,
                             ell, nullptr, nullptr, n_masked, t_out, nullptr, false, true, nullptr,
                             s);
     if (st != BGPO_OK) return st;
@@ -257,18 +279,20 @@ int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16
   return BGPO_OK;
 }
 
-int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
-                             const uint16_t* W_head, const int32_t* targets,
-                             const uint8_t* resp_mask, const float* adv, const double* ell_old,
-                             double loss_scale, float* dX, float* dW, double* ell, double* g,
-                             double* loss, int32_t* n_masked, float* t_out, int32_t* status_flags,
-                             void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof) {
+// dX (and dgamma with the norm) are per sample at dX + (j - j_begin) * stride.
+static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
+                         const int32_t* targets, const uint8_t* resp_mask, const float* adv,
+                         const double* ell_old, double loss_scale, float* dX, float* dgamma,
+                         float* dW, double* ell, double* g, double* loss, int32_t* n_masked,
+                         float* t_out, int32_t* status_flags, void* workspace, size_t ws_bytes,
+                         void* stream, bgpo_timing* prof) {
   int st = check_problem(prob);
   if (st != BGPO_OK) return st;
-  if (!hidden || !W_head || !targets || !resp_mask || !adv || !dX || !dW || !ell || !g || !loss ||
-      !n_masked || !isfinite(loss_scale))
+  if (!act.x || !W_head || !targets || !resp_mask || !adv || !dX || !dW || !ell || !g || !loss ||
+      !n_masked || !isfinite(loss_scale) || (act.gamma && !dgamma))
     return BGPO_ERR_INVALID_ARG;
-  if (!aligned16(hidden) || !aligned16(W_head) || !aligned16(dX) || !aligned16(dW))
+  if (!aligned16(act.x) || !aligned16(W_head) || !aligned16(dX) || !aligned16(dW) ||
+      (act.gamma && !aligned16(act.gamma)))
     return BGPO_ERR_INVALID_ARG;
   if ((st = check_workspace(prob, workspace, ws_bytes)) != BGPO_OK) return st;
   const bool exact = prob->bound == BGPO_BOUND_EXACT;
@@ -289,7 +313,7 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
   const double* dbar = nullptr;
   if (exact && ell_old) {
     for (int j = 0; j < prob->n_t; ++j) {
-      st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, nullptr, nullptr,
+      st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, nullptr, nullptr,
                               0.0, ell, nullptr, nullptr, n_masked, t_out, status_flags, false,
                               true, nullptr, s);
       if (st != BGPO_OK) return st;
@@ -303,7 +327,7 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
   for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.dw_batch) {
     const int j1 = std::min<int>(j_end, j0 + (int)ws.dw_batch);
     for (int j = j0; j < j1; ++j) {
-      st = run_forward_sample(prob, ws, tm, grid, j, hidden, targets, resp_mask, adv, ell_old,
+      st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, adv, ell_old,
                               loss_scale, ell, g, loss, n_masked, t_out, status_flags, true,
                               j == j0, dbar, s);
       if (st != BGPO_OK) return st;
@@ -314,7 +338,11 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
       BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
       BGPO_TRY(tm.end());
       BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
-      BGPO_TRY(launch_dx_reduce(ws, dX, dm.d, s));
+      float* dXj = dX + (int64_t)(j - prob->j_begin) * act.stride;
+      if (act.gamma)
+        BGPO_TRY(launch_dx_reduce_rmsnorm(ws, act.at(j), act.gamma, dXj, dgamma, dm.d, s));
+      else
+        BGPO_TRY(launch_dx_reduce(ws, dXj, dm.d, s));
       BGPO_TRY(tm.end());
     }
     // one dW GEMM for the batch: K runs over the batch's samples side by side
@@ -324,6 +352,56 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
   }
   BGPO_TRY(tm.finish());
   return BGPO_OK;
+}
+
+static Act act_of(const bgpo_problem* p, const uint16_t* x, const float* gamma) {
+  return Act{x, gamma, p ? p->norm_eps : 0.f, p ? p->sample_stride : 0, p ? p->j_begin : 0};
+}
+
+}  // namespace bgpo
+
+extern "C" {
+
+int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16_t* W_head,
+                  const int32_t* targets, const uint8_t* resp_mask, double* ell,
+                  int32_t* n_masked, float* t_out, void* workspace, size_t ws_bytes, void* stream,
+                  bgpo_timing* prof) {
+  return elbo_fwd_impl(prob, act_of(prob, hidden, nullptr), W_head, targets, resp_mask, ell,
+                       n_masked, t_out, workspace, ws_bytes, stream, prof);
+}
+
+int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
+                             const uint16_t* W_head, const int32_t* targets,
+                             const uint8_t* resp_mask, const float* adv, const double* ell_old,
+                             double loss_scale, float* dX, float* dW, double* ell, double* g,
+                             double* loss, int32_t* n_masked, float* t_out, int32_t* status_flags,
+                             void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof) {
+  return elbo_bwd_impl(prob, act_of(prob, hidden, nullptr), W_head, targets, resp_mask, adv,
+                       ell_old, loss_scale, dX, nullptr, dW, ell, g, loss, n_masked, t_out,
+                       status_flags, workspace, ws_bytes, stream, prof);
+}
+
+int bgpo_elbo_fwd_rmsnorm(const bgpo_problem* prob, const uint16_t* x, const float* norm_weight,
+                          const uint16_t* W_head, const int32_t* targets,
+                          const uint8_t* resp_mask, double* ell, int32_t* n_masked, float* t_out,
+                          void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof) {
+  if (!norm_weight) return BGPO_ERR_INVALID_ARG;
+  return elbo_fwd_impl(prob, act_of(prob, x, norm_weight), W_head, targets, resp_mask, ell,
+                       n_masked, t_out, workspace, ws_bytes, stream, prof);
+}
+
+int bgpo_elbo_bwd_accumulate_rmsnorm(const bgpo_problem* prob, const uint16_t* x,
+                                     const float* norm_weight, const uint16_t* W_head,
+                                     const int32_t* targets, const uint8_t* resp_mask,
+                                     const float* adv, const double* ell_old, double loss_scale,
+                                     float* dx, float* d_norm_weight, float* dW, double* ell,
+                                     double* g, double* loss, int32_t* n_masked, float* t_out,
+                                     int32_t* status_flags, void* workspace, size_t ws_bytes,
+                                     void* stream, bgpo_timing* prof) {
+  if (!norm_weight || !d_norm_weight) return BGPO_ERR_INVALID_ARG;
+  return elbo_bwd_impl(prob, act_of(prob, x, norm_weight), W_head, targets, resp_mask, adv,
+                       ell_old, loss_scale, dx, d_norm_weight, dW, ell, g, loss, n_masked, t_out,
+                       status_flags, workspace, ws_bytes, stream, prof);
 }
 
 }  // extern "C"

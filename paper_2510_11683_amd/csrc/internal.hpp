@@ -54,6 +54,8 @@ struct Workspace {
   float* lp;           // [NP]         log p of the target
   float* row_scale;    // [NP]         gradient scale s of each row (0 for padding)
   double* dbar;        // [B]          mean log-ratio over all samples (exact objective)
+  float* inv_rms;      // [NP]         final-RMSNorm 1/rms of each compacted row
+  float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks
   uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16 (first the fp16 exponentials)
   uint16_t* dZT;       // [V, KT]      the same, transposed; samples of a dW batch side by side
   float* dx_part;      // [S, NP, d]   split-vocabulary partial dX
@@ -77,7 +79,9 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
                                float* t_out, int t_stride, int row_cap, int V,
                                int first_in_batch, const DxPlan& plan, hipStream_t s);
-hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s);
+hipError_t launch_row_rms(const uint16_t* x, const Workspace& ws, int d, float eps, hipStream_t s);
+hipError_t launch_gather(const uint16_t* hidden, const float* gamma, const Workspace& ws, int d,
+                         hipStream_t s);
 hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool store_u,
                            hipStream_t s);
 hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s);
@@ -92,6 +96,8 @@ hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s);
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s);
 hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s);
+hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, const uint16_t* x, const float* gamma,
+                                    float* dx, float* dgamma, int d, hipStream_t s);
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s);
 
 int gemm_grid(int device);  // persistent grid size of the GEMM kernels on `device`

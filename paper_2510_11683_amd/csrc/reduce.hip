@@ -316,4 +316,99 @@ hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s
   return hipGetLastError();
 }
 
+// Split reduction followed by the backward of the final RMSNorm
+// h = gamma x r, r = (mean x^2 + eps)^(-1/2), for one row per workgroup:
+//   dh       = sum_s part[s][row]                     (d loss / d h)
+//   dx_k    += r gamma_k dh_k - (r^3 / d) x_k sum_i gamma_i dh_i x_i
+//   c_k      = dh_k x_k r  -> part[0][row][k], summed over rows into dgamma
+// Every thread revisits only the elements it wrote, so part[0] needs no
+// cross-thread ordering; the row dot product goes through LDS.
+__global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
+    float* __restrict__ part, const int32_t* __restrict__ idx, const SampleMeta* __restrict__ meta,
+    const uint16_t* __restrict__ x, const float* __restrict__ gamma,
+    const float* __restrict__ inv_rms, float* __restrict__ dx, int d, int64_t split_stride) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  if (r >= meta->n_rows) return;
+  const int n_split = meta->dx_split;
+  const int tid = threadIdx.x;
+  float* p0 = part + (int64_t)r * d;
+  const uint16_t* xr = x + (int64_t)idx[r] * d;
+  float dot = 0.f;
+  for (int c = tid * 4; c < d; c += 1024) {
+    float4 acc = *reinterpret_cast<const float4*>(p0 + c);
+    for (int sp = 1; sp < n_split; ++sp) {
+      const float4 v = *reinterpret_cast<const float4*>(p0 + sp * split_stride + c);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    *reinterpret_cast<float4*>(p0 + c) = acc;
+    const uint2 xv = *reinterpret_cast<const uint2*>(xr + c);
+    const float4 g = *reinterpret_cast<const float4*>(gamma + c);
+    dot = fmaf(g.x * acc.x, __uint_as_float(xv.x << 16), dot);
+    dot = fmaf(g.y * acc.y, __uint_as_float(xv.x & 0xFFFF0000u), dot);
+    dot = fmaf(g.z * acc.z, __uint_as_float(xv.y << 16), dot);
+    dot = fmaf(g.w * acc.w, __uint_as_float(xv.y & 0xFFFF0000u), dot);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) dot += __shfl_xor(dot, off, 64);
+  if ((tid & 63) == 0) red[tid >> 6] = dot;
+  __syncthreads();
+  dot = red[0] + red[1] + red[2] + red[3];
+  const float ir = inv_rms[r];
+  const float cx = ir * ir * ir * dot / (float)d;
+  float* dxr = dx + (int64_t)idx[r] * d;
+  for (int c = tid * 4; c < d; c += 1024) {
+    const float4 dh = *reinterpret_cast<const float4*>(p0 + c);
+    const uint2 xv = *reinterpret_cast<const uint2*>(xr + c);
+    const float4 g = *reinterpret_cast<const float4*>(gamma + c);
+    const float x0 = __uint_as_float(xv.x << 16), x1 = __uint_as_float(xv.x & 0xFFFF0000u);
+    const float x2 = __uint_as_float(xv.y << 16), x3 = __uint_as_float(xv.y & 0xFFFF0000u);
+    float4 o = *reinterpret_cast<float4*>(dxr + c);
+    o.x += ir * g.x * dh.x - cx * x0;
+    o.y += ir * g.y * dh.y - cx * x1;
+    o.z += ir * g.z * dh.z - cx * x2;
+    o.w += ir * g.w * dh.w - cx * x3;
+    *reinterpret_cast<float4*>(dxr + c) = o;
+    *reinterpret_cast<float4*>(p0 + c) = make_float4(dh.x * x0 * ir, dh.y * x1 * ir, dh.z * x2 * ir, dh.w * x3 * ir);
+  }
+}
+
+// dgamma[k] += sum over the sample's rows of part[0][row][k], in a fixed order:
+// partial sums over 256-row chunks, then the chunks in order.
+__global__ __launch_bounds__(256) void k_dgamma_partial(const float* __restrict__ part,
+                                                        const SampleMeta* __restrict__ meta,
+                                                        float* __restrict__ gpart, int d) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int r0 = blockIdx.y * 256;
+  if (k >= d) return;
+  const int r1 = min(meta->n_rows, r0 + 256);
+  float acc = 0.f;
+  for (int r = r0; r < r1; ++r) acc += part[(int64_t)r * d + k];
+  gpart[(int64_t)blockIdx.y * d + k] = acc;
+}
+
+__global__ __launch_bounds__(256) void k_dgamma_final(const float* __restrict__ gpart,
+                                                      const SampleMeta* __restrict__ meta,
+                                                      float* __restrict__ dgamma, int d) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= d) return;
+  const int chunks = (meta->n_rows + 255) / 256;
+  float acc = 0.f;
+  for (int c = 0; c < chunks; ++c) acc += gpart[(int64_t)c * d + k];
+  dgamma[k] += acc;
+}
+
+hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, const uint16_t* x, const float* gamma,
+                                    float* dx, float* dgamma, int d, hipStream_t s) {
+  k_dx_reduce_rmsnorm<<<(unsigned)ws.NP, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta, x, gamma,
+                                                     ws.inv_rms, dx, d, ws.NP * d);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 g1((unsigned)((d + 255) / 256), (unsigned)(ws.NP / 256));
+  k_dgamma_partial<<<g1, 256, 0, s>>>(ws.dx_part, ws.meta, ws.gpart, d);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  k_dgamma_final<<<(unsigned)((d + 255) / 256), 256, 0, s>>>(ws.gpart, ws.meta, dgamma, d);
+  return hipGetLastError();
+}
+
 }  // namespace bgpo

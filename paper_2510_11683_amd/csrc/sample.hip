@@ -174,11 +174,48 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
 }
 
 // ---------------------------------------------------------------------------
+// Inverse RMS of the masked rows of the pre-norm activations x (for the final
+// RMSNorm h = gamma x r, r = (mean x^2 + eps)^(-1/2)): one wave per row, fp32
+// sum of squares.
+__global__ __launch_bounds__(256) void k_row_rms(const uint16_t* __restrict__ x,
+                                                 const int32_t* __restrict__ idx,
+                                                 const SampleMeta* __restrict__ meta,
+                                                 float* __restrict__ inv_rms, int d, float eps) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= meta->n_rows) return;
+  const uint16_t* xr = x + (int64_t)idx[row] * d;
+  float acc = 0.f;
+  for (int k = lane * 8; k < d; k += 64 * 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(xr + k);
+    const uint32_t a[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __uint_as_float(a[e] << 16), hi = __uint_as_float(a[e] & 0xFFFF0000u);
+      acc = fmaf(lo, lo, acc);
+      acc = fmaf(hi, hi, acc);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+  if (lane == 0) inv_rms[row] = 1.f / sqrtf(acc / (float)d + eps);
+}
+
+hipError_t launch_row_rms(const uint16_t* x, const Workspace& ws, int d, float eps, hipStream_t s) {
+  k_row_rms<<<(unsigned)(ws.NP / 4), 256, 0, s>>>(x, ws.idx, ws.meta, ws.inv_rms, d, eps);
+  return hipGetLastError();
+}
+
 // Gather: Hc[r, :] = hidden[idx[r], :] and HcT[:, col_off + r] for r < N; zeros
 // for N <= r < N_pad.  64x64 tiles staged in LDS for the transposed copy.
+// With `gamma`, `hidden` holds the pre-norm activations and the gathered row is
+// the final RMSNorm bf16(x * inv_rms[r] * gamma) (fp32 arithmetic, one
+// rounding to bfloat16).
 __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hidden,
                                                 const int32_t* __restrict__ idx,
                                                 const SampleMeta* __restrict__ meta,
+                                                const float* __restrict__ gamma,
+                                                const float* __restrict__ inv_rms,
                                                 uint16_t* __restrict__ Hc,
                                                 uint16_t* __restrict__ HcT, int d, int64_t ldt) {
   __shared__ uint16_t tile[64][72];
@@ -194,7 +231,22 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
     const int row = q >> 3, ch = q & 7;
     const int r = r0 + row;
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < N) v = *reinterpret_cast<const uint4*>(hidden + (int64_t)idx[r] * d + c0 + ch * 8);
+    if (r < N) {
+      v = *reinterpret_cast<const uint4*>(hidden + (int64_t)idx[r] * d + c0 + ch * 8);
+      if (gamma) {
+        const float ir = inv_rms[r];
+        const float4 g0 = *reinterpret_cast<const float4*>(gamma + c0 + ch * 8);
+        const float4 g1 = *reinterpret_cast<const float4*>(gamma + c0 + ch * 8 + 4);
+        const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        uint32_t a[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __uint_as_float(a[e] << 16), hi = __uint_as_float(a[e] & 0xFFFF0000u);
+          a[e] = pack_bf16x2(lo * ir * gg[2 * e], hi * ir * gg[2 * e + 1]);
+        }
+        v = make_uint4(a[0], a[1], a[2], a[3]);
+      }
+    }
     *reinterpret_cast<uint4*>(Hc + (int64_t)r * d + c0 + ch * 8) = v;
     *reinterpret_cast<uint4*>(&tile[row][ch * 8]) = v;
   }
@@ -212,9 +264,10 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
   }
 }
 
-hipError_t launch_gather(const uint16_t* hidden, const Workspace& ws, int d, hipStream_t s) {
+hipError_t launch_gather(const uint16_t* hidden, const float* gamma, const Workspace& ws, int d,
+                         hipStream_t s) {
   dim3 grid((unsigned)(ws.NP / 64), (unsigned)(d / 64));
-  k_gather<<<grid, 256, 0, s>>>(hidden, ws.idx, ws.meta, ws.Hc, ws.HcT, d, ws.KT);
+  k_gather<<<grid, 256, 0, s>>>(hidden, ws.idx, ws.meta, gamma, ws.inv_rms, ws.Hc, ws.HcT, d, ws.KT);
   return hipGetLastError();
 }
 

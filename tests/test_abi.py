@@ -64,6 +64,8 @@ def test_workspace_independent_of_n_t(b):
     (dict(d=4000), -4), (dict(V=126000), -4), (dict(d=32), -4), (dict(B=5000, L=1), -4),
     (dict(B=2048, L=1024), -4), (dict(B=0), -1), (dict(L=0), -1), (dict(n_t=0), -1),
     (dict(j_begin=-1), -1), (dict(j_begin=60, j_count=5), -1), (dict(t_mode=2), -1),
+    (dict(bound=4), -1), (dict(sample_stride=-8), -1), (dict(sample_stride=12), -1),
+    (dict(norm_eps=float("nan")), -1), (dict(norm_eps=-1.0), -1),
 ])
 def test_problem_validation(b, kw, status):
     with pytest.raises(b.BgpoError) as e:
@@ -113,6 +115,31 @@ def test_null_pointers_and_workspace_rejected_before_hip(b):
 
 
 def test_problem_struct_layout(b):
-    # matches the C struct: 8 int32, uint64, uint32, int32 = 48 bytes
-    assert ctypes.sizeof(b._Problem) == 48
+    # matches the C struct: 8 int32, uint64, uint32, int32, int64, float, int32 = 64 bytes
+    assert ctypes.sizeof(b._Problem) == 64
     assert b._Problem.seed.offset == 32
+    assert b._Problem.bound.offset == 44
+    assert b._Problem.sample_stride.offset == 48
+    assert b._Problem.norm_eps.offset == 56
+
+
+def test_reserved_field_and_rmsnorm_arguments_rejected_before_hip(b):
+    lib = b._lib
+    fake = ctypes.c_void_p(0x1000)
+    nbytes = ctypes.c_size_t(0)
+    q = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
+    q.reserved = 1
+    assert lib.bgpo_workspace_size(ctypes.byref(q), ctypes.byref(nbytes)) == -1
+    p = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
+    assert lib.bgpo_workspace_size(ctypes.byref(p), ctypes.byref(nbytes)) == 0
+    ws = ctypes.c_void_p(0x100000)
+    # missing norm weight / its gradient
+    assert lib.bgpo_elbo_fwd_rmsnorm(ctypes.byref(p), fake, None, fake, fake, fake, fake, fake,
+                                     None, ws, nbytes.value, None, None) == -1
+    assert lib.bgpo_elbo_bwd_accumulate_rmsnorm(ctypes.byref(p), fake, fake, fake, fake, fake,
+                                                fake, None, 0.125, fake, None, fake, fake, fake,
+                                                fake, fake, None, None, ws, nbytes.value, None,
+                                                None) == -1
+    # misaligned norm weight
+    assert lib.bgpo_elbo_fwd_rmsnorm(ctypes.byref(p), fake, ctypes.c_void_p(0x1004), fake, fake,
+                                     fake, fake, fake, None, ws, nbytes.value, None, None) == -1

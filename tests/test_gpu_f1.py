@@ -1,0 +1,216 @@
+"""Per-sample head inputs and the fused final RMSNorm, HIP path (C ABI) vs
+the float64 oracle.
+
+* MID shape (several tiles, ragged rows / vocabulary / hidden size), off-policy
+  with both bound branches: per-sample activations through the norm
+  (``bgpo_elbo_bwd_accumulate_rmsnorm`` with sample_stride = B*L*d), the same
+  without the norm (``bgpo_elbo_bwd_accumulate`` with a stride), and shared
+  activations through the norm; against ``elbo_per_sample`` with the head
+  input rounded to bfloat16 as the head's operand (off-policy, the Jensen
+  branch scales the gradient by e^d, so an absolute error of l from an
+  unrounded head input would show up in dX and dW).  Bars as in
+  test_gpu_parity: l within 1e-3, g tightly given l, dx / dgamma / dW within
+  2e-2 relative max-norm.
+* on-policy: l from ``bgpo_elbo_fwd_rmsnorm`` fed back gives d == 0 exactly.
+* LLaDA head shape B8 L512 n_t 64 with the norm (shared activations, all
+  samples): l, g, sampled dx rows and dW columns against the collapsed
+  oracle on the float64 norm output.
+* the same shape, per-sample copies of one tensor: identical l and dW and
+  the per-sample dx summing to the shared dx (a property at any size).
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import elbo, rmsnorm
+from gpu_util import lib, rel_maxnorm
+
+pytestmark = pytest.mark.gpu
+
+ELL_RTOL = 1e-3
+GRAD_RTOL = 2e-2
+EPS = 1e-6
+MID = workloads.Workload("mid_B4_L200_d576_V4288_nt3", B=4, L=200, d=576, V=4288, n_t=3,
+                         lengths=(120, 200), group=4, data_seed=2001, philox_seed=0xB6B10001)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _bf16_dev(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+class Run:
+    """Device inputs / outputs of one workload for the f1 entry points."""
+
+    def __init__(self, w, x_bits, gamma, per_sample, j_count=None):
+        b = lib()
+        base = workloads.generate(w, with_hidden=False)
+        self.w, self.base = w, base
+        self.dev = b.device_inputs(dict(base, hidden=None) | {"hidden": np.zeros((1,), np.uint16)})
+        jc = w.n_t if j_count is None else j_count
+        self.prob = b.Problem(w.B, w.L, w.d, w.V, w.n_t, j_begin=0, j_count=jc, seed=w.philox_seed,
+                              seq_id_base=w.seq_id_base, t_mode=w.t_mode,
+                              sample_stride=w.B * w.L * w.d if per_sample else 0, norm_eps=EPS)
+        self.x = _bf16_dev(x_bits)
+        self.gamma = None if gamma is None else torch.from_numpy(gamma).cuda()
+        self.ws = b.alloc_workspace(self.prob)
+        B, nt = w.B, w.n_t
+        self.dx = torch.zeros(self.x.shape, dtype=torch.float32, device="cuda")
+        self.dgamma = torch.zeros(w.d, dtype=torch.float32, device="cuda")
+        self.dW = torch.zeros(w.d, w.V, dtype=torch.float32, device="cuda")
+        self.ell = torch.zeros(B, nt, dtype=torch.float64, device="cuda")
+        self.g = torch.zeros_like(self.ell)
+        self.loss = torch.zeros(1, dtype=torch.float64, device="cuda")
+        self.nm = torch.zeros(B, nt, dtype=torch.int32, device="cuda")
+        self.t = torch.zeros(B, nt, dtype=torch.float32, device="cuda")
+        self.flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def fwd(self):
+        b, d = lib(), self.dev
+        if self.gamma is None:
+            b.bgpo_elbo_fwd(self.prob, self.x, d["W"], d["targets"], d["resp_mask"], self.ell,
+                            self.nm, self.t, self.ws)
+        else:
+            b.bgpo_elbo_fwd_rmsnorm(self.prob, self.x, self.gamma, d["W"], d["targets"],
+                                    d["resp_mask"], self.ell, self.nm, self.t, self.ws)
+
+    def bwd(self, ell_old=None, loss_scale=0.25):
+        b, d = lib(), self.dev
+        eo = None if ell_old is None else torch.as_tensor(ell_old, dtype=torch.float64).cuda().contiguous()
+        if self.gamma is None:
+            b.bgpo_elbo_bwd_accumulate(self.prob, self.x, d["W"], d["targets"], d["resp_mask"],
+                                       d["adv"], eo, loss_scale, self.dx, self.dW, self.ell, self.g,
+                                       self.loss, self.nm, self.t, self.flags, self.ws)
+        else:
+            b.bgpo_elbo_bwd_accumulate_rmsnorm(self.prob, self.x, self.gamma, d["W"], d["targets"],
+                                               d["resp_mask"], d["adv"], eo, loss_scale, self.dx,
+                                               self.dgamma, self.dW, self.ell, self.g, self.loss,
+                                               self.nm, self.t, self.flags, self.ws)
+
+    def out(self):
+        torch.cuda.synchronize()
+        return {k: getattr(self, k).cpu().numpy() for k in ("ell", "g", "nm", "t", "dx", "dgamma", "dW", "flags")} | \
+            {"loss": float(self.loss.item())}
+
+
+def _oracle_problem(w):
+    return elbo.Problem(w.B, w.L, w.d, w.V, w.n_t, seed=w.philox_seed, seq_id_base=w.seq_id_base,
+                        t_mode=w.t_mode)
+
+
+def _check(w, o, ref, adv, ell_old, loss_scale, with_norm):
+    for j in range(w.n_t):
+        assert np.array_equal(o["nm"][:, j], ref.n_masked[:, j])
+        assert np.array_equal(o["t"][:, j].astype(np.float64), ref.t[:, j])
+        np.testing.assert_allclose(o["ell"][:, j], ref.ell[:, j], rtol=ELL_RTOL, atol=0)
+    g_of_ell = np.array([[elbo.bound_term(o["ell"][b, j] - ell_old[b, j], float(adv[b]), w.n_t)[0]
+                          for j in range(w.n_t)] for b in range(w.B)])
+    np.testing.assert_allclose(o["g"], g_of_ell, rtol=1e-12, atol=1e-15)
+    assert abs(o["loss"] + loss_scale * g_of_ell.sum()) <= 1e-12 * loss_scale * np.abs(g_of_ell).sum()
+    assert o["flags"] == 0
+    assert rel_maxnorm(o["dx"], ref.dX) <= GRAD_RTOL, rel_maxnorm(o["dx"], ref.dX)
+    assert rel_maxnorm(o["dW"], ref.dW) <= GRAD_RTOL, rel_maxnorm(o["dW"], ref.dW)
+    if with_norm:
+        assert rel_maxnorm(o["dgamma"], ref.dgamma) <= GRAD_RTOL, rel_maxnorm(o["dgamma"], ref.dgamma)
+
+
+@pytest.mark.parametrize("per_sample,with_norm", [(True, True), (True, False), (False, True)],
+                         ids=["per_sample_rmsnorm", "per_sample_plain", "shared_rmsnorm"])
+def test_mid_parity_off_policy(per_sample, with_norm):
+    w = MID
+    xb = workloads.pre_norm_activations(w, w.n_t if per_sample else 0)
+    gamma = workloads.norm_weight(w) if with_norm else None
+    run = Run(w, xb, gamma, per_sample)
+    base = run.base
+    X = elbo.bf16_to_f64(xb).reshape(xb.shape)
+    W = elbo.bf16_to_f64(base["W"]).reshape(w.d, w.V)
+    op = _oracle_problem(w)
+    g64 = None if gamma is None else gamma.astype(np.float64)
+    ell_old = elbo.elbo_per_sample(op, X, W, base["targets"], base["resp_mask"], base["adv"],
+                                   backward=False, gamma=g64, eps=EPS, per_sample=per_sample,
+                                   head_bf16=True).ell
+    ell_old = ell_old + np.random.default_rng(8).normal(0, 1.0, ell_old.shape)
+    ref = elbo.elbo_per_sample(op, X, W, base["targets"], base["resp_mask"], base["adv"],
+                               ell_old=ell_old, loss_scale=0.25, gamma=g64, eps=EPS,
+                               per_sample=per_sample, head_bf16=True)
+    assert (base["adv"] > 0).any() and (base["adv"] < 0).any()
+    run.bwd(ell_old=ell_old, loss_scale=0.25)
+    _check(w, run.out(), ref, base["adv"], ell_old, 0.25, with_norm)
+
+
+def test_rmsnorm_on_policy_d_is_exactly_zero():
+    w = MID
+    run = Run(w, workloads.pre_norm_activations(w, w.n_t), workloads.norm_weight(w), True)
+    run.fwd()
+    ell_fwd = run.out()["ell"].copy()
+    run.bwd(ell_old=ell_fwd)
+    o = run.out()
+    assert np.array_equal(o["ell"], ell_fwd)
+    adv = run.base["adv"].astype(np.float64)
+    assert np.array_equal(o["g"], np.repeat((adv / w.n_t)[:, None], w.n_t, axis=1))
+
+
+def test_llada_head_rmsnorm_shared_all_samples():
+    w = workloads.LLADA_L512_NT64
+    xb = workloads.pre_norm_activations(w)
+    gamma = workloads.norm_weight(w)
+    run = Run(w, xb, gamma, per_sample=False)
+    base = run.base
+    run.bwd(loss_scale=1.0 / 8)
+    torch.cuda.synchronize()
+    op = _oracle_problem(w)
+    used = np.zeros((w.B, w.L), dtype=bool)
+    for j in op.js:
+        used |= elbo.sample_masks(op, base["resp_mask"], j)[2]
+    rng = np.random.default_rng(9)
+    rows = np.concatenate([b * w.L + rng.choice(np.flatnonzero(used[b]), 6, replace=False) for b in (1, 6)])
+    tg = base["targets"].reshape(-1)[base["resp_mask"].reshape(-1) != 0]
+    vals, counts = np.unique(tg, return_counts=True)
+    cols = np.unique(np.concatenate([vals[np.argsort(-counts)[:256]], rng.choice(w.V, 768, replace=False)]))
+    o = {k: getattr(run, k) for k in ("ell", "g", "nm", "t")}
+    o = {k: v.cpu().numpy() for k, v in o.items()}
+    dx = run.dx.reshape(-1, w.d)[torch.from_numpy(rows).cuda()].cpu().numpy()
+    dW = run.dW[:, torch.from_numpy(cols).cuda()].cpu().numpy()
+    flags = int(run.flags.item())
+    del run
+    torch.cuda.empty_cache()
+    X = elbo.bf16_to_f64(xb).reshape(w.B, w.L, w.d)
+    H = rmsnorm.round_to_bf16(rmsnorm.rmsnorm(X, gamma.astype(np.float64), EPS)[0])
+    ref = elbo.elbo_collapsed(op, None, base["W"], base["targets"], base["resp_mask"], base["adv"],
+                              dx_rows=rows, dw_cols=cols, hidden_f64=H)
+    dx_ref, _ = rmsnorm.rmsnorm_backward(X.reshape(-1, w.d)[rows], gamma.astype(np.float64), EPS, ref.dX)
+    assert flags == 0
+    assert np.array_equal(o["nm"], ref.n_masked)
+    np.testing.assert_allclose(o["ell"], ref.ell, rtol=ELL_RTOL, atol=0)
+    np.testing.assert_allclose(o["g"], ref.g, rtol=1e-12, atol=1e-15)      # on-policy: A / n_t
+    assert rel_maxnorm(dx, dx_ref) <= GRAD_RTOL, rel_maxnorm(dx, dx_ref)
+    assert rel_maxnorm(dW, ref.dW) <= GRAD_RTOL, rel_maxnorm(dW, ref.dW)
+
+
+def test_llada_head_per_sample_copies_equal_shared():
+    w = workloads.LLADA_L512_NT64
+    xb = workloads.pre_norm_activations(w)
+    gamma = workloads.norm_weight(w)
+    jc = 4
+    outs = []
+    for per_sample in (False, True):
+        bits = np.stack([xb] * jc) if per_sample else xb
+        run = Run(w, bits, gamma, per_sample, j_count=jc)
+        run.bwd(loss_scale=1.0 / 8)
+        o = run.out()
+        outs.append(o)
+        del run
+        torch.cuda.empty_cache()
+    sh, ps = outs
+    assert np.array_equal(sh["ell"], ps["ell"]) and np.array_equal(sh["g"], ps["g"])
+    assert np.array_equal(sh["dW"], ps["dW"]) and np.array_equal(sh["dgamma"], ps["dgamma"])
+    assert np.abs(sh["dx"]).max() > 0
+    assert rel_maxnorm(ps["dx"].astype(np.float64).sum(axis=0), sh["dx"]) <= 1e-5

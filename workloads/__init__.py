@@ -180,3 +180,30 @@ def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True
 
     return dict(hidden=hidden, W=W, targets=targets, resp_mask=resp_mask, adv=adv,
                 lengths=lengths)
+
+
+def pre_norm_activations(w: Workload, n_samples: int = 0) -> np.ndarray:
+    """Activations x in front of the final RMSNorm, as bf16 bits: N(0, 1)
+    entries times a per-row scale drawn log-uniformly from [1/4, 4] (so the
+    norm's 1/rms varies across rows).  ``n_samples`` = 0 gives one tensor
+    [B, L, d] shared by all samples, n > 0 gives [n, B, L, d], sample q from
+    its own stream."""
+    B, L, d = w.B, w.L, w.d
+    base = np.random.SeedSequence(w.data_seed).spawn(7)[5]
+    n = max(1, n_samples)
+    out = np.empty((n, B * L, d), dtype=np.uint16)
+    for q, sq in enumerate(base.spawn(n)):
+        def fill(c, rng, q=q):
+            rows = min(B * L, c + _CHUNK_ROWS) - c
+            scale = np.exp(rng.uniform(np.log(0.25), np.log(4.0), size=(rows, 1))).astype(np.float32)
+            x = rng.standard_normal((rows, d), dtype=np.float32) * scale
+            out[q, c:c + rows] = f32_to_bf16_bits(x).reshape(rows, d)
+        _chunked(sq, B * L, fill)
+    out = out.reshape(n, B, L, d)
+    return out[0] if n_samples == 0 else out
+
+
+def norm_weight(w: Workload) -> np.ndarray:
+    """Final-RMSNorm weight, float32 [d]: 1 + 0.1 N(0, 1)."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(w.data_seed).spawn(7)[6]))
+    return (1.0 + 0.1 * rng.standard_normal(w.d)).astype(np.float32)
