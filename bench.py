@@ -150,6 +150,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the per-sample + final-RMSNorm variant measurement")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -268,9 +270,55 @@ def main():
         "status_flags": int(flags.item()),
         "input_gen_s": gen_s,
     }
+    if not args.no_variants:
+        out["variants"] = {"per_sample_rmsnorm": per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x, args.cpu_budget)
     print(json.dumps(out))
+
+
+def per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens_main):
+    """The same workload through the final-RMSNorm entry point with one
+    activation tensor per sample (device copies of one pre-norm tensor) and a
+    dx per sample: the per-sample form of the step."""
+    import dataclasses
+    import torch
+    from paper_2510_11683_amd import bgpo
+    B, L, d, V, nt = w.B, w.L, w.d, w.V, w.n_t
+    xb = workloads.pre_norm_activations(w)
+    x1 = torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16)
+    x = x1.unsqueeze(0).expand(nt, B, L, d).contiguous()
+    del x1
+    gamma = torch.from_numpy(workloads.norm_weight(w)).cuda()
+    p = dataclasses.replace(prob, sample_stride=B * L * d, norm_eps=1e-6)
+    dx = torch.zeros(nt, B, L, d, dtype=torch.float32, device="cuda")
+    dgam = torch.zeros(d, dtype=torch.float32, device="cuda")
+    dW = torch.zeros(d, V, dtype=torch.float32, device="cuda")
+    ell = torch.zeros(B, nt, dtype=torch.float64, device="cuda")
+    g = torch.zeros_like(ell)
+    loss = torch.zeros(1, dtype=torch.float64, device="cuda")
+    nm = torch.zeros(B, nt, dtype=torch.int32, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def step():
+        bgpo.bgpo_elbo_bwd_accumulate_rmsnorm(p, x, gamma, dev["W"], dev["targets"],
+                                              dev["resp_mask"], dev["adv"], None, 1.0 / 8, dx,
+                                              dgam, dW, ell, g, loss, nm, None, flags, ws)
+    steps = max(1, min(args.steps, 3))
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    tokens = int(nm.sum().item())
+    assert tokens == tokens_main            # same masks as the main measurement
+    return {"value": tokens / (ms / 1e3), "unit": "masked tokens/s", "ms_per_step": ms,
+            "steps": steps, "sample_stride": B * L * d, "status_flags": int(flags.item())}
 
 
 if __name__ == "__main__":
