@@ -67,11 +67,16 @@ def _load():
     lib.bgpo_elbo_bwd_accumulate_rmsnorm.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, vp,
                                                      ctypes.c_double, vp, vp, vp, vp, vp, vp, vp,
                                                      vp, vp, vp, sz, vp, P(Timing)]
+    lib.bgpo_moments_update.argtypes = [vp, vp, vp, ctypes.c_int64, i32, vp]
+    lib.bgpo_moments_workspace_size.restype = sz
+    lib.bgpo_moments_workspace_size.argtypes = []
+    lib.bgpo_moments_summary.argtypes = [vp, vp, vp, ctypes.c_int64, i32, vp, vp, sz, vp]
     lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
     lib.bgpo_test_gemm_variant.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, vp]
     for f in ("bgpo_workspace_size", "bgpo_sample_masks", "bgpo_elbo_fwd",
               "bgpo_elbo_bwd_accumulate", "bgpo_elbo_fwd_rmsnorm",
-              "bgpo_elbo_bwd_accumulate_rmsnorm", "bgpo_test_gemm_nt", "bgpo_test_gemm_variant"):
+              "bgpo_elbo_bwd_accumulate_rmsnorm", "bgpo_moments_update", "bgpo_moments_summary",
+              "bgpo_test_gemm_nt", "bgpo_test_gemm_variant"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -253,6 +258,30 @@ def bgpo_elbo_bwd_accumulate_rmsnorm(prob: Problem, x, norm_weight, W_head, targ
         _ptr(status_flags, "status_flags", (torch.int32,), (1,), allow_none=True),
         _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(), _stream(stream),
         ctypes.byref(timing) if timing is not None else None), "bgpo_elbo_bwd_accumulate_rmsnorm")
+
+
+def bgpo_moments_update(g, mean, m2, count: int, stream=None):
+    """Fold estimate number `count` (0-based) of a gradient into running moments."""
+    n = g.numel()
+    _check(_lib.bgpo_moments_update(_ptr(g, "g", (torch.float32,)),
+                                    _ptr(mean, "mean", (torch.float32,), tuple(g.shape)),
+                                    _ptr(m2, "m2", (torch.float32,), tuple(g.shape)), n, int(count),
+                                    _stream(stream)), "bgpo_moments_update")
+
+
+def moments_workspace(device="cuda") -> torch.Tensor:
+    return torch.empty(_lib.bgpo_moments_workspace_size(), dtype=torch.uint8, device=device)
+
+
+def bgpo_moments_summary(mean, m2, ref, count: int, out, workspace, stream=None):
+    """out[0] mean per-element sample std, out[1] mean |mean - ref|, out[2] mean |ref|."""
+    _check(_lib.bgpo_moments_summary(_ptr(mean, "mean", (torch.float32,)),
+                                     _ptr(m2, "m2", (torch.float32,), tuple(mean.shape)),
+                                     _ptr(ref, "ref", (torch.float32,), tuple(mean.shape), allow_none=True),
+                                     mean.numel(), int(count),
+                                     _ptr(out, "out", (torch.float64,), (3,)),
+                                     _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(),
+                                     _stream(stream)), "bgpo_moments_summary")
 
 
 def bgpo_test_gemm_nt(A, B, C, stream=None):

@@ -13,7 +13,7 @@ LIB = os.path.join(ROOT, "paper_2510_11683_amd", "libbgpo.so")
 
 def _declared():
     names = set()
-    for h in ("bgpo.h", "bgpo_testing.h"):
+    for h in ("bgpo.h", "bgpo_testing.h", "bgpo_stats.h"):
         src = open(os.path.join(ROOT, "include", h)).read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
         names |= set(re.findall(r"\b(bgpo_\w+)\s*\(", src))
