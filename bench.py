@@ -271,10 +271,53 @@ def main():
         "input_gen_s": gen_s,
     }
     if not args.no_variants:
-        out["variants"] = {"per_sample_rmsnorm": per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens)}
+        out["variants"] = {"per_sample_rmsnorm": per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens),
+                           "exact_objective_off_policy": exact_objective_leg(w, prob, dev, ws, args,
+                                                                             tokens)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x, args.cpu_budget)
     print(json.dumps(out))
+
+
+def exact_objective_leg(w, prob, dev, ws, args, tokens_main):
+    """The exact ratio objective (bound mode 3) off-policy: ell_old from a
+    forward pass, so the call runs its forward pass over all samples for the
+    mean log-ratio before the per-sample backward loop."""
+    import dataclasses
+    import torch
+    from paper_2510_11683_amd import bgpo
+    B, L, d, V, nt = w.B, w.L, w.d, w.V, w.n_t
+    p = dataclasses.replace(prob, bound=bgpo.BGPO_BOUND_EXACT)
+    ell_old = torch.zeros(B, nt, dtype=torch.float64, device="cuda")
+    nm = torch.zeros(B, nt, dtype=torch.int32, device="cuda")
+    bgpo.bgpo_elbo_fwd(prob, dev["hidden"], dev["W"], dev["targets"], dev["resp_mask"], ell_old,
+                       nm, None, ws)
+    dX = torch.zeros(B, L, d, dtype=torch.float32, device="cuda")
+    dW = torch.zeros(d, V, dtype=torch.float32, device="cuda")
+    ell = torch.zeros_like(ell_old)
+    g = torch.zeros_like(ell_old)
+    loss = torch.zeros(1, dtype=torch.float64, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def step():
+        bgpo.bgpo_elbo_bwd_accumulate(p, dev["hidden"], dev["W"], dev["targets"], dev["resp_mask"],
+                                      dev["adv"], ell_old, 1.0 / 8, dX, dW, ell, g, loss, nm, None,
+                                      flags, ws)
+    steps = max(1, min(args.steps, 3))
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    tokens = int(nm.sum().item())
+    assert tokens == tokens_main
+    return {"value": tokens / (ms / 1e3), "unit": "masked tokens/s", "ms_per_step": ms,
+            "steps": steps, "status_flags": int(flags.item())}
 
 
 def per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens_main):
