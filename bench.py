@@ -274,9 +274,60 @@ def main():
         out["variants"] = {"per_sample_rmsnorm": per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens),
                            "exact_objective_off_policy": exact_objective_leg(w, prob, dev, ws, args,
                                                                              tokens)}
+        del ws
+        torch.cuda.empty_cache()
+        out["variants"]["exact_objective_retained"] = retained_memory_leg(w, prob, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x, args.cpu_budget)
     print(json.dumps(out))
+
+
+def retained_memory_leg(w, prob, dev, n_ts=(1, 4, 16)):
+    """The exact objective computed by keeping every sample's state (as when
+    all n_t computational graphs are retained): peak device memory and time
+    of one off-policy call for several n_t, against the constant-memory mode."""
+    import dataclasses
+    import torch
+    from paper_2510_11683_amd import bgpo
+    B, L, d, V = w.B, w.L, w.d, w.V
+    res = {"n_t": list(n_ts), "workspace_bytes": [], "peak_mem_bytes": [], "ms_per_call": [],
+           "masked_tokens": []}
+    for nt in n_ts:
+        p = dataclasses.replace(prob, n_t=nt, bound=bgpo.BGPO_BOUND_EXACT, retain_samples=1)
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        ws = bgpo.alloc_workspace(p)
+        dX = torch.zeros(B, L, d, dtype=torch.float32, device="cuda")
+        dW = torch.zeros(d, V, dtype=torch.float32, device="cuda")
+        ell_old = torch.zeros(B, nt, dtype=torch.float64, device="cuda")
+        ell, g = torch.zeros_like(ell_old), torch.zeros_like(ell_old)
+        loss = torch.zeros(1, dtype=torch.float64, device="cuda")
+        nm = torch.zeros(B, nt, dtype=torch.int32, device="cuda")
+        flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+        bgpo.bgpo_elbo_fwd(p, dev["hidden"], dev["W"], dev["targets"], dev["resp_mask"], ell_old,
+                           nm, None, ws)
+
+        def call():
+            bgpo.bgpo_elbo_bwd_accumulate(p, dev["hidden"], dev["W"], dev["targets"],
+                                          dev["resp_mask"], dev["adv"], ell_old, 1.0 / 8, dX, dW,
+                                          ell, g, loss, nm, None, flags, ws)
+        call()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        call()
+        b.record()
+        torch.cuda.synchronize()
+        res["workspace_bytes"].append(ws.numel())
+        res["peak_mem_bytes"].append(torch.cuda.max_memory_allocated())
+        res["ms_per_call"].append(a.elapsed_time(b))
+        res["masked_tokens"].append(int(nm.sum().item()))
+        del ws, dX, dW
+        torch.cuda.empty_cache()
+    res["workspace_bytes_n_t_64"] = bgpo.bgpo_workspace_size(
+        dataclasses.replace(prob, n_t=64, bound=bgpo.BGPO_BOUND_EXACT, retain_samples=1))
+    res["constant_mode_workspace_bytes"] = bgpo.bgpo_workspace_size(
+        dataclasses.replace(prob, bound=bgpo.BGPO_BOUND_EXACT))
+    return res
 
 
 def exact_objective_leg(w, prob, dev, ws, args, tokens_main):

@@ -41,7 +41,8 @@
  *     wait for its own timing events before returning.
  *   - The library never allocates device memory; scratch space is the
  *     caller's `workspace` of at least bgpo_workspace_size() bytes (256-byte
- *     aligned).  Its size depends on B, L, d and V, never on n_t.
+ *     aligned).  Its size depends on B, L, d and V, never on n_t (except in
+ *     the retain_samples contrast mode below).
  *   - Host-detectable errors return a negative bgpo_status before anything is
  *     enqueued; HIP launch errors return BGPO_ERR_HIP.  No C++ exception
  *     crosses the ABI.  Entry points keep no mutable global state; calls on
@@ -93,7 +94,18 @@ enum { BGPO_T_IID = 0, BGPO_T_STRATIFIED = 1 };
  *                      BGPO_ERR_INVALID_ARG) and, off-policy, first runs a
  *                      forward pass over every sample to form dbar (memory
  *                      stays constant in n_t; the forward work doubles).
- * On-policy (d == 0) all four give g_j = A / n_t and the same gradient. */
+ * On-policy (d == 0) all four give g_j = A / n_t and the same gradient.
+ *
+ * retain_samples = 1 (exact objective only) computes the same result the way
+ * an implementation that keeps all n_t computational graphs does (Section 2.2:
+ * the exponential of Eq. elbo_ratio needs every sample before any gradient):
+ * every sample's forward runs once and its state (masked rows, log-sum-exp
+ * partials, gathered rows, the exponentials of its logits) is kept until the
+ * mean log-ratio is known.  bgpo_workspace_size then grows linearly with n_t
+ * (about 2.2 GB per sample at B=8, L=512, d=4096, V=126464), which is the
+ * memory cost that BGPO's linear bound removes; use it to measure that
+ * contrast.  retain_samples = 1 with another bound returns
+ * BGPO_ERR_INVALID_ARG. */
 enum { BGPO_BOUND_PAPER = 0, BGPO_BOUND_TAYLOR = 1, BGPO_BOUND_JENSEN = 2, BGPO_BOUND_EXACT = 3 };
 
 /* Bits of *status_flags (device int32, OR-ed in, never cleared by the library). */
@@ -117,7 +129,9 @@ typedef struct bgpo_problem {
                            dX + (j - j_begin) * sample_stride.  0 = one hidden[B, L, d]
                            shared by every sample and one dX.  A multiple of 8, >= 0. */
   float norm_eps;       /* epsilon of the final RMSNorm (the _rmsnorm entry points) */
-  int32_t reserved;     /* must be 0 */
+  int32_t retain_samples;/* 0, or 1 with bound = BGPO_BOUND_EXACT: keep the state of
+                           every sample instead of running the forward twice (see
+                           below); the workspace then grows with n_t */
 } bgpo_problem;
 
 /* Kernel classes reported by the optional timing record. */

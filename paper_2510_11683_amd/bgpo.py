@@ -36,7 +36,7 @@ class _Problem(ctypes.Structure):
                 ("j_count", ctypes.c_int32), ("t_mode", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("seq_id_base", ctypes.c_uint32),
                 ("bound", ctypes.c_int32), ("sample_stride", ctypes.c_int64),
-                ("norm_eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
+                ("norm_eps", ctypes.c_float), ("retain_samples", ctypes.c_int32)]
 
 
 class Timing(ctypes.Structure):
@@ -111,6 +111,7 @@ class Problem:
     bound: int = BGPO_BOUND_PAPER
     sample_stride: int = 0        # elements between per-sample head inputs / dX; 0 = shared
     norm_eps: float = 1e-6        # final RMSNorm epsilon (the _rmsnorm calls)
+    retain_samples: int = 0       # 1: exact objective keeping every sample's state (memory ~ n_t)
 
     @property
     def jc(self) -> int:
@@ -119,7 +120,7 @@ class Problem:
     def c(self) -> _Problem:
         return _Problem(self.B, self.L, self.d, self.V, self.n_t, self.j_begin, self.jc, self.t_mode,
                         self.seed & 0xFFFFFFFFFFFFFFFF, self.seq_id_base & 0xFFFFFFFF, self.bound,
-                        self.sample_stride, self.norm_eps, 0)
+                        self.sample_stride, self.norm_eps, self.retain_samples)
 
 
 def _ptr(t: Optional[torch.Tensor], name: str, dtypes=None, shape=None, allow_none=False):

@@ -23,7 +23,8 @@ static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 constexpr int64_t kMaxDwBatch = 8;
 
-size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
+size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
+                        Workspace* samples) {
   const int64_t P = (int64_t)dm.B * dm.L;
   const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
   const int64_t nvt = (dm.V + kVocabTile - 1) / kVocabTile;
@@ -32,9 +33,12 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   const int64_t per_split = NP * dm.d * 4;
   const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t(4) << 30) / per_split));
   // samples per dW GEMM: amortises the fp32 read-modify-write of dW over
-  // several samples while keeping H_c^T and dZ^T within about 16 GB
+  // several samples while keeping H_c^T and dZ^T within about 16 GB; with
+  // every sample retained, all n_t samples form one batch
   const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2;
-  const int64_t dw_batch = std::max<int64_t>(1, std::min<int64_t>(kMaxDwBatch, (int64_t(16) << 30) / per_sample));
+  const int64_t dw_batch =
+      retain ? dm.n_t
+             : std::max<int64_t>(1, std::min<int64_t>(kMaxDwBatch, (int64_t(16) << 30) / per_sample));
   const int64_t KT = dw_batch * NP;
 
   size_t off = 0;
@@ -44,26 +48,29 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
     off = align_up(off + bytes, 256);
     return p;
   };
+  // the state of one sample: masks and rows, log-sum-exp partials, H_c, dZ
+  auto take_sample = [&](Workspace& w) {
+    w.meta = static_cast<SampleMeta*>(take(sizeof(SampleMeta)));
+    w.idx = static_cast<int32_t*>(take(P * 4));
+    w.row_tgt = static_cast<int32_t*>(take(NP * 4));
+    w.row_seq = static_cast<int32_t*>(take(NP * 4));
+    w.seg_off = static_cast<int32_t*>(take((dm.B + 1) * 4));
+    w.t24 = static_cast<uint32_t*>(take(dm.B * 4));
+    w.ztgt = static_cast<float*>(take(NP * 4));
+    w.lse2 = static_cast<float*>(take(NP * 4));
+    w.lp = static_cast<float*>(take(NP * 4));
+    w.row_scale = static_cast<float*>(take(NP * 4));
+    w.inv_rms = static_cast<float*>(take(NP * 4));
+    w.part_m = static_cast<float*>(take(nvt * NP * 4));
+    w.part_s = static_cast<float*>(take(nvt * NP * 4));
+    w.Hc = static_cast<uint16_t*>(take(NP * dm.d * 2));
+    w.dZ = static_cast<uint16_t*>(take(NP * dm.V * 2));
+  };
   Workspace w;
-  w.meta = static_cast<SampleMeta*>(take(sizeof(SampleMeta)));
-  w.idx = static_cast<int32_t*>(take(P * 4));
-  w.row_tgt = static_cast<int32_t*>(take(NP * 4));
-  w.row_seq = static_cast<int32_t*>(take(NP * 4));
-  w.seg_off = static_cast<int32_t*>(take((dm.B + 1) * 4));
-  w.t24 = static_cast<uint32_t*>(take(dm.B * 4));
-  w.ztgt = static_cast<float*>(take(NP * 4));
-  w.lse2 = static_cast<float*>(take(NP * 4));
-  w.lp = static_cast<float*>(take(NP * 4));
-  w.row_scale = static_cast<float*>(take(NP * 4));
   w.dbar = static_cast<double*>(take(dm.B * 8));
-  w.inv_rms = static_cast<float*>(take(NP * 4));
   w.gpart = static_cast<float*>(take((NP / 256) * dm.d * 4));
-  w.part_m = static_cast<float*>(take(nvt * NP * 4));
-  w.part_s = static_cast<float*>(take(nvt * NP * 4));
-  w.Hc = static_cast<uint16_t*>(take(NP * dm.d * 2));
   w.HcT = static_cast<uint16_t*>(take(KT * dm.d * 2));
   w.WT = static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2));
-  w.dZ = static_cast<uint16_t*>(take(NP * dm.V * 2));
   w.dZT = static_cast<uint16_t*>(take(KT * dm.V * 2));
   w.dx_part = static_cast<float*>(take(n_split * NP * dm.d * 4));
   w.P = P;
@@ -72,6 +79,13 @@ size_t workspace_layout(const Dims& dm, void* base, Workspace* ws) {
   w.n_split = n_split;
   w.dw_batch = dw_batch;
   w.KT = KT;
+  take_sample(w);
+  for (int j = 1; retain && j < dm.n_t; ++j) {
+    Workspace sj = w;
+    take_sample(sj);
+    if (samples) samples[j] = sj;
+  }
+  if (samples) samples[0] = w;
   if (ws) *ws = w;
   return off;
 }
@@ -129,7 +143,8 @@ static int check_problem(const bgpo_problem* p) {
       (int64_t)p->j_begin + p->j_count > p->n_t || (p->t_mode != BGPO_T_IID && p->t_mode != BGPO_T_STRATIFIED) ||
       p->bound < BGPO_BOUND_PAPER || p->bound > BGPO_BOUND_EXACT || p->d < 1 || p->V < 1 ||
       p->sample_stride < 0 || p->sample_stride % 8 || !isfinite(p->norm_eps) || p->norm_eps < 0.f ||
-      p->reserved != 0)
+      (p->retain_samples != 0 && p->retain_samples != 1) ||
+      (p->retain_samples && p->bound != BGPO_BOUND_EXACT))
     return BGPO_ERR_INVALID_ARG;
   if (p->B > 4096 || (int64_t)p->B * p->L > (1 << 20) || p->d % 64 || p->V % 64 || p->d < 64 ||
       p->d > 65536 || p->V < 64 || p->V > (1 << 20))
@@ -166,20 +181,21 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
                               const uint8_t* resp, const float* adv, const double* ell_old,
                               double loss_scale, double* ell, double* g, double* loss,
                               int32_t* n_masked, float* t_out, int32_t* flags, bool backward,
-                              bool first_in_batch, const double* dbar, hipStream_t s) {
+                              bool store_u, const SampleMeta* prev, const double* dbar,
+                              hipStream_t s) {
   const Dims dm = dims_of(p);
   BGPO_TRY(tm.begin(BGPO_K_MASK));
   BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, p->t_mode, p->seed,
                                p->seq_id_base, ws.idx, ws.row_tgt, ws.row_seq, ws.seg_off, ws.t24,
                                ws.meta, n_masked + j, dm.n_t, t_out ? t_out + j : nullptr, dm.n_t,
-                               (int)ws.NP, dm.V, first_in_batch ? 1 : 0, dx_plan(dm, ws, grid), s));
+                               (int)ws.NP, dm.V, prev, dx_plan(dm, ws, grid), s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
   if (act.gamma) BGPO_TRY(launch_row_rms(act.at(j), ws, dm.d, act.eps, s));
   BGPO_TRY(launch_gather(act.at(j), act.gamma, ws, dm.d, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_FWD));
-  BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, backward, s));
+  BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, store_u, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_ELL));
   BGPO_TRY(launch_target_logit(ws, dm.d, s));
@@ -220,7 +236,7 @@ int bgpo_workspace_size(const bgpo_problem* prob, size_t* bytes) {
   const int st = check_problem(prob);
   if (st != BGPO_OK) return st;
   if (!bytes) return BGPO_ERR_INVALID_ARG;
-  *bytes = workspace_layout(dims_of(prob), nullptr, nullptr);
+  *bytes = workspace_layout(dims_of(prob), prob->retain_samples, nullptr, nullptr, nullptr);
   return BGPO_OK;
 }
 
@@ -231,7 +247,7 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
   if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
   if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, prob->t_mode,
                           prob->seed, prob->seq_id_base, idx, nullptr, nullptr, nullptr, nullptr,
-                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, 1, DxPlan{1, 1, 1, 1},
+                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, nullptr, DxPlan{1, 1, 1, 1},
                           (hipStream_t)stream) != hipSuccess)
     return BGPO_ERR_HIP;
   return BGPO_OK;
@@ -241,13 +257,81 @@ static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 static int check_workspace(const bgpo_problem* prob, void* workspace, size_t ws_bytes) {
   if (!workspace || ((uintptr_t)workspace % 256) != 0) return BGPO_ERR_WORKSPACE;
-  if (ws_bytes < workspace_layout(dims_of(prob), nullptr, nullptr)) return BGPO_ERR_WORKSPACE;
+  if (ws_bytes < workspace_layout(dims_of(prob), prob->retain_samples, nullptr, nullptr, nullptr))
+    return BGPO_ERR_WORKSPACE;
   return BGPO_OK;
 }
 
 }  // extern "C"
 
 namespace bgpo {
+
+// the gradient part of one sample once its scale is known: dZ, dX (with the
+// norm backward), leaving its dZ^T columns for the batch's dW GEMM
+static int sample_backward(const Workspace& ws, const Act& act, int j, int j_begin,
+                           const uint16_t* W_head, float* dX, float* dgamma, const Dims& dm,
+                           int grid, Timer& tm, hipStream_t s) {
+  BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
+  BGPO_TRY(launch_softmax_grad(ws, dm.V, s));
+  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.begin(BGPO_K_DX));
+  BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
+  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
+  float* dXj = dX + (int64_t)(j - j_begin) * act.stride;
+  if (act.gamma)
+    BGPO_TRY(launch_dx_reduce_rmsnorm(ws, act.at(j), act.gamma, dXj, dgamma, dm.d, s));
+  else
+    BGPO_TRY(launch_dx_reduce(ws, dXj, dm.d, s));
+  BGPO_TRY(tm.end());
+  return BGPO_OK;
+}
+
+// The exact objective with every sample's state retained (the way an
+// implementation that keeps all n_t computational graphs works): each
+// forward runs once and keeps its exponentials, the mean log-ratio is formed,
+// then every sample's gradient comes from its kept state; memory grows with
+// n_t.
+static int bwd_retained(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
+                        const int32_t* targets, const uint8_t* resp_mask, const float* adv,
+                        const double* ell_old, double loss_scale, float* dX, float* dgamma,
+                        float* dW, double* ell, double* g, double* loss, int32_t* n_masked,
+                        float* t_out, int32_t* status_flags, void* workspace, int grid, Timer& tm,
+                        hipStream_t s) {
+  const Dims dm = dims_of(prob);
+  std::vector<Workspace> S(dm.n_t);
+  Workspace ws;
+  workspace_layout(dm, 1, workspace, &ws, S.data());
+  BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
+  BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
+  BGPO_TRY(tm.end());
+  for (int j = 0; j < dm.n_t; ++j) {
+    const int st = run_forward_sample(prob, S[j], tm, grid, j, act, targets, resp_mask, nullptr,
+                                      nullptr, 0.0, ell, nullptr, nullptr, n_masked, t_out,
+                                      status_flags, false, true, j ? S[j - 1].meta : nullptr,
+                                      nullptr, s);
+    if (st != BGPO_OK) return st;
+  }
+  const double* dbar = nullptr;
+  if (ell_old) {
+    BGPO_TRY(tm.begin(BGPO_K_ELL));
+    BGPO_TRY(launch_mean_ratio(ell, ell_old, dm.B, dm.n_t, ws.dbar, s));
+    BGPO_TRY(tm.end());
+    dbar = ws.dbar;
+  }
+  for (int j = 0; j < dm.n_t; ++j) {
+    BGPO_TRY(tm.begin(BGPO_K_ELL));
+    BGPO_TRY(launch_seq_terms(S[j], dm.B, dm.n_t, j, adv, ell_old, loss_scale, ell, g, loss,
+                              status_flags, true, prob->bound, dbar, s));
+    BGPO_TRY(tm.end());
+    const int st = sample_backward(S[j], act, j, 0, W_head, dX, dgamma, dm, grid, tm, s);
+    if (st != BGPO_OK) return st;
+  }
+  BGPO_TRY(tm.begin(BGPO_K_DW));
+  BGPO_TRY(launch_gemm_dw(S[dm.n_t - 1], dW, dm.d, dm.V, grid, s));
+  BGPO_TRY(tm.end());
+  return BGPO_OK;
+}
 
 static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
                          const int32_t* targets, const uint8_t* resp_mask, double* ell,
@@ -262,7 +346,9 @@ static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
   if (prob->j_count == 0) return BGPO_OK;
   hipStream_t s = (hipStream_t)stream;
   Workspace ws;
-  workspace_layout(dims_of(prob), workspace, &ws);
+  // the layout the workspace was checked against (with retain_samples the
+  // first sample's state and the shared buffers; one sample at a time)
+  workspace_layout(dims_of(prob), prob->retain_samples, workspace, &ws, nullptr);
   int grid = 0;
   if ((st = device_grid(&grid)) != BGPO_OK) return st;
   Timer tm(prof, s);
@@ -271,8 +357,8 @@ static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
   BGPO_TRY(tm.end());
   for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
     st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, nullptr, nullptr, 0.0,
-                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, true, nullptr,
-                            s);
+                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, false, nullptr,
+                            nullptr, s);
     if (st != BGPO_OK) return st;
   }
   BGPO_TRY(tm.finish());
@@ -300,11 +386,18 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
   if (prob->j_count == 0) return BGPO_OK;
   hipStream_t s = (hipStream_t)stream;
   const Dims dm = dims_of(prob);
-  Workspace ws;
-  workspace_layout(dm, workspace, &ws);
   int grid = 0;
   if ((st = device_grid(&grid)) != BGPO_OK) return st;
   Timer tm(prof, s);
+  if (prob->retain_samples) {
+    st = bwd_retained(prob, act, W_head, targets, resp_mask, adv, ell_old, loss_scale, dX, dgamma,
+                      dW, ell, g, loss, n_masked, t_out, status_flags, workspace, grid, tm, s);
+    if (st != BGPO_OK) return st;
+    BGPO_TRY(tm.finish());
+    return BGPO_OK;
+  }
+  Workspace ws;
+  workspace_layout(dm, 0, workspace, &ws, nullptr);
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
   BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
@@ -315,7 +408,7 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
     for (int j = 0; j < prob->n_t; ++j) {
       st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, nullptr, nullptr,
                               0.0, ell, nullptr, nullptr, n_masked, t_out, status_flags, false,
-                              true, nullptr, s);
+                              false, nullptr, nullptr, s);
       if (st != BGPO_OK) return st;
     }
     BGPO_TRY(tm.begin(BGPO_K_ELL));
@@ -328,22 +421,11 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
     const int j1 = std::min<int>(j_end, j0 + (int)ws.dw_batch);
     for (int j = j0; j < j1; ++j) {
       st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, adv, ell_old,
-                              loss_scale, ell, g, loss, n_masked, t_out, status_flags, true,
-                              j == j0, dbar, s);
+                              loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, true,
+                              j == j0 ? nullptr : ws.meta, dbar, s);
       if (st != BGPO_OK) return st;
-      BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
-      BGPO_TRY(launch_softmax_grad(ws, dm.V, s));
-      BGPO_TRY(tm.end());
-      BGPO_TRY(tm.begin(BGPO_K_DX));
-      BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
-      BGPO_TRY(tm.end());
-      BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
-      float* dXj = dX + (int64_t)(j - prob->j_begin) * act.stride;
-      if (act.gamma)
-        BGPO_TRY(launch_dx_reduce_rmsnorm(ws, act.at(j), act.gamma, dXj, dgamma, dm.d, s));
-      else
-        BGPO_TRY(launch_dx_reduce(ws, dXj, dm.d, s));
-      BGPO_TRY(tm.end());
+      st = sample_backward(ws, act, j, prob->j_begin, W_head, dX, dgamma, dm, grid, tm, s);
+      if (st != BGPO_OK) return st;
     }
     // one dW GEMM for the batch: K runs over the batch's samples side by side
     BGPO_TRY(tm.begin(BGPO_K_DW));

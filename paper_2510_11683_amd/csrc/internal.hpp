@@ -69,7 +69,14 @@ struct Dims {
   int B, L, d, V, n_t;
 };
 
-size_t workspace_layout(const Dims& dm, void* base, Workspace* ws);  // base may be NULL
+// Views into the caller's workspace (base may be NULL: sizes only).
+// retain = 0: the state of one sample at a time, dW batches of up to
+//             kMaxDwBatch samples; the size does not depend on n_t.
+// retain = 1: the state of every one of the n_t samples is kept
+//             (samples[0 .. n_t), each with its own meta, rows, partials, H_c
+//             and dZ; H_c^T / dZ^T hold all samples' columns; one dW batch).
+size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
+                        Workspace* samples);
 
 // ---- launchers (return hipSuccess or the launch error) ----
 hipError_t launch_transpose_w(const uint16_t* W, uint16_t* WT, int d, int V, hipStream_t s);
@@ -78,7 +85,7 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
                                SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
                                float* t_out, int t_stride, int row_cap, int V,
-                               int first_in_batch, const DxPlan& plan, hipStream_t s);
+                               const SampleMeta* prev, const DxPlan& plan, hipStream_t s);
 hipError_t launch_row_rms(const uint16_t* x, const Workspace& ws, int d, float eps, hipStream_t s);
 hipError_t launch_gather(const uint16_t* hidden, const float* gamma, const Workspace& ws, int d,
                          hipStream_t s);

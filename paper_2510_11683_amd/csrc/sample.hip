@@ -68,9 +68,9 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     const uint8_t* __restrict__ resp, const int32_t* __restrict__ targets, int B, int L, int n_t,
     int j, int t_mode, uint32_t k0, uint32_t k1, uint32_t seq_base, int32_t* __restrict__ idx,
     int32_t* __restrict__ row_tgt, int32_t* __restrict__ row_seq, int32_t* __restrict__ seg_off,
-    uint32_t* __restrict__ t24_out, SampleMeta* __restrict__ meta, int32_t* __restrict__ nm_out,
+    uint32_t* __restrict__ t24_out, SampleMeta* meta, int32_t* __restrict__ nm_out,
     int nm_stride, float* __restrict__ t_out, int t_stride, int row_cap, int V,
-    int first_in_batch, DxPlan plan) {
+    const SampleMeta* prev, DxPlan plan) {
   __shared__ uint32_t sT[kMaxB];
   __shared__ int32_t sSeg[kMaxB + 1];
   __shared__ int32_t sWave[kMaskThreads / 64];
@@ -143,8 +143,9 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     if (meta) {
       meta->n_rows = total;
       meta->n_rows_pad = total_pad;
-      // this sample's columns in H_c^T / dZ^T follow the previous sample's
-      const int off = first_in_batch ? 0 : meta->col_end;
+      // this sample's columns in H_c^T / dZ^T follow those of the previous
+      // sample of the dW batch (prev may be this same record: read first)
+      const int off = prev ? prev->col_end : 0;
       meta->col_off = off;
       meta->col_end = off + (total + 63) / 64 * 64;
       choose_dx_split(total_pad / kRowPad, plan, &meta->dx_split, &meta->dx_kslab);
@@ -164,12 +165,12 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
                                SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
                                float* t_out, int t_stride, int row_cap, int V,
-                               int first_in_batch, const DxPlan& plan, hipStream_t s) {
+                               const SampleMeta* prev, const DxPlan& plan, hipStream_t s) {
   k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, t_mode,
                                             (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
                                             seq_base, idx, row_tgt, row_seq, seg_off, t24, meta,
                                             n_masked_out, nm_stride, t_out, t_stride, row_cap, V,
-                                            first_in_batch, plan);
+                                            prev, plan);
   return hipGetLastError();
 }
 

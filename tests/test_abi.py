@@ -123,13 +123,48 @@ def test_problem_struct_layout(b):
     assert b._Problem.norm_eps.offset == 56
 
 
+def test_retained_workspace_grows_linearly_with_n_t(b):
+    sizes = [b.bgpo_workspace_size(_prob(b, n_t=n, bound=3, retain_samples=1)) for n in (1, 2, 4, 16, 64)]
+    per = sizes[1] - sizes[0]
+    assert per > 2 * 10 ** 9                       # H_c^T, dZ^T columns + state, B8 L512 head
+    for n, sz in zip((1, 2, 4, 16, 64), sizes):
+        assert sz == sizes[0] + (n - 1) * per
+    assert b.bgpo_workspace_size(_prob(b, n_t=64, bound=3)) < sizes[3]   # constant mode, any n_t
+
+
+def test_every_entry_point_lays_out_what_it_checked(b):
+    """One byte short of bgpo_workspace_size() is refused, for the retained
+    and the constant layouts alike; the entry points then use the layout they
+    checked (workspace_layout with the problem's retain flag, or the fixed
+    layout of a branch taken only for that flag), so an accepted workspace is
+    never overrun."""
+    lib = b._lib
+    fake = ctypes.c_void_p(0x1000)
+    for retain in (0, 1):
+        pr = _prob(b, B=2, L=64, d=128, V=1024, n_t=4, bound=3, retain_samples=retain, j_begin=1,
+                   j_count=2).c()
+        n = ctypes.c_size_t(0)
+        assert lib.bgpo_workspace_size(ctypes.byref(pr), ctypes.byref(n)) == 0
+        ws = ctypes.c_void_p(0x100000)
+        # one byte short: refused before anything is enqueued
+        assert lib.bgpo_elbo_fwd(ctypes.byref(pr), fake, fake, fake, fake, fake, fake, None, ws,
+                                 n.value - 1, None, None) == -2
+    src = open(os.path.join(ROOT, "paper_2510_11683_amd", "csrc", "api.hip")).read()
+    # every layout call that sits next to a checked workspace uses the problem's flag or the
+    # retained / constant layout of its own branch
+    calls = re.findall(r"workspace_layout\(([^;]*)\);", src)
+    assert all("retain_samples" in c or ", 1," in c or ", 0," in c for c in calls), calls
+    assert any("prob->retain_samples, workspace" in c for c in calls)
+
+
 def test_reserved_field_and_rmsnorm_arguments_rejected_before_hip(b):
     lib = b._lib
     fake = ctypes.c_void_p(0x1000)
     nbytes = ctypes.c_size_t(0)
-    q = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
-    q.reserved = 1
-    assert lib.bgpo_workspace_size(ctypes.byref(q), ctypes.byref(nbytes)) == -1
+    for bound, retain in ((0, 1), (3, 2), (3, -1)):        # retain needs the exact bound, 0 or 1
+        q = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
+        q.bound, q.retain_samples = bound, retain
+        assert lib.bgpo_workspace_size(ctypes.byref(q), ctypes.byref(nbytes)) == -1
     p = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
     assert lib.bgpo_workspace_size(ctypes.byref(p), ctypes.byref(nbytes)) == 0
     ws = ctypes.c_void_p(0x100000)

@@ -168,6 +168,39 @@ def test_every_bound_mode_identical_on_policy():
         assert o["loss"] == outs[0]["loss"]
 
 
+def test_retained_exact_mode_matches_oracle_and_two_pass_mode():
+    """retain_samples = 1 keeps every sample's state instead of running the
+    forward twice: same oracle parity, and the same l, g, loss and dX as the
+    two-pass mode bit for bit (identical kernels in the same order); dW differs
+    only by the order of its fp32 accumulation (one batch of all samples)."""
+    from paper_2510_11683_amd import bgpo
+    w = MID
+    x = workloads.generate(w)
+    op = dataclasses.replace(_oracle_problem(w), bound=3)
+    ell_old = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                                backward=False).ell
+    ell_old = ell_old + np.random.default_rng(7).normal(0, 1.0, ell_old.shape)
+    ref = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                            ell_old=ell_old, loss_scale=0.25)
+    outs = []
+    for retain in (0, 1):
+        r = Runner(w, x)
+        pr = dataclasses.replace(problem(w, bound=3), retain_samples=retain)
+        r.ws = bgpo.alloc_workspace(pr)
+        d = r.dev
+        eo = torch.as_tensor(ell_old, dtype=torch.float64).cuda()
+        bgpo.bgpo_elbo_bwd_accumulate(pr, d["hidden"], d["W"], d["targets"], d["resp_mask"],
+                                      d["adv"], eo, 0.25, r.dX, r.dW, r.ell, r.g, r.loss, r.nm,
+                                      r.t, r.flags, r.ws)
+        outs.append(r.out())
+    two, ret = outs
+    _check_against_oracle(w, ret, ref, range(w.n_t), x["adv"], ell_old, 0.25, 3)
+    for k in ("ell", "g", "nm", "t", "dX"):
+        assert np.array_equal(two[k], ret[k]), k
+    assert two["loss"] == ret["loss"]
+    assert rel_maxnorm(ret["dW"], two["dW"]) <= 1e-5
+
+
 def test_exact_mode_partial_range_refused():
     w = MID
     x = workloads.generate(w, with_weights=True)
