@@ -6,8 +6,10 @@ sampled outputs.
   l_{b,j} and g_{b,j}, the loss, dX on sampled positions and dW on sampled
   vocabulary columns (random ones plus the most frequent target tokens, whose
   columns carry the one-hot term and the largest entries).
-* B=16, L=1024, stratified t (the largest workload), first three samples: the
-  same checks on the rows those samples mask.
+* B=8, L=256, n_t=16 and B=8, L=512 with ragged lengths, n_t=16: the same
+  checks over all samples.
+* B=16, L=1024, stratified t (the largest workload), all 32 samples: the same
+  checks.
 The oracle's collapsed form runs the log-softmax once per masked position in
 float64, so these tests take tens of seconds of host time.
 """
@@ -87,6 +89,13 @@ def test_llada_head_B8_L512_nt64_all_samples():
     assert n > 100_000
 
 
-def test_largest_workload_B16_L1024_stratified_first_samples():
-    n = _run_and_compare(workloads.STRESS_L1024, 0, 3, seqs=(3, 12))
+@pytest.mark.parametrize("w", [workloads.LLADA_L256, workloads.LLADA_L512_RAGGED], ids=lambda w: w.name)
+def test_llada_head_nt16_all_samples(w):
+    n = _run_and_compare(w, 0, w.n_t, seqs=(2, 7))
+    assert n > 0
+
+
+def test_largest_workload_B16_L1024_stratified_all_samples():
+    w = workloads.STRESS_L1024
+    n = _run_and_compare(w, 0, w.n_t, seqs=(3, 12))
     assert n > 0
