@@ -172,10 +172,11 @@ __device__ __forceinline__ void sched_pattern() {
 #if defined(__HIP_DEVICE_COMPILE__)
   if constexpr (I < MF) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // MFMA
-    // fragment reads first (one per MFMA slot, so the next sub-step's operands
-    // land well before it starts), slab loads spread over the whole step
+    // fragment reads and slab loads both spread evenly over the step's MFMA
+    // slots (measured: front-loading the reads made no difference for the
+    // forward and cost 2-3 % of MFMA-busy cycles in the dX and dW GEMMs)
     constexpr int v = (I + 1) * NV / MF - I * NV / MF;
-    constexpr int d = I < ND ? 1 : 0;
+    constexpr int d = (I + 1) * ND / MF - I * ND / MF;
     if constexpr (d > 0) __builtin_amdgcn_sched_group_barrier(0x100, d, 0);   // DS read
     if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);   // VMEM read
     sched_pattern<I + 1, MF, NV, ND>();
