@@ -45,44 +45,62 @@ hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s) {
   return hipGetLastError();
 }
 
-// One wave per row: lanes stride over the vocabulary-tile partials.
-__global__ __launch_bounds__(256) void k_combine_rows(const float* __restrict__ part_m,
-                                                      const float* __restrict__ part_s,
-                                                      const float* __restrict__ ztgt,
-                                                      const SampleMeta* __restrict__ meta,
-                                                      float* __restrict__ lse2, float* __restrict__ lp,
-                                                      int nvt, int64_t ldp) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= meta->n_rows) return;
-  float m = -INFINITY, s = 0.f;
-  for (int t = lane; t < nvt; t += 64) {
-    const float mt = part_m[(int64_t)t * ldp + row], st = part_s[(int64_t)t * ldp + row];
-    if (st > 0.f) {
-      const float mn = fmaxf(m, mt);
-      s = s * exp2f(m - mn) + st * exp2f(mt - mn);
-      m = mn;
+// log-sum-exp of every row from its per-slice (max, sum) partials, and the
+// target's log p.  64 rows per workgroup, one per lane, so each load of a
+// slice's partials is 64 consecutive floats; the 16 waves take every 16th
+// slice, 8 slices' loads in flight at a time, and are combined in LDS in a
+// fixed order.
+constexpr int kCombineWaves = 16;
+
+__global__ __launch_bounds__(64 * kCombineWaves) void k_combine_rows(
+    const float* __restrict__ part_m, const float* __restrict__ part_s,
+    const float* __restrict__ ztgt, const SampleMeta* __restrict__ meta,
+    float* __restrict__ lse2, float* __restrict__ lp, int nvt, int64_t ldp) {
+  __shared__ float sm[kCombineWaves][64], ss[kCombineWaves][64];
+  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int row = blockIdx.x * 64 + lane;
+  const int n_rows = meta->n_rows;
+  if (blockIdx.x * 64 >= n_rows) return;
+  float m = -INFINITY, sum = 0.f;
+  if (row < n_rows) {
+    for (int t0 = q; t0 < nvt; t0 += kCombineWaves * 8) {
+      float mt[8], st[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int t = t0 + kCombineWaves * k;
+        mt[k] = t < nvt ? part_m[(int64_t)t * ldp + row] : -INFINITY;
+        st[k] = t < nvt ? part_s[(int64_t)t * ldp + row] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (st[k] > 0.f) {
+          const float mn = fmaxf(m, mt[k]);
+          sum = sum * exp2f(m - mn) + st[k] * exp2f(mt[k] - mn);
+          m = mn;
+        }
+      }
     }
   }
+  sm[q][lane] = m;
+  ss[q][lane] = sum;
+  __syncthreads();
+  if (q == 0 && row < n_rows) {
+    float M = -INFINITY;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const float mo = __shfl_xor(m, off, 64), so = __shfl_xor(s, off, 64);
-    const float mn = fmaxf(m, mo);
-    const float a = s > 0.f ? s * exp2f(m - mn) : 0.f;
-    const float b = so > 0.f ? so * exp2f(mo - mn) : 0.f;
-    s = a + b;
-    m = mn;
-  }
-  if (lane == 0) {
-    const float l2 = m + log2f(s);
+    for (int k = 0; k < kCombineWaves; ++k) M = fmaxf(M, sm[k][lane]);
+    float S = 0.f;
+#pragma unroll
+    for (int k = 0; k < kCombineWaves; ++k)
+      if (ss[k][lane] > 0.f) S += ss[k][lane] * exp2f(sm[k][lane] - M);
+    const float l2 = M + log2f(S);
     lse2[row] = l2;
     lp[row] = ztgt[row] - l2 * kLn2;
   }
 }
 
 hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s) {
-  k_combine_rows<<<(unsigned)(ws.NP / 4), 256, 0, s>>>(ws.part_m, ws.part_s, ws.ztgt, ws.meta,
-                                                      ws.lse2, ws.lp, (int)ws.nvt, ws.NP);
+  k_combine_rows<<<(unsigned)(ws.NP / 64), 64 * kCombineWaves, 0, s>>>(
+      ws.part_m, ws.part_s, ws.ztgt, ws.meta, ws.lse2, ws.lp, (int)ws.nvt, ws.NP);
   return hipGetLastError();
 }
 
