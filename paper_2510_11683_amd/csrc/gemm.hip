@@ -242,12 +242,34 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
     const int mw = m0 + wm * WM, nw = n0 + wn * WN;
     const int mlane = 4 * (lane >> 5);
     f32x16 acc[TM][TN];
+    // dW accumulates in place: a full tile starts from the current output
+    // (buffer loads issued before the slab loads, so the wait for the first
+    // slab covers them) and ends with plain stores; a partial tile starts
+    // from zero and adds in its epilogue
+    const bool preload = EPI == EPI_F32_ACCUM && m0 + BM <= M && n0 + BN <= N;
+    if (preload) {
+      const float* src = p.out + (int64_t)split * p.split_stride + (int64_t)m0 * p.ldo + n0;
+      const __amdgpu_buffer_rsrc_t o_rsrc =
+          __builtin_amdgcn_make_buffer_rsrc((void*)src, (short)0, 0x7FFFFFFF, 0x00020000);
+      const int lane_off = ((mw - m0 + mlane) * (int)p.ldo + (nw - n0) + (lane & 31)) * 4;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+          for (int e = 0; e < 16; ++e)
+            acc[i][j][e] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(
+                           o_rsrc, lane_off,
+                           ((32 * i + (e & 3) + 8 * (e >> 2)) * (int)p.ldo + 32 * j) * 4, 0));
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    }
 
     // Operand panels as buffer resources (wave-uniform): rows [m0, m0 + BM) of A
     // and [n0, n0 + BN) of B.  Each load instruction moves 64 lanes x 16 bytes
@@ -425,11 +447,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
         }
       }
     } else {
-      // fp32 store (dX partials) or read-modify-write accumulate (dW); one
-      // 32-row band of the wave tile at a time keeps the loads in flight
-      // without spilling.
+      // fp32 store of the tile (dX partials, or a full dW tile that started
+      // from its previous value), or read-modify-write of a partial dW tile;
+      // one 32-row band of the wave tile at a time.
       float* outb = p.out + (int64_t)split * p.split_stride;
-      if (m0 + BM <= M && n0 + BN <= N) epi_f32<EPI == EPI_F32_ACCUM, true, TM, TN>(acc, outb, p.ldo, mw, nw, mlane, lane, M, N);
+      if (m0 + BM <= M && n0 + BN <= N) epi_f32<false, true, TM, TN>(acc, outb, p.ldo, mw, nw, mlane, lane, M, N);
       else epi_f32<EPI == EPI_F32_ACCUM, false, TM, TN>(acc, outb, p.ldo, mw, nw, mlane, lane, M, N);
     }
     __syncthreads();
