@@ -1,13 +1,15 @@
 // Host orchestration and the C ABI of libbgpo.
 //
 // One call walks the Monte-Carlo samples j of its range in order (Algorithm 1,
-// inner loop): draw t and the mask, compact and gather the masked rows, run the
-// fused LM-head forward (which, with backward, also keeps the exponentials of
-// the logits), form l, d, g and the gradient scale, turn the exponentials into
-// dZ = s (softmax - onehot) and accumulate dX and dW before the
-// next sample starts.  All buffers are views into the caller's workspace,
-// sized by B, L, d and V; nothing depends on n_t, so device memory is the same
-// for any number of samples.
+// inner loop): draw t and the mask, compact and gather the masked rows (through
+// the final RMSNorm for the _rmsnorm calls), run the fused LM-head forward
+// (which, with backward, also keeps the exponentials of the logits), form l,
+// d, g and the gradient scale, turn the exponentials into
+// dZ = s (softmax - onehot) and accumulate dX before the next sample starts;
+// dW is accumulated once per batch of samples.  All buffers are views into the
+// caller's workspace, sized by B, L, d and V; nothing depends on n_t, so
+// device memory is the same for any number of samples (except in the
+// retained-state contrast mode of the exact objective).
 #include <math.h>
 #include <string.h>
 

@@ -4,22 +4,25 @@
 //     C[m][n] = sum_k A[m][k] * B[n][k]      (A, B row-major, K contiguous),
 // so both operands load as 16-byte K-contiguous vectors that match the
 // v_mfma_f32_32x32x16_bf16 operand layout directly:
-//   forward / recompute   Z^T[v][row] = WT[v][:] . Hc[row][:]     (K = d)
+//   forward               Z^T[v][row] = WT[v][:] . Hc[row][:]     (K = d)
 //   dX (split over V)     dX[row][c]  = dZ[row][:] . W[c][:]      (K = V)
 //   dW                    dW[c][v]   += HcT[c][:] . dZT[v][:]     (K = rows)
 // The logits are produced as Z^T (vocabulary along M) so that, in the 32x32
 // accumulator layout, each lane holds 64 vocabulary entries of only 4 rows:
 // the per-row max / sum-exp reductions are in-lane plus one lane swap.
 //
-// Scheduling: a persistent grid of one 256-thread workgroup per compute unit
-// walks the tile list; consecutive tiles (sharing an operand panel) are given
-// to workgroups of the same XCD (workgroup w runs on XCD w mod 8), so the
-// shared panel is served from that XCD's L2.
+// Scheduling: a persistent grid of one 512-thread workgroup (eight waves, two
+// per SIMD) per compute unit walks the tile list in bands of M tiles;
+// consecutive tiles (sharing operand panels) go to workgroups of the same XCD
+// (workgroup w runs on XCD w mod 8), so the shared panels are served from that
+// XCD's L2.
 //
-// Pipeline: two LDS stages; the next K slab is loaded into registers while
-// the current one feeds the MFMAs, then written to the other stage.  LDS rows
-// are XOR-swizzled in 16-byte chunks so that the fragment reads of 8
-// consecutive rows hit distinct banks.
+// Pipeline: a two-stage LDS ring of 64-deep K slabs, filled by direct
+// buffer-to-LDS loads (no staging registers); a stage is refilled with the
+// slab two ahead as soon as the barrier that ends its last use has passed.
+// LDS rows are XOR-swizzled in 16-byte chunks so that fragment reads of
+// consecutive rows hit distinct banks.  Fragment reads for the next K
+// sub-step and the slab loads are spread evenly between the MFMAs.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -73,8 +76,8 @@ struct Cfg {
   }
 };
 
-// fp32 store (dX partials) or read-modify-write accumulate (dW), one 32-row
-// band of the wave tile at a time so the loads stay in flight without spills.
+// fp32 store of a wave tile (ACCUM: read-modify-write), one 32-row band at a
+// time so the loads stay in flight without spills.
 template <bool ACCUM, bool FULL, int TM, int TN>
 __device__ __forceinline__ void epi_f32(const f32x16 (&acc)[TM][TN], float* outb, int64_t ldo,
                                         int mw, int nw, int mlane, int lane, int M, int N) {
@@ -528,7 +531,7 @@ int gemm_grid(int device) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
       cus <= 0)
     cus = 256;
-  return cus;  // one 256-thread workgroup per compute unit
+  return cus;  // one workgroup per compute unit
 }
 
 }  // namespace bgpo
