@@ -210,6 +210,43 @@ def test_exact_mode_partial_range_refused():
         r.bwd(j_begin=1, j_count=1, bound=3)
 
 
+@pytest.mark.parametrize("w_std", [0.2, 0.5], ids=["logit_std_4.8", "logit_std_12"])
+def test_mid_parity_peaky_logits(w_std):
+    """Trained heads give far peakier softmaxes than N(0, 0.02) weights: with
+    W ~ N(0, w_std^2) the logits have std w_std * sqrt(d), most of the
+    probability sits on a few tokens and the stored exponentials of the others
+    underflow fp16; off-policy, both bound branches."""
+    w = MID.replace(w_std=w_std)
+    x = workloads.generate(w)
+    op = _oracle_problem(w)
+    ell_old = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                                backward=False).ell
+    ell_old = ell_old + np.random.default_rng(9).normal(0, 1.0, ell_old.shape)
+    ref = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                            ell_old=ell_old, loss_scale=0.25)
+    r = Runner(w, x)
+    r.bwd(ell_old=ell_old, loss_scale=0.25)
+    _check_against_oracle(w, r.out(), ref, range(w.n_t), x["adv"], ell_old, 0.25)
+
+
+@pytest.mark.parametrize("B,L,d,V,n_t", [(1, 1, 64, 64, 3), (3, 3, 64, 192, 5), (2, 70, 128, 64, 2)],
+                         ids=["B1_L1_d64_V64", "B3_L3_d64_V192", "B2_L70_d128_V64"])
+def test_smallest_shapes(B, L, d, V, n_t):
+    """The smallest supported sizes: one partial tile in every GEMM dimension,
+    a vocabulary of one 64-wide half slice, single-position responses."""
+    w = workloads.TINY.replace(B=B, L=L, d=d, V=V, n_t=n_t, adv="normal", data_seed=2100 + B * L)
+    x = workloads.generate(w)
+    op = _oracle_problem(w)
+    ell_old = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                                backward=False).ell
+    ell_old = ell_old + np.random.default_rng(10).normal(0, 0.5, ell_old.shape)
+    ref = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                            ell_old=ell_old, loss_scale=0.25)
+    r = Runner(w, x)
+    r.bwd(ell_old=ell_old, loss_scale=0.25)
+    _check_against_oracle(w, r.out(), ref, range(w.n_t), x["adv"], ell_old, 0.25)
+
+
 def test_on_policy_d_is_exactly_zero():
     """ell from the forward entry point fed back as ell_old gives d == 0 bit-exactly,
     so g = A / n_t exactly (the equivalence case)."""
