@@ -233,13 +233,11 @@ def main():
         per_kernel[k] = e
     # HBM-bound kernel classes: achieved bandwidth from the committed counter
     # bytes and from the algorithmic bytes, against the 8 TB/s peak
-    n_rows = tokens / nt                                   # masked rows per sample (mean)
-    algo_bytes = {                                         # per launch
-        "gather": 6.0 * n_rows * d,                        # read rows, write H_c and H_c^T
-        "softmax_grad": 6.0 * n_rows * V,                  # read u, write dZ and dZ^T (2 bytes each)
-        "dx_reduce": None,                                 # depends on the per-sample split count
-        "transpose_w": 4.0 * d * V,
-    }
+    def algo_bytes(k, launches):                         # per launch
+        rows = tokens / launches                         # masked rows one launch processes
+        return {"gather": 6.0 * rows * d,                # read rows, write H_c and H_c^T
+                "softmax_grad": 6.0 * rows * V,          # read u, write dZ and dZ^T (2 bytes each)
+                "transpose_w": 4.0 * d * V}.get(k)       # dx_reduce: depends on the split count
     for k, e in per_kernel.items():
         if k in GEMM_CLASSES:
             continue
@@ -248,8 +246,9 @@ def main():
         if tb is not None:
             e["counter_gbs"] = tb / secs / 1e9
             e["counter_hbm_frac"] = e["counter_gbs"] / PEAK_HBM_GBS
-        if algo_bytes.get(k):
-            e["algorithmic_gbs"] = algo_bytes[k] / secs / 1e9
+        ab = algo_bytes(k, e["launches_per_step"])
+        if ab:
+            e["algorithmic_gbs"] = ab / secs / 1e9
             e["algorithmic_hbm_frac"] = e["algorithmic_gbs"] / PEAK_HBM_GBS
     dom = max((k for k in per_kernel if k in GEMM_CLASSES), key=lambda k: per_kernel[k]["ms_per_step"])
     achieved = per_kernel[dom]["tflops"]

@@ -19,13 +19,14 @@ int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
                       int32_t K, void* stream);
 
 /* Tile-configuration variants of the same GEMM (fp32 store), for tuning:
- * variant 0: 256x256 tile, K slab 32, 4-stage LDS ring (the production one)
+ * variant 0: 256x256 tile, K slab 32, 4-stage LDS ring (four waves of 128x128)
  *         1: 5 stages, 2: K slab 64 in 2 stages,
  *         3: 256x128 tile, 3 stages, two workgroups per compute unit
  *         4: 128x256 tile, 3 stages, two workgroups per compute unit
  *         5: 256x256 tile, K slab 64, 2 stages, 8 waves of 128x64
  *         6: as 5 with 8 waves of 64x128
- *         7: as 2 with the 256-byte LDS swizzle; 8: as 5 with that swizzle
+ *         7: as 2 with the 256-byte LDS swizzle; 8: as 5 with that swizzle (the
+ *            configuration of the production kernels)
  *         9: 8 waves of 128x64, K slab 32, 4 stages; 10: as 9 with 5 stages
  *         11: as 6 with the 256-byte swizzle
  *         12: 256x128 tile, K slab 32, 3 stages, 256-byte swizzle, two

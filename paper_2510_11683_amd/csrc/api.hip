@@ -1,15 +1,21 @@
 // Host orchestration and the C ABI of libbgpo.
 //
 // One call walks the Monte-Carlo samples j of its range in order (Algorithm 1,
-// inner loop): draw t and the mask, compact and gather the masked rows (through
-// the final RMSNorm for the _rmsnorm calls), run the fused LM-head forward
-// (which, with backward, also keeps the exponentials of the logits), form l,
-// d, g and the gradient scale, turn the exponentials into
-// dZ = s (softmax - onehot) and accumulate dX before the next sample starts;
-// dW is accumulated once per batch of samples.  All buffers are views into the
-// caller's workspace, sized by B, L, d and V; nothing depends on n_t, so
-// device memory is the same for any number of samples (except in the
-// retained-state contrast mode of the exact objective).
+// inner loop), in units of up to G consecutive samples: draw t and the mask of
+// each sample of the unit, compact its masked rows after those of the unit's
+// earlier samples and gather them (through the final RMSNorm for the _rmsnorm
+// calls), run the fused LM-head forward once over the unit's rows (with
+// backward it also keeps the exponentials of the logits), form l, d, g and
+// the gradient scale of every (sample, response), turn the exponentials into
+// dZ = s (softmax - onehot), run one dX GEMM over the unit's rows and add each
+// sample's rows into dX in sample order; dW is accumulated once per unit.  The
+// samples stay independent (the bound is a sum over samples, Eq.
+// lower_bound_def): a unit only shares the GEMM launches, which saves the
+// padded rows and partly filled GEMM rounds of one sample at a time.  All
+// buffers are views into the caller's workspace, sized by B, L, d and V;
+// nothing depends on n_t, so device memory is the same for any number of
+// samples (except in the retained-state contrast mode of the exact
+// objective).
 #include <math.h>
 #include <string.h>
 
@@ -23,25 +29,30 @@ namespace bgpo {
 
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-constexpr int64_t kMaxDwBatch = 8;
+constexpr int64_t kMaxUnit = 8;
 
 size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
-                        Workspace* samples) {
+                        Workspace* units) {
   const int64_t P = (int64_t)dm.B * dm.L;
   const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
   const int64_t nvt = (dm.V + kVocabTile - 1) / kVocabTile;
+  // samples per unit: up to kMaxUnit while the unit's dZ, dZ^T, H_c and H_c^T
+  // stay within about 20 GB and its 64-row chunks within one grid dimension
+  // of the row kernels.  With every sample retained, the same units (at most
+  // n_t samples each) each keep their own state and all of them form the one
+  // dW batch, so both modes run the same unit compositions.
+  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2 * 2;
+  int64_t G = std::max<int64_t>(
+      1, std::min({kMaxUnit, (int64_t(20) << 30) / per_sample, int64_t(65535) * 64 / NP}));
+  if (retain) G = std::min<int64_t>(G, dm.n_t);
+  const int64_t n_units = retain ? (dm.n_t + G - 1) / G : 1;
+  const int64_t RP = G * NP;
   // capacity of the split-vocabulary dX partials: up to 16 splits (the mask
-  // kernel picks each sample's count), within about 4 GB
-  const int64_t per_split = NP * dm.d * 4;
+  // kernel picks each unit's count), within about 4 GB
+  const int64_t per_split = RP * dm.d * 4;
   const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t(4) << 30) / per_split));
-  // samples per dW GEMM: amortises the fp32 read-modify-write of dW over
-  // several samples while keeping H_c^T and dZ^T within about 16 GB; with
-  // every sample retained, all n_t samples form one batch
-  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2;
-  const int64_t dw_batch =
-      retain ? dm.n_t
-             : std::max<int64_t>(1, std::min<int64_t>(kMaxDwBatch, (int64_t(16) << 30) / per_sample));
-  const int64_t KT = dw_batch * NP;
+  const int64_t dw_batch = n_units;
+  const int64_t KT = dw_batch * RP;
 
   size_t off = 0;
   char* b = static_cast<char*>(base);
@@ -50,23 +61,24 @@ size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
     off = align_up(off + bytes, 256);
     return p;
   };
-  // the state of one sample: masks and rows, log-sum-exp partials, H_c, dZ
-  auto take_sample = [&](Workspace& w) {
-    w.meta = static_cast<SampleMeta*>(take(sizeof(SampleMeta)));
-    w.idx = static_cast<int32_t*>(take(P * 4));
-    w.row_tgt = static_cast<int32_t*>(take(NP * 4));
-    w.row_seq = static_cast<int32_t*>(take(NP * 4));
-    w.seg_off = static_cast<int32_t*>(take((dm.B + 1) * 4));
-    w.t24 = static_cast<uint32_t*>(take(dm.B * 4));
-    w.ztgt = static_cast<float*>(take(NP * 4));
-    w.lse2 = static_cast<float*>(take(NP * 4));
-    w.lp = static_cast<float*>(take(NP * 4));
-    w.row_scale = static_cast<float*>(take(NP * 4));
-    w.inv_rms = static_cast<float*>(take(NP * 4));
-    w.part_m = static_cast<float*>(take(nvt * NP * 4));
-    w.part_s = static_cast<float*>(take(nvt * NP * 4));
-    w.Hc = static_cast<uint16_t*>(take(NP * dm.d * 2));
-    w.dZ = static_cast<uint16_t*>(take(NP * dm.V * 2));
+  // the state of one unit: masks and rows, log-sum-exp partials, H_c, dZ
+  auto take_unit = [&](Workspace& w) {
+    w.meta = static_cast<SampleMeta*>(take(G * sizeof(SampleMeta)));
+    w.idx = static_cast<int32_t*>(take(G * P * 4));
+    w.row_tgt = static_cast<int32_t*>(take(RP * 4));
+    w.row_seq = static_cast<int32_t*>(take(RP * 4));
+    w.seg_off = static_cast<int32_t*>(take(G * (dm.B + 1) * 4));
+    w.t24 = static_cast<uint32_t*>(take(G * dm.B * 4));
+    w.seq_scale = static_cast<float*>(take(G * dm.B * 4));
+    w.ztgt = static_cast<float*>(take(RP * 4));
+    w.lse2 = static_cast<float*>(take(RP * 4));
+    w.lp = static_cast<float*>(take(RP * 4));
+    w.row_scale = static_cast<float*>(take(RP * 4));
+    w.inv_rms = static_cast<float*>(take(RP * 4));
+    w.part_m = static_cast<float*>(take(nvt * RP * 4));
+    w.part_s = static_cast<float*>(take(nvt * RP * 4));
+    w.Hc = static_cast<uint16_t*>(take(RP * dm.d * 2));
+    w.dZ = static_cast<uint16_t*>(take(RP * dm.V * 2));
   };
   Workspace w;
   w.dbar = static_cast<double*>(take(dm.B * 8));
@@ -74,20 +86,23 @@ size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
   w.HcT = static_cast<uint16_t*>(take(KT * dm.d * 2));
   w.WT = static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2));
   w.dZT = static_cast<uint16_t*>(take(KT * dm.V * 2));
-  w.dx_part = static_cast<float*>(take(n_split * NP * dm.d * 4));
+  w.dx_part = static_cast<float*>(take(n_split * RP * dm.d * 4));
   w.P = P;
   w.NP = NP;
   w.nvt = nvt;
+  w.G = G;
+  w.RP = RP;
   w.n_split = n_split;
   w.dw_batch = dw_batch;
   w.KT = KT;
-  take_sample(w);
-  for (int j = 1; retain && j < dm.n_t; ++j) {
-    Workspace sj = w;
-    take_sample(sj);
-    if (samples) samples[j] = sj;
+  w.g_used = (int)G;
+  take_unit(w);
+  for (int64_t u = 1; u < n_units; ++u) {
+    Workspace wu = w;
+    take_unit(wu);
+    if (units) units[u] = wu;
   }
-  if (samples) samples[0] = w;
+  if (units) units[0] = w;
   if (ws) *ws = w;
   return off;
 }
@@ -177,24 +192,29 @@ struct Act {
   const uint16_t* at(int j) const { return x + (int64_t)(j - j0) * stride; }
 };
 
-// forward part of one sample: mask .. l (and, with backward, g / loss / scale)
-static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer& tm, int grid,
-                              int j, const Act& act, const int32_t* targets,
-                              const uint8_t* resp, const float* adv, const double* ell_old,
-                              double loss_scale, double* ell, double* g, double* loss,
-                              int32_t* n_masked, float* t_out, int32_t* flags, bool backward,
-                              bool store_u, const SampleMeta* prev, const double* dbar,
-                              hipStream_t s) {
+// forward part of the unit of samples j0 .. j0 + n_s - 1: masks .. l (and,
+// with backward, g / loss / scale); prev_unit: record of the previous unit of
+// the dW batch (NULL for the first)
+static int run_forward_unit(const bgpo_problem* p, Workspace& ws, Timer& tm, int grid, int j0,
+                            int n_s, const Act& act, const int32_t* targets, const uint8_t* resp,
+                            const float* adv, const double* ell_old, double loss_scale,
+                            double* ell, double* g, double* loss, int32_t* n_masked, float* t_out,
+                            int32_t* flags, bool backward, bool store_u,
+                            const SampleMeta* prev_unit, const double* dbar, hipStream_t s) {
   const Dims dm = dims_of(p);
+  ws.g_used = n_s;
   BGPO_TRY(tm.begin(BGPO_K_MASK));
-  BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, p->t_mode, p->seed,
-                               p->seq_id_base, ws.idx, ws.row_tgt, ws.row_seq, ws.seg_off, ws.t24,
-                               ws.meta, n_masked + j, dm.n_t, t_out ? t_out + j : nullptr, dm.n_t,
-                               (int)ws.NP, dm.V, prev, dx_plan(dm, ws, grid), s));
+  for (int gs = 0; gs < n_s; ++gs) {
+    const int j = j0 + gs;
+    BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, gs, p->t_mode, p->seed,
+                                 p->seq_id_base, &ws, nullptr, n_masked + j, dm.n_t,
+                                 t_out ? t_out + j : nullptr, dm.n_t, dm.V,
+                                 gs ? ws.meta + (gs - 1) : prev_unit, dx_plan(dm, ws, grid), s));
+  }
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
-  if (act.gamma) BGPO_TRY(launch_row_rms(act.at(j), ws, dm.d, act.eps, s));
-  BGPO_TRY(launch_gather(act.at(j), act.gamma, ws, dm.d, s));
+  if (act.gamma) BGPO_TRY(launch_row_rms(act.at(j0), act.stride, dm.B, ws, dm.d, act.eps, s));
+  BGPO_TRY(launch_gather(act.at(j0), act.stride, dm.B, act.gamma, ws, dm.d, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_FWD));
   BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, store_u, s));
@@ -202,7 +222,7 @@ static int run_forward_sample(const bgpo_problem* p, const Workspace& ws, Timer&
   BGPO_TRY(tm.begin(BGPO_K_ELL));
   BGPO_TRY(launch_target_logit(ws, dm.d, s));
   BGPO_TRY(launch_combine_rows(ws, dm.V, s));
-  BGPO_TRY(launch_seq_terms(ws, dm.B, dm.n_t, j, adv, ell_old, loss_scale, ell, g, loss, flags,
+  BGPO_TRY(launch_seq_terms(ws, dm.B, dm.n_t, j0, adv, ell_old, loss_scale, ell, g, loss, flags,
                             backward, p->bound, dbar, s));
   BGPO_TRY(tm.end());
   return BGPO_OK;
@@ -247,10 +267,9 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
   const int st = check_problem(prob);
   if (st != BGPO_OK) return st;
   if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
-  if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, prob->t_mode,
-                          prob->seed, prob->seq_id_base, idx, nullptr, nullptr, nullptr, nullptr,
-                          nullptr, n_masked, 1, t_out, 1, 0, prob->V, nullptr, DxPlan{1, 1, 1, 1},
-                          (hipStream_t)stream) != hipSuccess)
+  if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, 0, prob->t_mode,
+                          prob->seed, prob->seq_id_base, nullptr, idx, n_masked, 1, t_out, 1,
+                          prob->V, nullptr, DxPlan{1, 1, 1, 1}, (hipStream_t)stream) != hipSuccess)
     return BGPO_ERR_HIP;
   return BGPO_OK;
 }
@@ -268,11 +287,12 @@ static int check_workspace(const bgpo_problem* prob, void* workspace, size_t ws_
 
 namespace bgpo {
 
-// the gradient part of one sample once its scale is known: dZ, dX (with the
-// norm backward), leaving its dZ^T columns for the batch's dW GEMM
-static int sample_backward(const Workspace& ws, const Act& act, int j, int j_begin,
-                           const uint16_t* W_head, float* dX, float* dgamma, const Dims& dm,
-                           int grid, Timer& tm, hipStream_t s) {
+// the gradient part of a unit once its scales are known: dZ, dX (each
+// sample's rows in sample order, with the norm backward), leaving its dZ^T
+// columns for the dW GEMM
+static int unit_backward(const Workspace& ws, const Act& act, int j0, int j_begin,
+                         const uint16_t* W_head, float* dX, float* dgamma, const Dims& dm,
+                         int grid, Timer& tm, hipStream_t s) {
   BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
   BGPO_TRY(launch_softmax_grad(ws, dm.V, s));
   BGPO_TRY(tm.end());
@@ -280,11 +300,14 @@ static int sample_backward(const Workspace& ws, const Act& act, int j, int j_beg
   BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
-  float* dXj = dX + (int64_t)(j - j_begin) * act.stride;
-  if (act.gamma)
-    BGPO_TRY(launch_dx_reduce_rmsnorm(ws, act.at(j), act.gamma, dXj, dgamma, dm.d, s));
-  else
-    BGPO_TRY(launch_dx_reduce(ws, dXj, dm.d, s));
+  for (int gs = 0; gs < ws.g_used; ++gs) {
+    const int j = j0 + gs;
+    float* dXj = dX + (int64_t)(j - j_begin) * act.stride;
+    if (act.gamma)
+      BGPO_TRY(launch_dx_reduce_rmsnorm(ws, gs, act.at(j), act.gamma, dXj, dgamma, dm.d, s));
+    else
+      BGPO_TRY(launch_dx_reduce(ws, gs, dXj, dm.d, s));
+  }
   BGPO_TRY(tm.end());
   return BGPO_OK;
 }
@@ -293,7 +316,7 @@ static int sample_backward(const Workspace& ws, const Act& act, int j, int j_beg
 // implementation that keeps all n_t computational graphs works): each
 // forward runs once and keeps its exponentials, the mean log-ratio is formed,
 // then every sample's gradient comes from its kept state; memory grows with
-// n_t.
+// n_t.  The units are those of the two-pass mode, each with its own state.
 static int bwd_retained(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
                         const int32_t* targets, const uint8_t* resp_mask, const float* adv,
                         const double* ell_old, double loss_scale, float* dX, float* dgamma,
@@ -301,17 +324,20 @@ static int bwd_retained(const bgpo_problem* prob, const Act& act, const uint16_t
                         float* t_out, int32_t* status_flags, void* workspace, int grid, Timer& tm,
                         hipStream_t s) {
   const Dims dm = dims_of(prob);
-  std::vector<Workspace> S(dm.n_t);
   Workspace ws;
-  workspace_layout(dm, 1, workspace, &ws, S.data());
+  workspace_layout(dm, 1, workspace, &ws, nullptr);
+  const int G = (int)ws.G, n_units = (int)ws.dw_batch;
+  std::vector<Workspace> U(n_units);
+  workspace_layout(dm, 1, workspace, nullptr, U.data());
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
   BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
-  for (int j = 0; j < dm.n_t; ++j) {
-    const int st = run_forward_sample(prob, S[j], tm, grid, j, act, targets, resp_mask, nullptr,
-                                      nullptr, 0.0, ell, nullptr, nullptr, n_masked, t_out,
-                                      status_flags, false, true, j ? S[j - 1].meta : nullptr,
-                                      nullptr, s);
+  for (int u = 0; u < n_units; ++u) {
+    const int j0 = u * G, n_s = std::min(G, dm.n_t - j0);
+    const int st = run_forward_unit(prob, U[u], tm, grid, j0, n_s, act, targets, resp_mask,
+                                    nullptr, nullptr, 0.0, ell, nullptr, nullptr, n_masked, t_out,
+                                    status_flags, false, true, u ? U[u - 1].unit() : nullptr,
+                                    nullptr, s);
     if (st != BGPO_OK) return st;
   }
   const double* dbar = nullptr;
@@ -321,16 +347,17 @@ static int bwd_retained(const bgpo_problem* prob, const Act& act, const uint16_t
     BGPO_TRY(tm.end());
     dbar = ws.dbar;
   }
-  for (int j = 0; j < dm.n_t; ++j) {
+  for (int u = 0; u < n_units; ++u) {
+    const int j0 = u * G;
     BGPO_TRY(tm.begin(BGPO_K_ELL));
-    BGPO_TRY(launch_seq_terms(S[j], dm.B, dm.n_t, j, adv, ell_old, loss_scale, ell, g, loss,
+    BGPO_TRY(launch_seq_terms(U[u], dm.B, dm.n_t, j0, adv, ell_old, loss_scale, ell, g, loss,
                               status_flags, true, prob->bound, dbar, s));
     BGPO_TRY(tm.end());
-    const int st = sample_backward(S[j], act, j, 0, W_head, dX, dgamma, dm, grid, tm, s);
+    const int st = unit_backward(U[u], act, j0, 0, W_head, dX, dgamma, dm, grid, tm, s);
     if (st != BGPO_OK) return st;
   }
   BGPO_TRY(tm.begin(BGPO_K_DW));
-  BGPO_TRY(launch_gemm_dw(S[dm.n_t - 1], dW, dm.d, dm.V, grid, s));
+  BGPO_TRY(launch_gemm_dw(U[n_units - 1], dW, dm.d, dm.V, grid, s));
   BGPO_TRY(tm.end());
   return BGPO_OK;
 }
@@ -357,10 +384,12 @@ static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
   BGPO_TRY(launch_transpose_w(W_head, ws.WT, prob->d, prob->V, s));
   BGPO_TRY(tm.end());
-  for (int j = prob->j_begin; j < prob->j_begin + prob->j_count; ++j) {
-    st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, nullptr, nullptr, 0.0,
-                            ell, nullptr, nullptr, n_masked, t_out, nullptr, false, false, nullptr,
-                            nullptr, s);
+  const int j_end = prob->j_begin + prob->j_count;
+  for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.G) {
+    const int n_s = std::min<int>(j_end - j0, (int)ws.G);
+    st = run_forward_unit(prob, ws, tm, grid, j0, n_s, act, targets, resp_mask, nullptr, nullptr,
+                          0.0, ell, nullptr, nullptr, n_masked, t_out, nullptr, false, false,
+                          nullptr, nullptr, s);
     if (st != BGPO_OK) return st;
   }
   BGPO_TRY(tm.finish());
@@ -407,10 +436,11 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
   // mean log-ratio, which scales every sample's gradient (on-policy it is 0)
   const double* dbar = nullptr;
   if (exact && ell_old) {
-    for (int j = 0; j < prob->n_t; ++j) {
-      st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, nullptr, nullptr,
-                              0.0, ell, nullptr, nullptr, n_masked, t_out, status_flags, false,
-                              false, nullptr, nullptr, s);
+    for (int j0 = 0; j0 < prob->n_t; j0 += (int)ws.G) {
+      const int n_s = std::min<int>(prob->n_t - j0, (int)ws.G);
+      st = run_forward_unit(prob, ws, tm, grid, j0, n_s, act, targets, resp_mask, nullptr, nullptr,
+                            0.0, ell, nullptr, nullptr, n_masked, t_out, status_flags, false,
+                            false, nullptr, nullptr, s);
       if (st != BGPO_OK) return st;
     }
     BGPO_TRY(tm.begin(BGPO_K_ELL));
@@ -419,17 +449,15 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
     dbar = ws.dbar;
   }
   const int j_end = prob->j_begin + prob->j_count;
-  for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.dw_batch) {
-    const int j1 = std::min<int>(j_end, j0 + (int)ws.dw_batch);
-    for (int j = j0; j < j1; ++j) {
-      st = run_forward_sample(prob, ws, tm, grid, j, act, targets, resp_mask, adv, ell_old,
-                              loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, true,
-                              j == j0 ? nullptr : ws.meta, dbar, s);
-      if (st != BGPO_OK) return st;
-      st = sample_backward(ws, act, j, prob->j_begin, W_head, dX, dgamma, dm, grid, tm, s);
-      if (st != BGPO_OK) return st;
-    }
-    // one dW GEMM for the batch: K runs over the batch's samples side by side
+  for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.G) {
+    const int n_s = std::min<int>(j_end - j0, (int)ws.G);
+    st = run_forward_unit(prob, ws, tm, grid, j0, n_s, act, targets, resp_mask, adv, ell_old,
+                          loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, true,
+                          nullptr, dbar, s);
+    if (st != BGPO_OK) return st;
+    st = unit_backward(ws, act, j0, prob->j_begin, W_head, dX, dgamma, dm, grid, tm, s);
+    if (st != BGPO_OK) return st;
+    // one dW GEMM for the unit: K runs over its rows
     BGPO_TRY(tm.begin(BGPO_K_DW));
     BGPO_TRY(launch_gemm_dw(ws, dW, dm.d, dm.V, grid, s));
     BGPO_TRY(tm.end());

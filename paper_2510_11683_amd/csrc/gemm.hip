@@ -489,9 +489,9 @@ hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool sto
   GemmParams p = base_params();
   p.A = ws.WT; p.lda = d;
   p.B = ws.Hc; p.ldb = d;
-  p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.meta;
+  p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.unit();
   p.k_split = d;
-  p.part_m = ws.part_m; p.part_s = ws.part_s; p.ldp = ws.NP;
+  p.part_m = ws.part_m; p.part_s = ws.part_s; p.ldp = ws.RP;
   p.group_m = kGroupMFwd;
   if (store_u) {
     p.dZ = ws.dZ; p.ldz = V;
@@ -507,10 +507,10 @@ hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, 
   GemmParams p = base_params();
   p.A = ws.dZ; p.lda = V;
   p.B = W; p.ldb = V;
-  p.N = d; p.K = V; p.dyn_m = 1; p.meta = ws.meta;
+  p.N = d; p.K = V; p.dyn_m = 1; p.meta = ws.unit();
   p.dyn_split = 1;
   p.group_m = kGroupMdX;
-  p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.NP * d;
+  p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
   k_gemm<EPI_F32_STORE, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
   return hipGetLastError();
 }
@@ -519,7 +519,7 @@ hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid
   GemmParams p = base_params();
   p.A = ws.HcT; p.lda = ws.KT;
   p.B = ws.dZT; p.ldb = ws.KT;
-  p.M = d; p.N = V; p.dyn_k = 1; p.meta = ws.meta;
+  p.M = d; p.N = V; p.dyn_k = 1; p.meta = ws.unit();
   p.group_m = kGroupMdW;
   p.out = dW; p.ldo = V;
   k_gemm<EPI_F32_ACCUM, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);

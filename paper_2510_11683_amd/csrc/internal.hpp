@@ -16,19 +16,25 @@ constexpr int kVocabTile = 128;
 
 constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
 
-// Device-resident per-sample bookkeeping written by the mask kernel.
+// Device-resident bookkeeping written by the mask kernel, one record per
+// sample.  Samples are processed in units of up to G consecutive samples whose
+// masked rows sit back to back in one row space (the LM-head GEMMs and the row
+// kernels run once per unit); the unit-level fields are cumulative, so the
+// record of the unit's last sample describes the whole unit.
 struct SampleMeta {
-  int32_t n_rows;      // N_j: masked positions in this sample (all responses)
-  int32_t n_rows_pad;  // N_j rounded up to kRowPad
-  int32_t col_off;     // first column of this sample in H_c^T / dZ^T
-  int32_t col_end;     // col_off + N_j rounded up to 64: K of the batched dW GEMM
-  int32_t dx_split;    // vocabulary splits of this sample's dX GEMM
+  int32_t n_rows;      // masked rows of the unit up to and including this sample
+  int32_t n_rows_pad;  // n_rows rounded up to kRowPad
+  int32_t col_off;     // first column of the unit in H_c^T / dZ^T
+  int32_t col_end;     // col_off + n_rows rounded up to 64: K of the dW GEMM
+  int32_t dx_split;    // vocabulary splits of the unit's dX GEMM
   int32_t dx_kslab;    // 64-wide vocabulary slabs per split
-  int32_t pad[58];
+  int32_t s_rows;      // N_j: masked rows of this sample (all responses)
+  int32_t s_row_off;   // first row of this sample in the unit's row space
+  int32_t pad[56];
 };
 
-// What the mask kernel needs to choose the dX split of a sample (the split
-// count that best fills the persistent grid for the sample's row count).
+// What the mask kernel needs to choose the dX split of a unit (the split
+// count that best fills the persistent grid for the unit's row count).
 struct DxPlan {
   int kslabs;      // V / 64
   int col_tiles;   // d / 256
@@ -36,33 +42,40 @@ struct DxPlan {
   int s_max;       // splits the partial buffer holds
 };
 
-// Views into the caller's workspace.
+// Views into the caller's workspace: the state of one unit of G samples
+// (RP = G * NP rows) and the buffers shared by all units.
 struct Workspace {
-  SampleMeta* meta;
-  int32_t* idx;        // [P]          masked flat positions, ascending
-  int32_t* row_tgt;    // [NP]         target token of each compacted row
-  int32_t* row_seq;    // [NP]         response of each compacted row (B for padding)
-  int32_t* seg_off;    // [B+1]        first compacted row of each response
-  uint32_t* t24;       // [B]          integer timestep of each response
-  uint16_t* Hc;        // [NP, d]      gathered masked hidden rows (bf16)
-  uint16_t* HcT;       // [d, KT]      the same, transposed; samples of a dW batch side by side
+  SampleMeta* meta;    // [G]          one record per sample of the unit
+  int32_t* idx;        // [G*P]        masked flat positions, per sample ascending
+  int32_t* row_tgt;    // [RP]         target token of each compacted row
+  int32_t* row_seq;    // [RP]         g*B + b of each row (sample g of the unit, response b)
+  int32_t* seg_off;    // [G*(B+1)]    first row of each (sample, response), unit row space
+  uint32_t* t24;       // [G*B]        integer timestep of each (sample, response)
+  float* seq_scale;    // [G*B]        gradient scale s of each (sample, response)
+  uint16_t* Hc;        // [RP, d]      gathered masked hidden rows (bf16)
+  uint16_t* HcT;       // [d, KT]      the same, transposed; units of a dW batch side by side
   uint16_t* WT;        // [V, d]       W_head transposed (bf16)
-  float* part_m;       // [nvt, NP]    per-vocabulary-slice max (log2 units)
-  float* part_s;       // [nvt, NP]    per-vocabulary-slice sum of 2^(z*log2e - max)
-  float* ztgt;         // [NP]         target logit
-  float* lse2;         // [NP]         log2-sum-exp2 of each row (log2 units)
-  float* lp;           // [NP]         log p of the target
-  float* row_scale;    // [NP]         gradient scale s of each row (0 for padding)
+  float* part_m;       // [nvt, RP]    per-vocabulary-slice max (log2 units)
+  float* part_s;       // [nvt, RP]    per-vocabulary-slice sum of 2^(z*log2e - max)
+  float* ztgt;         // [RP]         target logit
+  float* lse2;         // [RP]         log2-sum-exp2 of each row (log2 units)
+  float* lp;           // [RP]         log p of the target
+  float* row_scale;    // [RP]         gradient scale s of each row (0 for padding)
   double* dbar;        // [B]          mean log-ratio over all samples (exact objective)
-  float* inv_rms;      // [NP]         final-RMSNorm 1/rms of each compacted row
-  float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks
-  uint16_t* dZ;        // [NP, V]      s (softmax - onehot), bf16 (first the fp16 exponentials)
-  uint16_t* dZT;       // [V, KT]      the same, transposed; samples of a dW batch side by side
-  float* dx_part;      // [S, NP, d]   split-vocabulary partial dX
+  float* inv_rms;      // [RP]         final-RMSNorm 1/rms of each compacted row
+  float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks of a sample
+  uint16_t* dZ;        // [RP, V]      s (softmax - onehot), bf16 (first the fp16 exponentials)
+  uint16_t* dZT;       // [V, KT]      the same, transposed; units of a dW batch side by side
+  float* dx_part;      // [S, RP, d]   split-vocabulary partial dX
   int64_t P, NP, nvt;
-  int64_t n_split;     // capacity of dx_part in splits (the per-sample count is in meta)
-  int64_t dw_batch;    // samples whose dW contributions share one GEMM
-  int64_t KT;          // dw_batch * NP: leading dimension of H_c^T and dZ^T
+  int64_t G;           // samples per unit
+  int64_t RP;          // G * NP: row capacity of a unit
+  int64_t n_split;     // capacity of dx_part in splits (the unit's count is in its meta)
+  int64_t dw_batch;    // units whose dW contributions share one GEMM
+  int64_t KT;          // dw_batch * RP: leading dimension of H_c^T and dZ^T
+  int g_used;          // samples in the current unit (host side; its record meta[g_used - 1]
+                       // describes the unit)
+  const SampleMeta* unit() const { return meta + (g_used - 1); }
 };
 
 struct Dims {
@@ -70,30 +83,38 @@ struct Dims {
 };
 
 // Views into the caller's workspace (base may be NULL: sizes only).
-// retain = 0: the state of one sample at a time, dW batches of up to
-//             kMaxDwBatch samples; the size does not depend on n_t.
-// retain = 1: the state of every one of the n_t samples is kept
-//             (samples[0 .. n_t), each with its own meta, rows, partials, H_c
-//             and dZ; H_c^T / dZ^T hold all samples' columns; one dW batch).
+// retain = 0: the state of one unit of G samples at a time (G chosen from the
+//             shapes, never from n_t), one unit per dW GEMM; the size does not
+//             depend on n_t.
+// retain = 1: the same units (G capped at n_t), each keeping its own state
+//             (units[0 .. ceil(n_t / G)): meta, rows, partials, H_c and dZ;
+//             H_c^T / dZ^T hold all units' columns; one dW batch), so memory
+//             grows with n_t.
 size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
-                        Workspace* samples);
+                        Workspace* units);
 
 // ---- launchers (return hipSuccess or the launch error) ----
 hipError_t launch_transpose_w(const uint16_t* W, uint16_t* WT, int d, int V, hipStream_t s);
-hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int B, int L, int n_t, int j,
-                               int t_mode, uint64_t seed, uint32_t seq_base, int32_t* idx,
-                               int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
-                               SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
-                               float* t_out, int t_stride, int row_cap, int V,
+// Mask and compaction of sample j, sample g of its unit: rows go after those of
+// the unit's earlier samples (prev = record of sample g - 1); for g = 0, prev
+// (may be NULL) is the record of the previous unit of the dW batch, whose
+// columns this unit's follow.
+hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int B, int L, int n_t,
+                               int j, int g, int t_mode, uint64_t seed, uint32_t seq_base,
+                               const Workspace* ws, int32_t* idx_out, int32_t* n_masked_out,
+                               int nm_stride, float* t_out, int t_stride, int V,
                                const SampleMeta* prev, const DxPlan& plan, hipStream_t s);
-hipError_t launch_row_rms(const uint16_t* x, const Workspace& ws, int d, float eps, hipStream_t s);
-hipError_t launch_gather(const uint16_t* hidden, const float* gamma, const Workspace& ws, int d,
-                         hipStream_t s);
+// x / hidden of row r is x + (row_seq[r] / B) * stride (the row's sample in the unit)
+hipError_t launch_row_rms(const uint16_t* x, int64_t stride, int B, const Workspace& ws, int d,
+                          float eps, hipStream_t s);
+hipError_t launch_gather(const uint16_t* hidden, int64_t stride, int B, const float* gamma,
+                         const Workspace& ws, int d, hipStream_t s);
 hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool store_u,
                            hipStream_t s);
 hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s);
 hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s);
-hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const float* adv,
+// per-response terms of the unit's samples j0 .. j0 + g_used - 1
+hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j0, const float* adv,
                             const double* ell_old, double loss_scale, double* ell, double* g,
                             double* loss, int32_t* flags, bool backward, int bound,
                             const double* dbar, hipStream_t s);
@@ -102,9 +123,12 @@ hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, in
 hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s);
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s);
-hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s);
-hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, const uint16_t* x, const float* gamma,
-                                    float* dx, float* dgamma, int d, hipStream_t s);
+// dX of sample g of the unit (its rows only; samples of a unit run one after
+// the other, so positions shared between samples are summed in sample order)
+hipError_t launch_dx_reduce(const Workspace& ws, int g, float* dX, int d, hipStream_t s);
+hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const uint16_t* x,
+                                    const float* gamma, float* dx, float* dgamma, int d,
+                                    hipStream_t s);
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s);
 
 int gemm_grid(int device);  // persistent grid size of the GEMM kernels on `device`

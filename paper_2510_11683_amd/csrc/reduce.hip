@@ -41,7 +41,8 @@ __global__ __launch_bounds__(256) void k_target_logit(const uint16_t* __restrict
 }
 
 hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s) {
-  k_target_logit<<<(unsigned)(ws.NP / 4), 256, 0, s>>>(ws.Hc, ws.WT, ws.row_tgt, ws.meta, ws.ztgt, d);
+  k_target_logit<<<(unsigned)(ws.RP / 4), 256, 0, s>>>(ws.Hc, ws.WT, ws.row_tgt, ws.unit(), ws.ztgt,
+                                                       d);
   return hipGetLastError();
 }
 
@@ -99,14 +100,14 @@ __global__ __launch_bounds__(64 * kCombineWaves) void k_combine_rows(
 }
 
 hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s) {
-  k_combine_rows<<<(unsigned)(ws.NP / 64), 64 * kCombineWaves, 0, s>>>(
-      ws.part_m, ws.part_s, ws.ztgt, ws.meta, ws.lse2, ws.lp, (int)ws.nvt, ws.NP);
+  k_combine_rows<<<(unsigned)(ws.RP / 64), 64 * kCombineWaves, 0, s>>>(
+      ws.part_m, ws.part_s, ws.ztgt, ws.unit(), ws.lse2, ws.lp, (int)ws.nvt, ws.RP);
   return hipGetLastError();
 }
 
-// Per-response terms of sample j.  One workgroup; responses in order.
+// Per-response terms of the samples of a unit.  One workgroup; samples and
+// responses in order.
 constexpr int kSeqThreads = 1024;
-constexpr int kSeqMaxB = 4096;
 
 // The objective's per-sample term g and its derivative dg/dl for
 // d = l - l_old:
@@ -131,66 +132,76 @@ __device__ __forceinline__ void bound_term(double dj, double A, int n_t, int bou
   }
 }
 
+// Sample g of the unit is sample j0 + g; its response b has rows
+// [seg_off[g (B+1) + b], seg_off[g (B+1) + b + 1]) and timestep t24[g B + b].
+// The gradient scale of (g, b) goes to seq_scale[g B + b] and from there to
+// every row of that response (row_seq[r] = g B + b).
 __global__ __launch_bounds__(kSeqThreads) void k_seq_terms(
     const float* __restrict__ lp, const int32_t* __restrict__ seg_off,
     const uint32_t* __restrict__ t24, const int32_t* __restrict__ row_seq,
-    const SampleMeta* __restrict__ meta, int B, int n_t, int j, const float* __restrict__ adv,
-    const double* __restrict__ ell_old, double loss_scale, double* __restrict__ ell,
-    double* __restrict__ g, double* __restrict__ loss, int32_t* __restrict__ flags,
-    float* __restrict__ row_scale, int backward, int bound, const double* __restrict__ dbar) {
+    const SampleMeta* __restrict__ meta, int B, int n_t, int j0, int n_samples,
+    const float* __restrict__ adv, const double* __restrict__ ell_old, double loss_scale,
+    double* __restrict__ ell, double* __restrict__ g, double* __restrict__ loss,
+    int32_t* __restrict__ flags, float* __restrict__ seq_scale, float* __restrict__ row_scale,
+    int backward, int bound, const double* __restrict__ dbar) {
   __shared__ double red[kSeqThreads / 64];
-  __shared__ float s_scale[kSeqMaxB];
   __shared__ int s_bad;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) s_bad = 0;
   double loss_acc = 0.0;
-  for (int b = 0; b < B; ++b) {
-    const int r0 = seg_off[b], r1 = seg_off[b + 1];
-    double acc = 0.0;
-    for (int r = r0 + tid; r < r1; r += kSeqThreads) acc += (double)lp[r];
+  for (int gs = 0; gs < n_samples; ++gs) {
+    const int j = j0 + gs;
+    for (int b = 0; b < B; ++b) {
+      const int r0 = seg_off[gs * (B + 1) + b], r1 = seg_off[gs * (B + 1) + b + 1];
+      double acc = 0.0;
+      for (int r = r0 + tid; r < r1; r += kSeqThreads) acc += (double)lp[r];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-    if (lane == 0) red[wave] = acc;
-    __syncthreads();
-    if (tid == 0) {
-      double sum = 0.0;
-      for (int w = 0; w < kSeqThreads / 64; ++w) sum += red[w];
-      const double t = (double)t24[b] * (1.0 / 16777216.0);
-      const double l = sum / t;                                      // Eq. per_step_loss
-      const int64_t o = (int64_t)b * n_t + j;
-      ell[o] = l;
-      if (backward) {
-        const double dj = ell_old ? l - ell_old[o] : 0.0;
-        double gj, dg;
-        bound_term(dj, (double)adv[b], n_t, bound, dbar ? dbar[b] : 0.0, &gj, &dg);
-        g[o] = gj;
-        loss_acc += -loss_scale * gj;
-        const double sc = loss_scale * dg / t;
-        s_scale[b] = (float)sc;
-        if (!isfinite(l) || !isfinite(gj) || !isfinite(sc) || !isfinite((float)sc)) s_bad = 1;
-      } else if (!isfinite(l)) {
-        s_bad = 1;
+      for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+      if (lane == 0) red[wave] = acc;
+      __syncthreads();
+      if (tid == 0) {
+        double sum = 0.0;
+        for (int w = 0; w < kSeqThreads / 64; ++w) sum += red[w];
+        const double t = (double)t24[gs * B + b] * (1.0 / 16777216.0);
+        const double l = sum / t;                                      // Eq. per_step_loss
+        const int64_t o = (int64_t)b * n_t + j;
+        ell[o] = l;
+        if (backward) {
+          const double dj = ell_old ? l - ell_old[o] : 0.0;
+          double gj, dg;
+          bound_term(dj, (double)adv[b], n_t, bound, dbar ? dbar[b] : 0.0, &gj, &dg);
+          g[o] = gj;
+          loss_acc += -loss_scale * gj;
+          const double sc = loss_scale * dg / t;
+          seq_scale[gs * B + b] = (float)sc;
+          if (!isfinite(l) || !isfinite(gj) || !isfinite(sc) || !isfinite((float)sc)) s_bad = 1;
+        } else if (!isfinite(l)) {
+          s_bad = 1;
+        }
       }
+      __syncthreads();
     }
-    __syncthreads();
   }
   if (tid == 0) {
     if (backward) loss[0] += loss_acc;
     if (s_bad && flags) atomicOr(flags, kFlagNonfinite);
   }
   if (backward) {
+    // seq_scale was written by thread 0 before the last barrier
+    __threadfence_block();
     const int N = meta->n_rows, NPr = meta->n_rows_pad;
-    for (int r = tid; r < NPr; r += kSeqThreads) row_scale[r] = r < N ? s_scale[row_seq[r]] : 0.f;
+    for (int r = tid; r < NPr; r += kSeqThreads) row_scale[r] = r < N ? seq_scale[row_seq[r]] : 0.f;
   }
 }
 
-hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j, const float* adv,
+hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j0, const float* adv,
                             const double* ell_old, double loss_scale, double* ell, double* g,
                             double* loss, int32_t* flags, bool backward, int bound,
                             const double* dbar, hipStream_t s) {
-  k_seq_terms<<<1, kSeqThreads, 0, s>>>(ws.lp, ws.seg_off, ws.t24, ws.row_seq, ws.meta, B, n_t, j,
-                                        adv, ell_old, loss_scale, ell, g, loss, flags,
-                                        ws.row_scale, backward ? 1 : 0, bound, dbar);
+  k_seq_terms<<<1, kSeqThreads, 0, s>>>(ws.lp, ws.seg_off, ws.t24, ws.row_seq, ws.unit(), B, n_t,
+                                        j0, ws.g_used, adv, ell_old, loss_scale, ell, g, loss,
+                                        flags, ws.seq_scale, ws.row_scale, backward ? 1 : 0, bound,
+                                        dbar);
   return hipGetLastError();
 }
 
@@ -299,22 +310,25 @@ __global__ __launch_bounds__(256) void k_softmax_grad(
 }
 
 hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s) {
-  dim3 grid((unsigned)ws.nvt, (unsigned)(ws.NP / 64));
+  dim3 grid((unsigned)ws.nvt, (unsigned)(ws.RP / 64));
   k_softmax_grad<<<grid, 256, 0, s>>>(ws.part_m, ws.lse2, ws.row_scale, ws.ztgt, ws.row_tgt,
-                                      ws.meta, ws.dZ, ws.dZT, V, ws.NP, ws.KT);
+                                      ws.unit(), ws.dZ, ws.dZT, V, ws.RP, ws.KT);
   return hipGetLastError();
 }
 
-// dX[idx[r], :] += sum_s part[s][r][:], float4 per thread; rows are unique
-// within a sample, so there are no write conflicts.
+// dX[idx[r], :] += sum_s part[s][r][:] over the rows r of one sample of the
+// unit (sm: its record; um: the unit's, which holds the split count), float4
+// per thread; rows are unique within a sample, so there are no write
+// conflicts.
 __global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ part,
                                                    const int32_t* __restrict__ idx,
-                                                   const SampleMeta* __restrict__ meta,
+                                                   const SampleMeta* __restrict__ sm,
+                                                   const SampleMeta* __restrict__ um,
                                                    float* __restrict__ dX, int d,
                                                    int64_t split_stride) {
-  const int r = blockIdx.x;
-  if (r >= meta->n_rows) return;
-  const int n_split = meta->dx_split;
+  if ((int)blockIdx.x >= sm->s_rows) return;
+  const int r = sm->s_row_off + blockIdx.x;
+  const int n_split = um->dx_split;
   const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
   if (c >= d) return;
   float4 acc = *reinterpret_cast<const float4*>(part + (int64_t)r * d + c);
@@ -328,27 +342,29 @@ __global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ par
   *dst = o;
 }
 
-hipError_t launch_dx_reduce(const Workspace& ws, float* dX, int d, hipStream_t s) {
+hipError_t launch_dx_reduce(const Workspace& ws, int g, float* dX, int d, hipStream_t s) {
   dim3 grid((unsigned)ws.NP, (unsigned)((d / 4 + 255) / 256));
-  k_dx_reduce<<<grid, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta, dX, d, ws.NP * d);
+  k_dx_reduce<<<grid, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta + g, ws.unit(), dX, d, ws.RP * d);
   return hipGetLastError();
 }
 
 // Split reduction followed by the backward of the final RMSNorm
-// h = gamma x r, r = (mean x^2 + eps)^(-1/2), for one row per workgroup:
+// h = gamma x r, r = (mean x^2 + eps)^(-1/2), for one row of one sample of the
+// unit per workgroup (x: that sample's activations):
 //   dh       = sum_s part[s][row]                     (d loss / d h)
 //   dx_k    += r gamma_k dh_k - (r^3 / d) x_k sum_i gamma_i dh_i x_i
 //   c_k      = dh_k x_k r  -> part[0][row][k], summed over rows into dgamma
 // Every thread revisits only the elements it wrote, so part[0] needs no
 // cross-thread ordering; the row dot product goes through LDS.
 __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
-    float* __restrict__ part, const int32_t* __restrict__ idx, const SampleMeta* __restrict__ meta,
-    const uint16_t* __restrict__ x, const float* __restrict__ gamma,
-    const float* __restrict__ inv_rms, float* __restrict__ dx, int d, int64_t split_stride) {
+    float* __restrict__ part, const int32_t* __restrict__ idx, const SampleMeta* __restrict__ sm,
+    const SampleMeta* __restrict__ um, const uint16_t* __restrict__ x,
+    const float* __restrict__ gamma, const float* __restrict__ inv_rms, float* __restrict__ dx,
+    int d, int64_t split_stride) {
   __shared__ float red[4];
-  const int r = blockIdx.x;
-  if (r >= meta->n_rows) return;
-  const int n_split = meta->dx_split;
+  if ((int)blockIdx.x >= sm->s_rows) return;
+  const int r = sm->s_row_off + blockIdx.x;
+  const int n_split = um->dx_split;
   const int tid = threadIdx.x;
   float* p0 = part + (int64_t)r * d;
   const uint16_t* xr = x + (int64_t)idx[r] * d;
@@ -391,41 +407,45 @@ __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
   }
 }
 
-// dgamma[k] += sum over the sample's rows of part[0][row][k], in a fixed order:
-// partial sums over 256-row chunks, then the chunks in order.
+// dgamma[k] += sum over one sample's rows of part[0][row][k], in a fixed
+// order: partial sums over 256-row chunks of the sample, then the chunks in
+// order.
 __global__ __launch_bounds__(256) void k_dgamma_partial(const float* __restrict__ part,
-                                                        const SampleMeta* __restrict__ meta,
+                                                        const SampleMeta* __restrict__ sm,
                                                         float* __restrict__ gpart, int d) {
   const int k = blockIdx.x * 256 + threadIdx.x;
   const int r0 = blockIdx.y * 256;
   if (k >= d) return;
-  const int r1 = min(meta->n_rows, r0 + 256);
+  const int r1 = min(sm->s_rows, r0 + 256);
+  const float* base = part + (int64_t)sm->s_row_off * d;
   float acc = 0.f;
-  for (int r = r0; r < r1; ++r) acc += part[(int64_t)r * d + k];
+  for (int r = r0; r < r1; ++r) acc += base[(int64_t)r * d + k];
   gpart[(int64_t)blockIdx.y * d + k] = acc;
 }
 
 __global__ __launch_bounds__(256) void k_dgamma_final(const float* __restrict__ gpart,
-                                                      const SampleMeta* __restrict__ meta,
+                                                      const SampleMeta* __restrict__ sm,
                                                       float* __restrict__ dgamma, int d) {
   const int k = blockIdx.x * 256 + threadIdx.x;
   if (k >= d) return;
-  const int chunks = (meta->n_rows + 255) / 256;
+  const int chunks = (sm->s_rows + 255) / 256;
   float acc = 0.f;
   for (int c = 0; c < chunks; ++c) acc += gpart[(int64_t)c * d + k];
   dgamma[k] += acc;
 }
 
-hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, const uint16_t* x, const float* gamma,
-                                    float* dx, float* dgamma, int d, hipStream_t s) {
-  k_dx_reduce_rmsnorm<<<(unsigned)ws.NP, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta, x, gamma,
-                                                     ws.inv_rms, dx, d, ws.NP * d);
+hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const uint16_t* x,
+                                    const float* gamma, float* dx, float* dgamma, int d,
+                                    hipStream_t s) {
+  const SampleMeta* sm = ws.meta + g;
+  k_dx_reduce_rmsnorm<<<(unsigned)ws.NP, 256, 0, s>>>(ws.dx_part, ws.idx, sm, ws.unit(), x, gamma,
+                                                     ws.inv_rms, dx, d, ws.RP * d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 g1((unsigned)((d + 255) / 256), (unsigned)(ws.NP / 256));
-  k_dgamma_partial<<<g1, 256, 0, s>>>(ws.dx_part, ws.meta, ws.gpart, d);
+  k_dgamma_partial<<<g1, 256, 0, s>>>(ws.dx_part, sm, ws.gpart, d);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  k_dgamma_final<<<(unsigned)((d + 255) / 256), 256, 0, s>>>(ws.gpart, ws.meta, dgamma, d);
+  k_dgamma_final<<<(unsigned)((d + 255) / 256), 256, 0, s>>>(ws.gpart, sm, dgamma, d);
   return hipGetLastError();
 }
 

@@ -36,7 +36,7 @@ struct MaskWalker {
   }
 };
 
-// Vocabulary split of the dX GEMM for a sample with row_tiles 256-row tiles:
+// Vocabulary split of the dX GEMM for a unit with row_tiles 256-row tiles:
 // the split count s minimising an estimate of the GEMM's time on the
 // persistent grid, in units of one 256x256x64 slab on one workgroup:
 //   ceil(tiles / grid) rounds x (slabs per split + ~10 for the tile's
@@ -45,7 +45,7 @@ struct MaskWalker {
 // A fixed split leaves most of the last round idle for some row counts
 // (576 tiles on 256 workgroups use 2.25 of 3 rounds).
 __device__ void choose_dx_split(int row_tiles, const DxPlan& pl, int* split, int* kslab) {
-  // 32-bit divisions (tiles <= 4096 x 1024 x 16), 64-bit cost
+  // 32-bit divisions (tiles <= 16384 x 256 x 16), 64-bit cost
   int best_s = 1, best_ks = pl.kslabs;
   uint64_t best = ~0ull;
   for (int sp = 1; sp <= pl.s_max && row_tiles > 0; ++sp) {
@@ -64,18 +64,33 @@ __device__ void choose_dx_split(int row_tiles, const DxPlan& pl, int* split, int
   *kslab = best_ks;
 }
 
+// Pointers of a unit's row state handed to the mask kernel (all NULL for the
+// mask-only test hook, which writes positions to idx at row 0).
+struct MaskOut {
+  int32_t* idx;          // [rows]  masked flat positions, indexed by unit row
+  int32_t* row_tgt;      // [rows]  target token
+  int32_t* row_seq;      // [rows]  g*B + b
+  int32_t* seg_off;      // [B+1]   this sample's response offsets (unit rows)
+  uint32_t* t24;         // [B]     this sample's timesteps
+  SampleMeta* meta;      // this sample's record
+  int row_cap;           // rows the unit holds (padding is written up to it)
+};
+
 __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     const uint8_t* __restrict__ resp, const int32_t* __restrict__ targets, int B, int L, int n_t,
-    int j, int t_mode, uint32_t k0, uint32_t k1, uint32_t seq_base, int32_t* __restrict__ idx,
-    int32_t* __restrict__ row_tgt, int32_t* __restrict__ row_seq, int32_t* __restrict__ seg_off,
-    uint32_t* __restrict__ t24_out, SampleMeta* meta, int32_t* __restrict__ nm_out,
-    int nm_stride, float* __restrict__ t_out, int t_stride, int row_cap, int V,
+    int j, int g, int t_mode, uint32_t k0, uint32_t k1, uint32_t seq_base, MaskOut out,
+    int32_t* __restrict__ nm_out, int nm_stride, float* __restrict__ t_out, int t_stride, int V,
     const SampleMeta* prev, DxPlan plan) {
   __shared__ uint32_t sT[kMaxB];
   __shared__ int32_t sSeg[kMaxB + 1];
   __shared__ int32_t sWave[kMaskThreads / 64];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
+
+  // where this sample's rows start: after the unit's earlier samples (g > 0),
+  // or at row 0 of a new unit whose columns follow the previous unit's
+  const int row0 = (g > 0 && prev) ? prev->n_rows : 0;
+  const int col0 = prev ? (g > 0 ? prev->col_off : prev->col_end) : 0;
 
   for (int b = tid; b < B; b += kMaskThreads)
     sT[b] = timestep_t24(k0, k1, seq_base + (uint32_t)b, j, n_t, t_mode);
@@ -116,13 +131,14 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     const int b = (int)(p / L);
     if (p == (int64_t)b * L) sSeg[b] = base;
     if (mw2.masked(resp, sT, p)) {
-      if (idx) idx[base] = (int32_t)p;
-      if (row_tgt) {
+      const int r = row0 + base;
+      if (out.idx) out.idx[r] = (int32_t)p;
+      if (out.row_tgt) {
         // ids outside [0, V) are clamped so that no kernel reads outside W
         const int y = targets[p];
-        row_tgt[base] = y < 0 ? 0 : (y >= V ? V - 1 : y);
+        out.row_tgt[r] = y < 0 ? 0 : (y >= V ? V - 1 : y);
       }
-      if (row_seq) row_seq[base] = b;
+      if (out.row_seq) out.row_seq[r] = g * B + b;
       ++base;
     }
   }
@@ -130,62 +146,73 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
   __syncthreads();
 
   const int total = sSeg[B];
-  const int total_pad = (total + kRowPad - 1) / kRowPad * kRowPad;
+  const int rows = row0 + total;
+  const int rows_pad = (rows + kRowPad - 1) / kRowPad * kRowPad;
   for (int b = tid; b < B; b += kMaskThreads) {
     const int nm = sSeg[b + 1] - sSeg[b];
     if (nm_out) nm_out[(int64_t)b * nm_stride] = nm;
     if (t_out) t_out[(int64_t)b * t_stride] = (float)sT[b] * (1.0f / 16777216.0f);
-    if (seg_off) seg_off[b] = sSeg[b];
-    if (t24_out) t24_out[b] = sT[b];
+    if (out.seg_off) out.seg_off[b] = row0 + sSeg[b];
+    if (out.t24) out.t24[b] = sT[b];
   }
   if (tid == 0) {
-    if (seg_off) seg_off[B] = total;
-    if (meta) {
-      meta->n_rows = total;
-      meta->n_rows_pad = total_pad;
-      // this sample's columns in H_c^T / dZ^T follow those of the previous
-      // sample of the dW batch (prev may be this same record: read first)
-      const int off = prev ? prev->col_end : 0;
-      meta->col_off = off;
-      meta->col_end = off + (total + 63) / 64 * 64;
-      choose_dx_split(total_pad / kRowPad, plan, &meta->dx_split, &meta->dx_kslab);
+    if (out.seg_off) out.seg_off[B] = rows;
+    if (out.meta) {
+      SampleMeta* m = out.meta;
+      m->n_rows = rows;
+      m->n_rows_pad = rows_pad;
+      m->col_off = col0;
+      m->col_end = col0 + (rows + 63) / 64 * 64;
+      m->s_rows = total;
+      m->s_row_off = row0;
+      choose_dx_split(rows_pad / kRowPad, plan, &m->dx_split, &m->dx_kslab);
     }
   }
-  if (row_cap > 0) {
-    const int pad_end = min(total_pad, row_cap);
-    for (int r = total + tid; r < pad_end; r += kMaskThreads) {
-      if (row_tgt) row_tgt[r] = 0;
-      if (row_seq) row_seq[r] = B;
-    }
+  // padding rows up to the next row tile (a later sample of the unit
+  // overwrites them with its own rows)
+  const int pad_end = min(rows_pad, out.row_cap);
+  for (int r = rows + tid; r < pad_end; r += kMaskThreads) {
+    if (out.row_tgt) out.row_tgt[r] = 0;
+    if (out.row_seq) out.row_seq[r] = 0;
   }
 }
 
 hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int B, int L, int n_t,
-                               int j, int t_mode, uint64_t seed, uint32_t seq_base, int32_t* idx,
-                               int32_t* row_tgt, int32_t* row_seq, int32_t* seg_off, uint32_t* t24,
-                               SampleMeta* meta, int32_t* n_masked_out, int nm_stride,
-                               float* t_out, int t_stride, int row_cap, int V,
+                               int j, int g, int t_mode, uint64_t seed, uint32_t seq_base,
+                               const Workspace* ws, int32_t* idx_out, int32_t* n_masked_out,
+                               int nm_stride, float* t_out, int t_stride, int V,
                                const SampleMeta* prev, const DxPlan& plan, hipStream_t s) {
-  k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, t_mode,
+  MaskOut out{idx_out, nullptr, nullptr, nullptr, nullptr, nullptr, 0};
+  if (ws) {
+    out.idx = ws->idx;
+    out.row_tgt = ws->row_tgt;
+    out.row_seq = ws->row_seq;
+    out.seg_off = ws->seg_off + (int64_t)g * (B + 1);
+    out.t24 = ws->t24 + (int64_t)g * B;
+    out.meta = ws->meta + g;
+    out.row_cap = (int)ws->RP;
+  }
+  k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, g, t_mode,
                                             (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
-                                            seq_base, idx, row_tgt, row_seq, seg_off, t24, meta,
-                                            n_masked_out, nm_stride, t_out, t_stride, row_cap, V,
-                                            prev, plan);
+                                            seq_base, out, n_masked_out, nm_stride, t_out,
+                                            t_stride, V, prev, plan);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // Inverse RMS of the masked rows of the pre-norm activations x (for the final
 // RMSNorm h = gamma x r, r = (mean x^2 + eps)^(-1/2)): one wave per row, fp32
-// sum of squares.
-__global__ __launch_bounds__(256) void k_row_rms(const uint16_t* __restrict__ x,
-                                                 const int32_t* __restrict__ idx,
+// sum of squares.  Row r of the unit reads sample g = row_seq[r] / B, i.e.
+// x + g * stride.
+__global__ __launch_bounds__(256) void k_row_rms(const uint16_t* __restrict__ x, int64_t stride,
+                                                 int B, const int32_t* __restrict__ idx,
+                                                 const int32_t* __restrict__ row_seq,
                                                  const SampleMeta* __restrict__ meta,
                                                  float* __restrict__ inv_rms, int d, float eps) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= meta->n_rows) return;
-  const uint16_t* xr = x + (int64_t)idx[row] * d;
+  const uint16_t* xr = x + (int64_t)(row_seq[row] / B) * stride + (int64_t)idx[row] * d;
   float acc = 0.f;
   for (int k = lane * 8; k < d; k += 64 * 8) {
     const uint4 v = *reinterpret_cast<const uint4*>(xr + k);
@@ -202,18 +229,23 @@ __global__ __launch_bounds__(256) void k_row_rms(const uint16_t* __restrict__ x,
   if (lane == 0) inv_rms[row] = 1.f / sqrtf(acc / (float)d + eps);
 }
 
-hipError_t launch_row_rms(const uint16_t* x, const Workspace& ws, int d, float eps, hipStream_t s) {
-  k_row_rms<<<(unsigned)(ws.NP / 4), 256, 0, s>>>(x, ws.idx, ws.meta, ws.inv_rms, d, eps);
+hipError_t launch_row_rms(const uint16_t* x, int64_t stride, int B, const Workspace& ws, int d,
+                          float eps, hipStream_t s) {
+  k_row_rms<<<(unsigned)(ws.RP / 4), 256, 0, s>>>(x, stride, B, ws.idx, ws.row_seq, ws.unit(),
+                                                  ws.inv_rms, d, eps);
   return hipGetLastError();
 }
 
-// Gather: Hc[r, :] = hidden[idx[r], :] and HcT[:, col_off + r] for r < N; zeros
-// for N <= r < N_pad.  64x64 tiles staged in LDS for the transposed copy.
-// With `gamma`, `hidden` holds the pre-norm activations and the gathered row is
-// the final RMSNorm bf16(x * inv_rms[r] * gamma) (fp32 arithmetic, one
-// rounding to bfloat16).
+// Gather: Hc[r, :] = hidden_g[idx[r], :] and HcT[:, col_off + r] for the unit's
+// rows r < N (g = row_seq[r] / B: the row's sample, hidden_g = hidden + g *
+// stride); zeros for N <= r < N_pad.  64x64 tiles staged in LDS for the
+// transposed copy.  With `gamma`, `hidden` holds the pre-norm activations and
+// the gathered row is the final RMSNorm bf16(x * inv_rms[r] * gamma) (fp32
+// arithmetic, one rounding to bfloat16).
 __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hidden,
+                                                int64_t stride, int B,
                                                 const int32_t* __restrict__ idx,
+                                                const int32_t* __restrict__ row_seq,
                                                 const SampleMeta* __restrict__ meta,
                                                 const float* __restrict__ gamma,
                                                 const float* __restrict__ inv_rms,
@@ -233,7 +265,8 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
     const int r = r0 + row;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (r < N) {
-      v = *reinterpret_cast<const uint4*>(hidden + (int64_t)idx[r] * d + c0 + ch * 8);
+      const uint16_t* src = hidden + (int64_t)(row_seq[r] / B) * stride + (int64_t)idx[r] * d;
+      v = *reinterpret_cast<const uint4*>(src + c0 + ch * 8);
       if (gamma) {
         const float ir = inv_rms[r];
         const float4 g0 = *reinterpret_cast<const float4*>(gamma + c0 + ch * 8);
@@ -265,10 +298,11 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
   }
 }
 
-hipError_t launch_gather(const uint16_t* hidden, const float* gamma, const Workspace& ws, int d,
-                         hipStream_t s) {
-  dim3 grid((unsigned)(ws.NP / 64), (unsigned)(d / 64));
-  k_gather<<<grid, 256, 0, s>>>(hidden, ws.idx, ws.meta, gamma, ws.inv_rms, ws.Hc, ws.HcT, d, ws.KT);
+hipError_t launch_gather(const uint16_t* hidden, int64_t stride, int B, const float* gamma,
+                         const Workspace& ws, int d, hipStream_t s) {
+  dim3 grid((unsigned)(ws.RP / 64), (unsigned)(d / 64));
+  k_gather<<<grid, 256, 0, s>>>(hidden, stride, B, ws.idx, ws.row_seq, ws.unit(), gamma,
+                                ws.inv_rms, ws.Hc, ws.HcT, d, ws.KT);
   return hipGetLastError();
 }
 

@@ -124,12 +124,17 @@ def test_problem_struct_layout(b):
 
 
 def test_retained_workspace_grows_linearly_with_n_t(b):
-    sizes = [b.bgpo_workspace_size(_prob(b, n_t=n, bound=3, retain_samples=1)) for n in (1, 2, 4, 16, 64)]
-    per = sizes[1] - sizes[0]
-    assert per > 2 * 10 ** 9                       # H_c^T, dZ^T columns + state, B8 L512 head
-    for n, sz in zip((1, 2, 4, 16, 64), sizes):
-        assert sz == sizes[0] + (n - 1) * per
-    assert b.bgpo_workspace_size(_prob(b, n_t=64, bound=3)) < sizes[3]   # constant mode, any n_t
+    """Retained mode keeps the state of every unit of samples (8 samples per
+    unit at this shape, fewer when n_t is smaller): memory grows with n_t,
+    by the same amount per added unit."""
+    size = {n: b.bgpo_workspace_size(_prob(b, n_t=n, bound=3, retain_samples=1))
+            for n in (1, 2, 4, 8, 16, 24, 64)}
+    assert size[1] < size[2] < size[4] < size[8]
+    per_unit = size[16] - size[8]
+    assert per_unit > 16 * 10 ** 9                 # H_c^T, dZ^T columns + state of 8 samples
+    assert size[24] - size[16] == per_unit
+    assert size[64] - size[16] == 6 * per_unit
+    assert b.bgpo_workspace_size(_prob(b, n_t=64, bound=3)) < size[16]   # constant mode, any n_t
 
 
 def test_every_entry_point_lays_out_what_it_checked(b):
