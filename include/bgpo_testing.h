@@ -33,6 +33,7 @@ int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
  *             independent 4-wave workgroups per compute unit; 13: 128x256
  *         14: 4 waves of 128x128, K slab 32, 4 stages, 256-byte swizzle;
  *         15: as 14 with 5 stages
+ *         16: as 9 with the 256-byte swizzle; 17: as 10 with that swizzle
  * flags bit 0: M tiles consecutive in the tile walk (else N tiles);
  *       bit 1: plain workgroup order (no XCD grouping);
  *       bits 8-15: if nonzero, band height (M tiles) of the tile walk;

@@ -591,6 +591,8 @@ extern "C" int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, floa
     case 13: k_gemm<EPI_F32_STORE, 128, 256, 32, 64, 128, 3, 2, 1><<<2 * cus, 256, 0, s>>>(p); break;
     case 14: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 128, 4, 1, 1><<<cus, 256, 0, s>>>(p); break;
     case 15: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 128, 5, 1, 1><<<cus, 256, 0, s>>>(p); break;
+    case 16: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 4, 1, 1><<<cus, 512, 0, s>>>(p); break;
+    case 17: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 5, 1, 1><<<cus, 512, 0, s>>>(p); break;
     default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -3;
