@@ -12,6 +12,9 @@ the float64 oracle.
   test_gpu_parity: l within 1e-3, g tightly given l, dx / dgamma / dW within
   2e-2 relative max-norm.
 * on-policy: l from ``bgpo_elbo_fwd_rmsnorm`` fed back gives d == 0 exactly.
+* a sample range that starts inside and spans more than one unit of samples
+  (samples 3 .. 15 of 20: units of 8 and 5), per-sample activations through
+  the norm, off-policy: every sample against the oracle.
 * LLaDA head shape B8 L512 n_t 64 with the norm (shared activations, all
   samples): l, g, sampled dx rows and dW columns against the collapsed
   oracle on the float64 norm output.
@@ -50,13 +53,13 @@ def _bf16_dev(bits):
 class Run:
     """Device inputs / outputs of one workload for the f1 entry points."""
 
-    def __init__(self, w, x_bits, gamma, per_sample, j_count=None):
+    def __init__(self, w, x_bits, gamma, per_sample, j_count=None, j_begin=0):
         b = lib()
         base = workloads.generate(w, with_hidden=False)
         self.w, self.base = w, base
         self.dev = b.device_inputs(dict(base, hidden=None) | {"hidden": np.zeros((1,), np.uint16)})
-        jc = w.n_t if j_count is None else j_count
-        self.prob = b.Problem(w.B, w.L, w.d, w.V, w.n_t, j_begin=0, j_count=jc, seed=w.philox_seed,
+        jc = w.n_t - j_begin if j_count is None else j_count
+        self.prob = b.Problem(w.B, w.L, w.d, w.V, w.n_t, j_begin=j_begin, j_count=jc, seed=w.philox_seed,
                               seq_id_base=w.seq_id_base, t_mode=w.t_mode,
                               sample_stride=w.B * w.L * w.d if per_sample else 0, norm_eps=EPS)
         self.x = _bf16_dev(x_bits)
@@ -101,19 +104,20 @@ class Run:
             {"loss": float(self.loss.item())}
 
 
-def _oracle_problem(w):
-    return elbo.Problem(w.B, w.L, w.d, w.V, w.n_t, seed=w.philox_seed, seq_id_base=w.seq_id_base,
-                        t_mode=w.t_mode)
+def _oracle_problem(w, j_begin=0, j_count=None):
+    return elbo.Problem(w.B, w.L, w.d, w.V, w.n_t, j_begin=j_begin, j_count=j_count,
+                        seed=w.philox_seed, seq_id_base=w.seq_id_base, t_mode=w.t_mode)
 
 
-def _check(w, o, ref, adv, ell_old, loss_scale, with_norm):
-    for j in range(w.n_t):
+def _check(w, o, ref, adv, ell_old, loss_scale, with_norm, js=None):
+    js = range(w.n_t) if js is None else js
+    for j in js:
         assert np.array_equal(o["nm"][:, j], ref.n_masked[:, j])
         assert np.array_equal(o["t"][:, j].astype(np.float64), ref.t[:, j])
         np.testing.assert_allclose(o["ell"][:, j], ref.ell[:, j], rtol=ELL_RTOL, atol=0)
     g_of_ell = np.array([[elbo.bound_term(o["ell"][b, j] - ell_old[b, j], float(adv[b]), w.n_t)[0]
-                          for j in range(w.n_t)] for b in range(w.B)])
-    np.testing.assert_allclose(o["g"], g_of_ell, rtol=1e-12, atol=1e-15)
+                          for j in js] for b in range(w.B)])
+    np.testing.assert_allclose(o["g"][:, list(js)], g_of_ell, rtol=1e-12, atol=1e-15)
     assert abs(o["loss"] + loss_scale * g_of_ell.sum()) <= 1e-12 * loss_scale * np.abs(g_of_ell).sum()
     assert o["flags"] == 0
     assert rel_maxnorm(o["dx"], ref.dX) <= GRAD_RTOL, rel_maxnorm(o["dx"], ref.dX)
@@ -214,3 +218,31 @@ def test_llada_head_per_sample_copies_equal_shared():
     assert np.array_equal(sh["dW"], ps["dW"]) and np.array_equal(sh["dgamma"], ps["dgamma"])
     assert np.abs(sh["dx"]).max() > 0
     assert rel_maxnorm(ps["dx"].astype(np.float64).sum(axis=0), sh["dx"]) <= 1e-5
+
+
+def test_range_across_units_per_sample_rmsnorm():
+    """Samples are processed in units of up to 8 whose rows share the GEMM
+    launches; a range starting at j = 3 with 13 samples gives a full unit and
+    a partial one, each sample reading its own activations."""
+    w = workloads.TINY.replace(n_t=20, lengths=(24, 64), adv="normal", data_seed=2203)
+    jb, jc = 3, 13
+    xb = workloads.pre_norm_activations(w, jc)
+    gamma = workloads.norm_weight(w)
+    run = Run(w, xb, gamma, per_sample=True, j_count=jc, j_begin=jb)
+    base = run.base
+    X = elbo.bf16_to_f64(xb).reshape(xb.shape)
+    W = elbo.bf16_to_f64(base["W"]).reshape(w.d, w.V)
+    op = _oracle_problem(w, jb, jc)
+    g64 = gamma.astype(np.float64)
+    ell_old = np.random.default_rng(10).normal(0, 1.0, (w.B, w.n_t)) + elbo.elbo_per_sample(
+        op, X, W, base["targets"], base["resp_mask"], base["adv"], backward=False, gamma=g64,
+        eps=EPS, per_sample=True, head_bf16=True).ell
+    ref = elbo.elbo_per_sample(op, X, W, base["targets"], base["resp_mask"], base["adv"],
+                               ell_old=ell_old, loss_scale=0.25, gamma=g64, eps=EPS,
+                               per_sample=True, head_bf16=True)
+    run.bwd(ell_old=ell_old, loss_scale=0.25)
+    o = run.out()
+    outside = [j for j in range(w.n_t) if not jb <= j < jb + jc]
+    assert not o["ell"][:, outside].any() and not o["nm"][:, outside].any()
+    assert o["nm"][:, jb:jb + jc].sum() > 0
+    _check(w, o, ref, base["adv"], ell_old, 0.25, True, js=range(jb, jb + jc))
