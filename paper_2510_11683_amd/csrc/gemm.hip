@@ -403,6 +403,15 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
             for (int e = 0; e < 16; ++e)
               if (mw + 32 * i + mlane + (e & 3) + 8 * (e >> 2) >= M) acc[i][j][e] = -INFINITY;
       }
+      // EPI_FWDU stages the tile's exponentials in LDS (free once the ring is
+      // drained; 256 rows x 256 vocabulary ids x fp16 = the ring's 128 KB) as
+      // [row][vocabulary], 16-byte chunk c of row r at chunk c ^ (r mod 32) so
+      // that the 32 rows one write instruction touches hit distinct banks; the
+      // rows are then written out whole (two 512-byte rows per instruction)
+      // instead of 8-byte pieces scattered over 32 rows.
+      char* stage_u = reinterpret_cast<char*>(smem);
+      static_assert(!kStore || (BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2),
+                    "staging tile: 512-byte rows that fit the ring");
       float mref[TN], ssum[TN];
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
@@ -429,12 +438,13 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
             if constexpr (kStore) pk[q] = pack_f16x2(u0, u1);
           }
           if constexpr (kStore) {
+            // into the LDS staging tile: vocabulary ids m .. m+3 of row n
+            const int nl = n - n0;
 #pragma unroll
             for (int e4 = 0; e4 < 4; ++e4) {
-              const int m = mw + 32 * i + mlane + 8 * e4;   // vocabulary ids m .. m+3
-              if (m < M && n < N)
-                *reinterpret_cast<uint2*>(p.dZ + (int64_t)n * p.ldz + m) =
-                    make_uint2(pk[2 * e4], pk[2 * e4 + 1]);
+              const int ml = mw - m0 + 32 * i + 8 * e4;
+              *reinterpret_cast<uint2*>(stage_u + nl * 512 + (((ml >> 3) ^ (nl & 31)) << 4) +
+                                        mlane * 2) = make_uint2(pk[2 * e4], pk[2 * e4 + 1]);
             }
           }
         }
@@ -447,6 +457,24 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
         if (lane < 32 && mw < M && n < n_valid) {
           p.part_m[(int64_t)vt * p.ldp + n] = mref[j];
           p.part_s[(int64_t)vt * p.ldp + n] = st;
+        }
+      }
+      if constexpr (kStore) {
+        __syncthreads();
+        // lane l of a store instruction: row 2 q + l / 32 of the wave's rows,
+        // stored chunk l mod 32, i.e. logical chunk (l mod 32) ^ (row mod 32)
+        constexpr int ROWS_PER_WAVE = BN / (NT / 64);
+        // (the lane's chunk is re-derived here every tile: hoisted out of the
+        // tile loop, its 16 per-row variants would be spilled)
+        int pc = lane & 31;
+        asm volatile("" : "+v"(pc));
+#pragma unroll
+        for (int q = 0; q < ROWS_PER_WAVE / 2; ++q) {
+          const int row = wave * ROWS_PER_WAVE + 2 * q + (lane >> 5);
+          const int m = m0 + 8 * (pc ^ (row & 31));
+          const uint4 v = *reinterpret_cast<const uint4*>(stage_u + row * 512 + pc * 16);
+          if (n0 + row < N && m < M)
+            *reinterpret_cast<uint4*>(p.dZ + (int64_t)(n0 + row) * p.ldz + m) = v;
         }
       }
     } else {
