@@ -112,9 +112,10 @@ class Timer {
  public:
   Timer(bgpo_timing* out, hipStream_t s) : out_(out), s_(s) {}
   ~Timer() {
+    // best-effort release; a failure here cannot be reported from a destructor
     for (auto& e : ev_) {
-      hipEventDestroy(e.a);
-      hipEventDestroy(e.b);
+      if (e.a) (void)hipEventDestroy(e.a);
+      if (e.b) (void)hipEventDestroy(e.b);
     }
   }
   hipError_t begin(int kind) {
