@@ -105,8 +105,9 @@ hipError_t launch_combine_rows(const Workspace& ws, int V, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Per-response terms of the samples of a unit.  One workgroup; samples and
-// responses in order.
+// Per-response terms of the samples of a unit.  One workgroup; each wave
+// takes (sample, response) segments wave, wave + 16, ...; the loss is then
+// summed by one thread over the segments in sample-then-response order.
 constexpr int kSeqThreads = 1024;
 
 // The objective's per-sample term g and its derivative dg/dl for
@@ -144,51 +145,49 @@ __global__ __launch_bounds__(kSeqThreads) void k_seq_terms(
     double* __restrict__ ell, double* __restrict__ g, double* __restrict__ loss,
     int32_t* __restrict__ flags, float* __restrict__ seq_scale, float* __restrict__ row_scale,
     int backward, int bound, const double* __restrict__ dbar) {
-  __shared__ double red[kSeqThreads / 64];
   __shared__ int s_bad;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) s_bad = 0;
-  double loss_acc = 0.0;
-  for (int gs = 0; gs < n_samples; ++gs) {
-    const int j = j0 + gs;
-    for (int b = 0; b < B; ++b) {
-      const int r0 = seg_off[gs * (B + 1) + b], r1 = seg_off[gs * (B + 1) + b + 1];
-      double acc = 0.0;
-      for (int r = r0 + tid; r < r1; r += kSeqThreads) acc += (double)lp[r];
+  __syncthreads();
+  const int n_seg = n_samples * B;
+  for (int sg = wave; sg < n_seg; sg += kSeqThreads / 64) {
+    const int gs = sg / B, b = sg - gs * B, j = j0 + gs;
+    const int r0 = seg_off[gs * (B + 1) + b], r1 = seg_off[gs * (B + 1) + b + 1];
+    double acc = 0.0;
+    for (int r = r0 + lane; r < r1; r += 64) acc += (double)lp[r];
 #pragma unroll
-      for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-      if (lane == 0) red[wave] = acc;
-      __syncthreads();
-      if (tid == 0) {
-        double sum = 0.0;
-        for (int w = 0; w < kSeqThreads / 64; ++w) sum += red[w];
-        const double t = (double)t24[gs * B + b] * (1.0 / 16777216.0);
-        const double l = sum / t;                                      // Eq. per_step_loss
-        const int64_t o = (int64_t)b * n_t + j;
-        ell[o] = l;
-        if (backward) {
-          const double dj = ell_old ? l - ell_old[o] : 0.0;
-          double gj, dg;
-          bound_term(dj, (double)adv[b], n_t, bound, dbar ? dbar[b] : 0.0, &gj, &dg);
-          g[o] = gj;
-          loss_acc += -loss_scale * gj;
-          const double sc = loss_scale * dg / t;
-          seq_scale[gs * B + b] = (float)sc;
-          if (!isfinite(l) || !isfinite(gj) || !isfinite(sc) || !isfinite((float)sc)) s_bad = 1;
-        } else if (!isfinite(l)) {
-          s_bad = 1;
-        }
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) {
+      const double t = (double)t24[gs * B + b] * (1.0 / 16777216.0);
+      const double l = acc / t;                                        // Eq. per_step_loss
+      const int64_t o = (int64_t)b * n_t + j;
+      ell[o] = l;
+      if (backward) {
+        const double dj = ell_old ? l - ell_old[o] : 0.0;
+        double gj, dg;
+        bound_term(dj, (double)adv[b], n_t, bound, dbar ? dbar[b] : 0.0, &gj, &dg);
+        g[o] = gj;
+        const double sc = loss_scale * dg / t;
+        seq_scale[gs * B + b] = (float)sc;
+        if (!isfinite(l) || !isfinite(gj) || !isfinite(sc) || !isfinite((float)sc)) s_bad = 1;
+      } else if (!isfinite(l)) {
+        s_bad = 1;
       }
-      __syncthreads();
     }
   }
+  // g and seq_scale of every segment are written (global memory) before here
+  __threadfence_block();
+  __syncthreads();
   if (tid == 0) {
-    if (backward) loss[0] += loss_acc;
+    if (backward) {
+      double loss_acc = 0.0;
+      for (int gs = 0; gs < n_samples; ++gs)
+        for (int b = 0; b < B; ++b) loss_acc += -loss_scale * g[(int64_t)b * n_t + j0 + gs];
+      loss[0] += loss_acc;
+    }
     if (s_bad && flags) atomicOr(flags, kFlagNonfinite);
   }
   if (backward) {
-    // seq_scale was written by thread 0 before the last barrier
-    __threadfence_block();
     const int N = meta->n_rows, NPr = meta->n_rows_pad;
     for (int r = tid; r < NPr; r += kSeqThreads) row_scale[r] = r < N ? seq_scale[row_seq[r]] : 0.f;
   }
