@@ -105,7 +105,10 @@ enum { BGPO_T_IID = 0, BGPO_T_STRATIFIED = 1 };
  * (about 2.2 GB per sample at B=8, L=512, d=4096, V=126464), which is the
  * memory cost that BGPO's linear bound removes; use it to measure that
  * contrast.  retain_samples = 1 with another bound returns
- * BGPO_ERR_INVALID_ARG. */
+ * BGPO_ERR_INVALID_ARG.  The retained rows (n_t rounded up to whole units of
+ * samples, times B*L rounded up to 256 per sample) must stay below 2^22;
+ * larger retained problems return BGPO_ERR_UNSUPPORTED from every entry
+ * point, bgpo_workspace_size included. */
 enum { BGPO_BOUND_PAPER = 0, BGPO_BOUND_TAYLOR = 1, BGPO_BOUND_JENSEN = 2, BGPO_BOUND_EXACT = 3 };
 
 /* Bits of *status_flags (device int32, OR-ed in, never cleared by the library). */

@@ -167,6 +167,13 @@ static int check_problem(const bgpo_problem* p) {
   if (p->B > 4096 || (int64_t)p->B * p->L > (1 << 20) || p->d % 64 || p->V % 64 || p->d < 64 ||
       p->d > 65536 || p->V < 64 || p->V > (1 << 20))
     return BGPO_ERR_UNSUPPORTED;
+  // H_c^T and dZ^T (leading dimension KT) are operand panels of the dW GEMM.
+  // One unit's row capacity stays within 65535 * 64 by construction; with
+  // every sample retained KT grows with n_t and is bounded here.
+  static_assert(int64_t(65535) * 64 <= kMaxPanelLd, "constant-mode KT must fit a panel");
+  Workspace w;
+  workspace_layout(Dims{p->B, p->L, p->d, p->V, p->n_t}, p->retain_samples, nullptr, &w, nullptr);
+  if (w.KT > kMaxPanelLd) return BGPO_ERR_UNSUPPORTED;
   return BGPO_OK;
 }
 

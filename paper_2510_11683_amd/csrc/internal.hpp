@@ -16,6 +16,11 @@ constexpr int kVocabTile = 128;
 
 constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
 
+// The GEMMs address each 256-row operand panel through one buffer descriptor
+// with 32-bit byte offsets below 2^31, so a bf16 operand's leading dimension
+// must stay at or below this.
+constexpr int64_t kMaxPanelLd = (int64_t(1) << 22) - 1;
+
 // Device-resident bookkeeping written by the mask kernel, one record per
 // sample.  Samples are processed in units of up to G consecutive samples whose
 // masked rows sit back to back in one row space (the LM-head GEMMs and the row

@@ -183,3 +183,18 @@ def test_reserved_field_and_rmsnorm_arguments_rejected_before_hip(b):
     # misaligned norm weight
     assert lib.bgpo_elbo_fwd_rmsnorm(ctypes.byref(p), fake, ctypes.c_void_p(0x1004), fake, fake,
                                      fake, fake, fake, None, ws, nbytes.value, None, None) == -1
+
+
+def test_retained_rows_bounded_by_the_dw_panel_range(b):
+    """The dW GEMM reads H_c^T and dZ^T through buffer descriptors whose byte
+    offsets stay below 2^31: with every sample retained, the kept rows (whole
+    units of samples, B*L rounded up to 256 per sample) must stay below 2^22.
+    At B*L = 2^20 a unit holds 3 samples: n_t = 3 keeps 3 * 2^20 rows, n_t = 4
+    two units (6 * 2^20); the constant mode takes any n_t."""
+    big = dict(B=4096, L=256, d=64, V=128, bound=3)
+    assert b.bgpo_workspace_size(_prob(b, n_t=3, retain_samples=1, **big)) > 0
+    for n_t in (4, 64):
+        with pytest.raises(b.BgpoError) as e:
+            b.bgpo_workspace_size(_prob(b, n_t=n_t, retain_samples=1, **big))
+        assert e.value.status == -4
+    assert b.bgpo_workspace_size(_prob(b, n_t=1000, **big)) == b.bgpo_workspace_size(_prob(b, n_t=1, **big))
