@@ -120,15 +120,17 @@ class Timer {
   }
   hipError_t begin(int kind) {
     if (!out_) return hipSuccess;
-    Ev e{kind, nullptr, nullptr};
+    Ev e{kind, 0, nullptr, nullptr};
     hipError_t r = hipEventCreate(&e.a);
     if (r == hipSuccess) r = hipEventCreate(&e.b);
     if (r == hipSuccess) r = hipEventRecord(e.a, s_);
     ev_.push_back(e);
     return r;
   }
-  hipError_t end() {
+  // closes the range opened by the last begin(); `launches` kernels ran in it
+  hipError_t end(int launches = 1) {
     if (!out_) return hipSuccess;
+    ev_.back().launches = launches;
     return hipEventRecord(ev_.back().b, s_);
   }
   hipError_t finish() {
@@ -140,14 +142,14 @@ class Timer {
       r = hipEventElapsedTime(&ms, e.a, e.b);
       if (r != hipSuccess) return r;
       out_->ms[e.kind] += ms;
-      out_->launches[e.kind] += 1;
+      out_->launches[e.kind] += e.launches;
     }
     return hipSuccess;
   }
 
  private:
   struct Ev {
-    int kind;
+    int kind, launches;
     hipEvent_t a, b;
   };
   bgpo_timing* out_;
@@ -219,11 +221,11 @@ static int run_forward_unit(const bgpo_problem* p, Workspace& ws, Timer& tm, int
                                  t_out ? t_out + j : nullptr, dm.n_t, dm.V,
                                  gs ? ws.meta + (gs - 1) : prev_unit, dx_plan(dm, ws, grid), s));
   }
-  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.end(n_s));
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
   if (act.gamma) BGPO_TRY(launch_row_rms(act.at(j0), act.stride, dm.B, ws, dm.d, act.eps, s));
   BGPO_TRY(launch_gather(act.at(j0), act.stride, dm.B, act.gamma, ws, dm.d, s));
-  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.end(act.gamma ? 2 : 1));
   BGPO_TRY(tm.begin(BGPO_K_FWD));
   BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, store_u, s));
   BGPO_TRY(tm.end());
@@ -232,7 +234,7 @@ static int run_forward_unit(const bgpo_problem* p, Workspace& ws, Timer& tm, int
   BGPO_TRY(launch_combine_rows(ws, dm.V, s));
   BGPO_TRY(launch_seq_terms(ws, dm.B, dm.n_t, j0, adv, ell_old, loss_scale, ell, g, loss, flags,
                             backward, p->bound, dbar, s));
-  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.end(3));
   return BGPO_OK;
 }
 
@@ -316,7 +318,7 @@ static int unit_backward(const Workspace& ws, const Act& act, int j0, int j_begi
     else
       BGPO_TRY(launch_dx_reduce(ws, gs, dXj, dm.d, s));
   }
-  BGPO_TRY(tm.end());
+  BGPO_TRY(tm.end(ws.g_used * (act.gamma ? 3 : 1)));   // the norm backward is 3 kernels
   return BGPO_OK;
 }
 
