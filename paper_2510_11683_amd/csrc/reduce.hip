@@ -229,23 +229,30 @@ hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, in
 // Eq. per_step_loss, d l / d z = (onehot - p) / t; s carries -loss_scale dg/dl
 // and the 1/t.)  At the target the value comes from the fp32 target logit,
 // s (2^(z_y log2e - lse2) - 1), not from the rounded u.  Padded rows become
-// zeros.  One workgroup per (64-row chunk, slice): the rows are read and
+// zeros.  One workgroup per (128-row chunk, slice): the rows are read and
 // rewritten in 256-byte runs, and the transposed copy dZ^T[v][col_off + row]
-// is assembled in LDS and written as 128-byte runs of 64 rows.
+// is assembled in LDS and written as 256-byte runs of 128 rows.
+constexpr int kGradRows = 128;
+static_assert(kRowPad % kGradRows == 0, "padded row counts must hold whole chunks");
+
 __global__ __launch_bounds__(256) void k_softmax_grad(
     const float* __restrict__ part_m, const float* __restrict__ lse2,
     const float* __restrict__ row_scale, const float* __restrict__ ztgt,
     const int32_t* __restrict__ row_tgt, const SampleMeta* __restrict__ meta,
     uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT, int V, int64_t ldp, int64_t ldzt) {
-  constexpr int kTS = 33;                                // words per vocabulary id in the tile
-  __shared__ float s_c[64], s_oh[64];
-  __shared__ int s_y[64];
-  __shared__ uint32_t tile[kVocabTile * kTS];            // [v][row pair], (row 2k, row 2k+1)
-  const int h = blockIdx.x, r0 = blockIdx.y * 64;
-  if (r0 >= meta->n_rows_pad) return;   // n_rows_pad is a multiple of 64: chunks are whole
+  constexpr int kPairs = kGradRows / 2;                  // words per vocabulary id in the tile
+  __shared__ float s_c[kGradRows], s_oh[kGradRows];
+  __shared__ int s_y[kGradRows];
+  // [v][row pair] words (row 2k, row 2k+1), row pair k of vocabulary id v at
+  // word v * kPairs + (k ^ 4 (v / 8)): the 16 lanes that read one row's slice
+  // (v / 8 = 0 .. 15) write 16 different banks, and aligned groups of 4 row
+  // pairs stay together and in order for the 16-byte reads of dZ^T
+  __shared__ __align__(16) uint32_t tile[kVocabTile * kPairs];
+  const int h = blockIdx.x, r0 = blockIdx.y * kGradRows;
+  if (r0 >= meta->n_rows_pad) return;   // n_rows_pad is a multiple of 256: chunks are whole
   const int N = meta->n_rows;
   const int tid = threadIdx.x;
-  if (tid < 64) {
+  if (tid < kGradRows) {
     const int r = r0 + tid;
     float c = 0.f, oh = 0.f;
     int y = -1;
@@ -264,7 +271,7 @@ __global__ __launch_bounds__(256) void k_softmax_grad(
   const int nv = min(kVocabTile, V - v_lo);   // 128, or 64 in a last half slice
   const int cpr = nv / 8;                     // 16-byte chunks per row
   // rows 2 rp and 2 rp + 1, vocabulary ids v0 .. v0 + 7
-  for (int q = tid; q < 32 * cpr; q += 256) {
+  for (int q = tid; q < kPairs * cpr; q += 256) {
     const int vc = q % cpr, rp = q / cpr;
     const int ra = 2 * rp, v0 = v_lo + vc * 8;
     uint4* pa = reinterpret_cast<uint4*>(dZ + (int64_t)(r0 + ra) * V + v0);
@@ -290,26 +297,27 @@ __global__ __launch_bounds__(256) void k_softmax_grad(
     }
     *pa = make_uint4(oa[0], oa[1], oa[2], oa[3]);
     *pb = make_uint4(ob[0], ob[1], ob[2], ob[3]);
+    const int w = rp ^ (4 * vc);              // vl / 8 == vc for all 8 ids below
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int vl = vc * 8 + 2 * k;
-      tile[vl * kTS + rp] = (oa[k] & 0xFFFFu) | (ob[k] << 16);
-      tile[(vl + 1) * kTS + rp] = (oa[k] >> 16) | (ob[k] & 0xFFFF0000u);
+      tile[vl * kPairs + w] = (oa[k] & 0xFFFFu) | (ob[k] << 16);
+      tile[(vl + 1) * kPairs + w] = (oa[k] >> 16) | (ob[k] & 0xFFFF0000u);
     }
   }
   __syncthreads();
-  // dZ^T: 8 lanes (64 rows, 128 bytes) per vocabulary id
+  // dZ^T: 16 lanes (128 rows, 256 bytes) per vocabulary id; lane c takes row
+  // pairs 4c .. 4c + 3, stored at 4 (c ^ (vl / 8))
   uint16_t* zt = dZT + meta->col_off;
-  for (int q = tid; q < nv * 8; q += 256) {
-    const int vl = q >> 3, c = q & 7;
-    const uint32_t* src = tile + vl * kTS + 4 * c;
-    *reinterpret_cast<uint4*>(zt + (int64_t)(v_lo + vl) * ldzt + r0 + 8 * c) =
-        make_uint4(src[0], src[1], src[2], src[3]);
+  for (int q = tid; q < nv * 16; q += 256) {
+    const int vl = q >> 4, c = q & 15;
+    const uint4 v = *reinterpret_cast<const uint4*>(tile + vl * kPairs + 4 * (c ^ (vl >> 3)));
+    *reinterpret_cast<uint4*>(zt + (int64_t)(v_lo + vl) * ldzt + r0 + 8 * c) = v;
   }
 }
 
 hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s) {
-  dim3 grid((unsigned)ws.nvt, (unsigned)(ws.RP / 64));
+  dim3 grid((unsigned)ws.nvt, (unsigned)(ws.RP / kGradRows));
   k_softmax_grad<<<grid, 256, 0, s>>>(ws.part_m, ws.lse2, ws.row_scale, ws.ztgt, ws.row_tgt,
                                       ws.unit(), ws.dZ, ws.dZT, V, ws.RP, ws.KT);
   return hipGetLastError();
