@@ -43,6 +43,10 @@
  *     caller's `workspace` of at least bgpo_workspace_size() bytes (256-byte
  *     aligned).  Its size depends on B, L, d and V, never on n_t (except in
  *     the retain_samples contrast mode below).
+ *   - Without a timing record a call only enqueues kernels (no allocation,
+ *     memory set or copy, no synchronisation), so it can be captured into a
+ *     HIP graph and replayed; the graph then reads and writes the buffers
+ *     that were passed at capture time.
  *   - Host-detectable errors return a negative bgpo_status before anything is
  *     enqueued; HIP launch errors return BGPO_ERR_HIP.  No C++ exception
  *     crosses the ABI.  Entry points keep no mutable global state; calls on

@@ -304,6 +304,74 @@ def test_timing_record_counts_kernel_launches():
     assert got2 == {**got, "transpose_w": 2, "mask": 20, "gather": 4, "fwd": 4, "ell": 12}
 
 
+def test_concurrent_streams_match_sequential():
+    """Two problems, each with its own workspace, run on two streams at the
+    same time give the same bits as one after the other: the entry points
+    keep no state between calls, and every reduction has a fixed order."""
+    wa = MID.replace(n_t=3)
+    wb = MID.replace(n_t=5, data_seed=2002, philox_seed=0xB6B10002)
+    xa, xb = workloads.generate(wa), workloads.generate(wb)
+    r = Runner(wb, xb)
+    r.fwd()
+    old_b = r.out()["ell"] + np.random.default_rng(12).normal(0, 0.5, (wb.B, wb.n_t))  # off-policy
+    del r
+    seq = []
+    for w, x, eo in ((wa, xa, None), (wb, xb, old_b)):
+        r = Runner(w, x)
+        r.bwd(ell_old=eo)
+        r.bwd(ell_old=eo)                 # the second call accumulates onto the first
+        seq.append(r.out())
+        del r
+    ra, rb = Runner(wa, xa), Runner(wb, xb)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    cur = torch.cuda.current_stream()
+    sa.wait_stream(cur)
+    sb.wait_stream(cur)
+    for _ in range(2):
+        with torch.cuda.stream(sa):
+            ra.bwd()
+        with torch.cuda.stream(sb):
+            rb.bwd(ell_old=old_b)
+    cur.wait_stream(sa)
+    cur.wait_stream(sb)
+    for o, e in ((ra.out(), seq[0]), (rb.out(), seq[1])):
+        for k in ("ell", "g", "nm", "t", "dX", "dW"):
+            assert np.array_equal(o[k], e[k]), k
+        assert o["loss"] == e["loss"] and o["flags"] == e["flags"] == 0
+        assert np.abs(o["dX"]).max() > 0
+
+
+def test_graph_capture_replays_match_eager():
+    """A whole backward call captured in a HIP graph (the library allocates
+    nothing, sets no memory and does not synchronise without a timing record,
+    so every launch records) and replayed three times, with eager zeroing and
+    a host synchronisation between replays: every replay gives the eager
+    call's bits."""
+    w = MID.replace(n_t=4)
+    x = workloads.generate(w)
+    r = Runner(w, x)
+    r.bwd()
+    eager = r.out()
+    b, d = lib(), r.dev
+    prob = problem(w)
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        b.bgpo_elbo_bwd_accumulate(prob, d["hidden"], d["W"], d["targets"], d["resp_mask"],
+                                   d["adv"], None, 1.0 / 8, r.dX, r.dW, r.ell, r.g, r.loss, r.nm,
+                                   r.t, r.flags, r.ws)
+    for _ in range(3):
+        r.zero_grads()
+        for t in (r.ell, r.g, r.nm, r.t):
+            t.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        o = r.out()
+        for k in ("ell", "g", "nm", "t", "dX", "dW"):
+            assert np.array_equal(o[k], eager[k]), k
+        assert o["loss"] == eager["loss"] and o["flags"] == 0
+
+
 def test_empty_range_and_empty_masks():
     w = MID
     x = workloads.generate(w)
