@@ -52,7 +52,11 @@ size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
   const int64_t per_split = RP * dm.d * 4;
   const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t(4) << 30) / per_split));
   const int64_t dw_batch = n_units;
-  const int64_t KT = dw_batch * RP;
+  // leading dimension of H_c^T and dZ^T: the dW GEMM reads 256-row panels of
+  // both, and with a power-of-two row pitch (32768 rows of bf16 = 64 KB at
+  // the benchmark shape) their rows crowd into the same memory channels;
+  // 64 extra columns (128 bytes) spread them
+  const int64_t KT = dw_batch * RP + kPanelPad;
 
   size_t off = 0;
   char* b = static_cast<char*>(base);
@@ -172,7 +176,8 @@ static int check_problem(const bgpo_problem* p) {
   // H_c^T and dZ^T (leading dimension KT) are operand panels of the dW GEMM.
   // One unit's row capacity stays within 65535 * 64 by construction; with
   // every sample retained KT grows with n_t and is bounded here.
-  static_assert(int64_t(65535) * 64 <= kMaxPanelLd, "constant-mode KT must fit a panel");
+  static_assert(int64_t(65535) * 64 / 256 * 256 + kPanelPad <= kMaxPanelLd,
+                "constant-mode KT must fit a panel");
   Workspace w;
   workspace_layout(Dims{p->B, p->L, p->d, p->V, p->n_t}, p->retain_samples, nullptr, &w, nullptr);
   if (w.KT > kMaxPanelLd) return BGPO_ERR_UNSUPPORTED;

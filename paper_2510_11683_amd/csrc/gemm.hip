@@ -1,28 +1,32 @@
-// bf16 MFMA GEMM core for gfx950 and its four epilogues.
+// bf16 MFMA GEMM cores for gfx950 and their four epilogues.
 //
 // Every contraction of the ELBO head is written in one "NT" form,
 //     C[m][n] = sum_k A[m][k] * B[n][k]      (A, B row-major, K contiguous),
-// so both operands load as 16-byte K-contiguous vectors that match the
-// v_mfma_f32_32x32x16_bf16 operand layout directly:
+// so both operands load as 16-byte K-contiguous vectors that match the MFMA
+// operand layouts directly:
 //   forward               Z^T[v][row] = WT[v][:] . Hc[row][:]     (K = d)
-//   dX (split over V)     dX[row][c]  = dZ[row][:] . W[c][:]      (K = V)
-//   dW                    dW[c][v]   += HcT[c][:] . dZT[v][:]     (K = rows)
-// The logits are produced as Z^T (vocabulary along M) so that, in the 32x32
-// accumulator layout, each lane holds 64 vocabulary entries of only 4 rows:
-// the per-row max / sum-exp reductions are in-lane plus one lane swap.
+//   dX (split over V)     dX^T[c][row] = W[c][:] . dZ[row][:]     (K = V)
+//   dW                    dW^T[v][c]  += dZT[v][:] . HcT[c][:]    (K = rows)
+// The logits are produced as Z^T (vocabulary along M) so that each lane holds
+// vocabulary entries of few rows: the per-row max / sum-exp reductions are
+// in-lane plus lane swaps.  dX and dW are produced transposed and stored
+// transposed, so that a lane's 4 accumulator values land in one 16-byte store.
 //
-// Scheduling: a persistent grid of one 512-thread workgroup (eight waves, two
-// per SIMD) per compute unit walks the tile list in bands of M tiles;
-// consecutive tiles (sharing operand panels) go to workgroups of the same XCD
-// (workgroup w runs on XCD w mod 8), so the shared panels are served from that
-// XCD's L2.
+// Scheduling: a persistent grid of one workgroup per compute unit walks the
+// tile list in bands of M tiles; consecutive tiles (sharing operand panels)
+// go to workgroups of the same XCD (workgroup w runs on XCD w mod 8), so the
+// shared panels are served from that XCD's L2.
 //
 // Pipeline: a two-stage LDS ring of 64-deep K slabs, filled by direct
 // buffer-to-LDS loads (no staging registers); a stage is refilled with the
 // slab two ahead as soon as the barrier that ends its last use has passed.
 // LDS rows are XOR-swizzled in 16-byte chunks so that fragment reads of
-// consecutive rows hit distinct banks.  Fragment reads for the next K
-// sub-step and the slab loads are spread evenly between the MFMAs.
+// consecutive rows hit distinct banks.
+//
+// k_gemm4w (production): four waves of 128x128 on 16x16x32 MFMAs in inline
+// assembly with accumulators in AGPRs, hand-ordered (see below).  k_gemm
+// (the earlier core, kept for the tile-configuration test hook): eight waves
+// of 128x64 on compiler-scheduled 32x32x16 MFMAs.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -490,12 +494,360 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, OCC) void k_gemm(GemmPa
 #endif
 }
 
-// Tile configuration of the production kernels: 256x256 block tile, K slab
-// 64 in a 2-stage LDS ring, eight waves (two per SIMD, so one wave's memory
-// instructions issue while the other's MFMAs run), each owning a 128x64
-// sub-tile (4x2 MFMA 32x32 tiles), 256-byte LDS swizzle.
-#define BGPO_TILE 256, 256, 64, 128, 64, 2, 1, 1
-constexpr int kGemmThreads = 512;
+// ---------------------------------------------------------------------------
+// The production kernel: one wave per SIMD on v_mfma_f32_16x16x32_bf16.
+//
+// Lane l of a 16x16x32 MFMA holds A[m = l % 16][k = 8 (l / 16) + t] and
+// B[k = 8 (l / 16) + t][n = l % 16] (t = 0..7: one 16-byte LDS chunk each)
+// and accumulates C[m = 4 (l / 16) + e][n = l % 16] (e = 0..3).  A 256x256
+// block tile is split over four waves of 128x128, so each wave holds 8x8
+// accumulator blocks (all 256 AGPRs) and reads, per 64-deep slab, its 128 rows
+// of A and of B once: a third less LDS traffic per MFMA than eight waves of
+// 128x64, and the 16x16x32 form moves half the accumulator bytes per FLOP of
+// the 32x32x16 form, which keeps the clock higher under the power cap.
+//
+// The MFMAs are inline assembly on accumulators tied to AGPRs ("+a"): with
+// the compiler's own MFMA builtins on 256 accumulator registers the register
+// allocator moved accumulators through spare AGPRs on every iteration.  The
+// instruction order is fixed by hand: per 32-deep sub-step 64 MFMAs, with one
+// fragment read of the next sub-step after every fourth MFMA (both operands'
+// fragments double-buffered in VGPRs) and, in the sub-step after a slab
+// barrier, one slab load after every fourth as well.  Because the compiler
+// does not see these MFMAs as such, the code pads the two hazards it would
+// otherwise cover: accumulator writes before the first MFMA reads them, and
+// the last MFMAs' results before the epilogue reads them.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define BGPO_MFMA16(acc, a, b) \
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b))
+
+// fp32 store of a wave tile of 16x16 accumulator blocks, transposed: element
+// (m, n) goes to out[n * ldo + m], so a lane's 4 values of one block
+// (m = 4 (lane / 16) .. + 3 of one n) are one 16-byte store.  ACCUM: add to
+// the current values (read first, one column block at a time).  M is a
+// multiple of 4 (the vocabulary and hidden sizes are multiples of 64).
+template <bool ACCUM, bool FULL, int TM, int TN>
+__device__ __forceinline__ void epi_f32_16t(const f32x4 (&acc)[TM][TN], float* outb, int64_t ldo,
+                                            int mw, int nw, int lane, int M, int N) {
+  const int mlane = 4 * (lane >> 4);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int n = nw + 16 * j + (lane & 15);
+    float* col = outb + (int64_t)n * ldo + mw + mlane;
+    f32x4 old[TM];
+    if constexpr (ACCUM) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        old[i] = (FULL || (mw + 16 * i + mlane < M && n < N))
+                     ? *reinterpret_cast<const f32x4*>(col + 16 * i)
+                     : (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      if (FULL || (mw + 16 * i + mlane < M && n < N))
+        *reinterpret_cast<f32x4*>(col + 16 * i) = ACCUM ? old[i] + acc[i][j] : acc[i][j];
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int EPI, int BM, int BN, int BK, int STAGES, int SWZ>
+__global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature
+  constexpr int WM = 128, WN = 128;
+  using C = Cfg<BM, BN, BK, WM, WN, SWZ>;
+  constexpr int NT = C::NT, KCH = C::KCH;
+  constexpr int TM = WM / 16, TN = WN / 16;
+  static_assert(C::NWAVES == 4 && BK == 64, "four waves, 64-deep slabs (two sub-steps)");
+  __shared__ uint4 smem[STAGES * (BM + BN) * KCH];
+  uint4* As = smem;                           // [STAGES][BM][KCH]
+  uint4* Bs = smem + STAGES * BM * KCH;       // [STAGES][BN][KCH]
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, kept in an SGPR
+  const int wm = wave / C::NWN, wn = wave % C::NWN;
+
+  int M = p.M, N = p.N, K = p.K, n_valid = p.N;
+  if (p.dyn_m) { M = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
+  if (p.dyn_n) { N = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
+  if (p.dyn_k) K = p.meta->col_end;    // batched dW: all samples' columns (multiple of 64)
+  int n_split = p.n_split;
+  int64_t k_split = p.k_split;
+  if (p.dyn_split) {
+    n_split = p.meta->dx_split;
+    k_split = (int64_t)p.meta->dx_kslab * BK;
+  }
+  if (EPI == EPI_F32_ACCUM && K == 0) return;   // nothing to add
+  const int tilesM = (M + BM - 1) / BM, tilesN = (N + BN - 1) / BN;
+  const int64_t total = (int64_t)tilesM * tilesN * n_split;
+  const int G = gridDim.x;
+  const int w = blockIdx.x;
+  const int xcd_slot = (G % 8 == 0 && !p.plain_order) ? (w % 8) * (G / 8) + w / 8 : w;
+
+  for (int64_t base = 0; base < total; base += G) {
+    const int64_t t = base + xcd_slot;
+    if (t >= total) continue;
+    // the lane index, re-derived every tile: addresses computed from it are
+    // then not hoisted out of the tile loop (with all 256 AGPRs holding
+    // accumulators, such hoisted values would be spilled)
+    int lane_t = tid & 63;
+    asm volatile("" : "+v"(lane_t));
+    const int lane = lane_t;
+    int mt, nt, split;
+    {
+      // bands of GM M tiles walk along N (as in k_gemm)
+      const int64_t per_split = (int64_t)tilesM * tilesN;
+      split = (int)(t / per_split);
+      const int64_t r = t - (int64_t)split * per_split;
+      const int GM = max(1, min(p.group_m, tilesM));
+      const int64_t band = r / ((int64_t)GM * tilesN);
+      const int gm = min(GM, tilesM - (int)band * GM);
+      const int64_t idx = r - band * GM * tilesN;
+      mt = (int)band * GM + (int)(idx % gm);
+      nt = (int)(idx / gm);
+    }
+    const int m0 = mt * BM, n0 = nt * BN;
+    const int64_t kb = (int64_t)split * k_split;
+    const int64_t ke = min((int64_t)K, kb + k_split);
+    const int nk = ke > kb ? (int)((ke - kb) / BK) : 0;
+
+    // accumulator element (i, j, e) sits at
+    //   m = mw + 16 i + 4 (lane >> 4) + e,  n = nw + 16 j + (lane & 15)
+    const int mw = m0 + wm * WM, nw = n0 + wn * WN;
+    const int mlane = 4 * (lane >> 4);
+    f32x4 acc[TM][TN];
+    // dW accumulates in place: a full tile starts from the current output
+    // (loaded straight into the accumulator registers before the slab loads,
+    // so the wait for the first slab covers them) and ends with plain stores;
+    // a partial tile starts from zero and adds in its epilogue
+    const bool preload = EPI == EPI_F32_ACCUM && m0 + BM <= M && n0 + BN <= N;
+    if (preload) {
+      const float* src = p.out + (int64_t)split * p.split_stride + (int64_t)(nw + (lane & 15)) * p.ldo +
+                         mw + mlane;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          asm volatile("global_load_dwordx4 %0, %1, off"
+                       : "=a"(acc[i][j])
+                       : "v"(src + (int64_t)16 * j * p.ldo + 16 * i));
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
+    asm volatile("s_nop 4");   // accumulator writes land before the first MFMA reads them
+
+    // Operand panels as buffer resources; each load instruction moves 64
+    // lanes x 16 bytes straight into LDS, the XOR swizzle applied on the
+    // global side; rows past the matrix are clamped to its last row.
+    const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.A + (int64_t)m0 * p.lda), (short)0, 0x7FFFFFFF, 0x00020000);
+    const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.B + (int64_t)n0 * p.ldb), (short)0, 0x7FFFFFFF, 0x00020000);
+    constexpr int RPI = 64 / KCH;                        // rows per load instruction
+    constexpr int A_INS = BM / RPI / C::NWAVES, B_INS = BN / RPI / C::NWAVES;
+    static_assert(A_INS + B_INS == 16, "one slab load per four MFMAs");
+    uint32_t a_voff[A_INS], b_voff[B_INS];
+#pragma unroll
+    for (int q = 0; q < A_INS; ++q) {
+      const int g = wave * A_INS + q, row = g * RPI + lane / KCH;
+      const int c = (lane % KCH) ^ C::swz(row);
+      const int rr = min(m0 + row, M - 1) - m0;
+      a_voff[q] = (uint32_t)(rr * p.lda * 2 + c * 16);
+    }
+#pragma unroll
+    for (int q = 0; q < B_INS; ++q) {
+      const int g = wave * B_INS + q, row = g * RPI + lane / KCH;
+      const int c = (lane % KCH) ^ C::swz(row);
+      const int rr = min(n0 + row, N - 1) - n0;
+      b_voff[q] = (uint32_t)(rr * p.ldb * 2 + c * 16);
+    }
+    if (nk > 0) {
+      // S-stage ring of K slabs as in k_gemm: slab q lives in stage q % S,
+      // slab c + S is loaded into slab c's stage right after the barrier that
+      // ends slab c, and slabs past the tile's K range re-load its last slab.
+      constexpr int NINS = A_INS + B_INS;
+      auto issue_one = [&](int q, int stage, int e) {   // load instruction e of slab q
+        const int qc = min(q, nk - 1);
+        const int soff = (int)((kb + (int64_t)qc * BK) * 2);
+        if (e < A_INS) {
+          uint4* dst = As + stage * BM * KCH + (wave * A_INS + e) * 64;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              a_rsrc, (__attribute__((address_space(3))) void*)dst, 16, a_voff[e], soff, 0, 0);
+        } else {
+          uint4* dst = Bs + stage * BN * KCH + (wave * B_INS + e - A_INS) * 64;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              b_rsrc, (__attribute__((address_space(3))) void*)dst, 16, b_voff[e - A_INS], soff,
+              0, 0);
+        }
+      };
+#pragma unroll
+      for (int q = 0; q < STAGES; ++q)
+#pragma unroll
+        for (int e = 0; e < NINS; ++e) issue_one(q, q, e);
+      wait_vmcnt<NINS * (STAGES - 1)>();
+      __builtin_amdgcn_s_barrier();
+
+      bf16x8 fa[2][TM], fb[2][TN];
+      const int arow = wm * WM + (lane & 15), brow = wn * WN + (lane & 15);
+      // fragment r of 32-deep sub-step ks of stage st: B block r for r < TN,
+      // else A block r - TN
+      auto rd = [&](bf16x8 (&da)[TM], bf16x8 (&db)[TN], int st, int ks, int r) {
+        const int ch = ks * 4 + (lane >> 4);
+        if (r < TN) {
+          const int row = brow + 16 * r;
+          db[r] = __builtin_bit_cast(bf16x8, Bs[st * BN * KCH + row * KCH + (ch ^ C::swz(row))]);
+        } else {
+          const int row = arow + 16 * (r - TN);
+          da[r - TN] =
+              __builtin_bit_cast(bf16x8, As[st * BM * KCH + row * KCH + (ch ^ C::swz(row))]);
+        }
+      };
+      // one sub-step on fragment set h: its 64 MFMAs, the reads of sub-step
+      // (nst, nks) into set 1 - h and, with `loads`, slab lq into stage lst
+      auto step = [&](int h, int nst, int nks, bool loads, int lq, int lst) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int m = i * TN + j;
+            BGPO_MFMA16(acc[i][j], fa[h][i], fb[h][j]);
+            if (loads && (m & 3) == 1) issue_one(lq, lst, m >> 2);
+            if ((m & 3) == 3) rd(fa[1 - h], fb[1 - h], nst, nks, m >> 2);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+      };
+#pragma unroll
+      for (int r = 0; r < TM + TN; ++r) rd(fa[0], fb[0], 0, 0, r);
+      // every slab, the last one included, runs the same code (the last
+      // one's reads and loads fetch data nobody uses), so the accumulators
+      // stay in their registers across the whole loop
+      for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt % STAGES;
+        step(0, cur, 1, false, 0, 0);
+        // slab kt + 1 landed (own loads) and, after the barrier, every wave is
+        // done with stage `cur`: refill it with slab kt + S during the second
+        // sub-step, which also reads slab kt + 1's first fragments
+        wait_vmcnt<NINS * (STAGES - 2)>();
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        step(1, (kt + 1) % STAGES, 0, true, kt + STAGES, cur);
+      }
+      // drain the ring (outstanding re-loads) before the epilogue may reuse LDS
+      __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_s_barrier();
+    }
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");   // the last MFMAs' results land
+
+    // ---------------- epilogues ----------------
+    if constexpr (EPI == EPI_FWD || EPI == EPI_FWDU) {
+      // Per (row, 128-entry vocabulary slice of this wave): max m and sum of
+      // 2^(z log2e - m), in log2 units, written to the partials (the slice of
+      // wave row wm is partial index mw / 128).  A row's 128 entries sit in
+      // its lane and the lanes l ^ 16, l ^ 32, l ^ 48.  EPI_FWDU also keeps
+      // the exponentials u = 2^(z log2e - m) as fp16 in dZ[row][v]; the
+      // softmax-gradient kernel turns them into s (p - onehot) with
+      // p = u 2^(m - lse).  Both variants sum in the same order, so l is
+      // bit-identical between them.
+      static_assert(WM == kVocabTile, "one partial per wave slice");
+      constexpr bool kStore = EPI == EPI_FWDU;
+      if (mw + WM > M) {
+        // the wave slice crosses the end of the vocabulary: entries past it
+        // become -inf, i.e. exponentials 0 (wave-uniform branch)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (mw + 16 * i + mlane + e >= M) acc[i][j][e] = -INFINITY;
+      }
+      // EPI_FWDU stages the tile's exponentials in LDS (free once the ring is
+      // drained; 256 rows x 256 vocabulary ids x fp16 = the ring's 128 KB) as
+      // [row][vocabulary], 16-byte chunk c of row r at chunk c ^ (r mod 32),
+      // and then writes whole rows (two 512-byte rows per instruction).
+      char* stage_u = reinterpret_cast<char*>(smem);
+      static_assert(!kStore || (BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2),
+                    "staging tile: 512-byte rows that fit the ring");
+      // one 16-row column block of the wave tile at a time, so that only its
+      // 32 values per lane are live outside the accumulators
+      const int vt = mw / WM;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) mx = fmaxf(mx, acc[i][j][e]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mref = mx > -INFINITY ? mx * kLog2e : 0.f;   // a slice past V has no entries
+        float ssum = 0.f;
+        const int nl = nw - n0 + 16 * j + (lane & 15);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          float u[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            u[e] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mref));
+            ssum += u[e];
+          }
+          if constexpr (kStore) {
+            // vocabulary ids ml .. ml + 3 of row nl into the staging tile
+            const int ml = mw - m0 + 16 * i + mlane;
+            *reinterpret_cast<uint2*>(stage_u + nl * 512 + (((ml >> 3) ^ (nl & 31)) << 4) +
+                                      (ml & 7) * 2) =
+                make_uint2(pack_f16x2(u[0], u[1]), pack_f16x2(u[2], u[3]));
+          }
+        }
+        float st = ssum + __shfl_xor(ssum, 16, 64);
+        st += __shfl_xor(st, 32, 64);
+        const int n = n0 + nl;
+        if (lane < 16 && mw < M && n < n_valid) {
+          p.part_m[(int64_t)vt * p.ldp + n] = mref;
+          p.part_s[(int64_t)vt * p.ldp + n] = st;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (kStore) {
+        __syncthreads();
+        // lane l of a store instruction: row 2 q + l / 32 of the wave's rows,
+        // stored chunk l mod 32, i.e. logical chunk (l mod 32) ^ (row mod 32)
+        constexpr int ROWS_PER_WAVE = BN / (NT / 64);
+        // (the lane's chunk is re-derived here every tile: hoisted out of the
+        // tile loop, its per-row variants would be spilled)
+        int pc = lane & 31;
+        asm volatile("" : "+v"(pc));
+#pragma unroll
+        for (int q = 0; q < ROWS_PER_WAVE / 2; ++q) {
+          const int row = wave * ROWS_PER_WAVE + 2 * q + (lane >> 5);
+          const int m = m0 + 8 * (pc ^ (row & 31));
+          const uint4 v = *reinterpret_cast<const uint4*>(stage_u + row * 512 + pc * 16);
+          if (n0 + row < N && m < M)
+            *reinterpret_cast<uint4*>(p.dZ + (int64_t)(n0 + row) * p.ldz + m) = v;
+        }
+      }
+    } else {
+      // fp32 store of the tile, transposed (dX partials, or a full dW tile
+      // that started from its previous value), or read-modify-write of a
+      // partial dW tile
+      float* outb = p.out + (int64_t)split * p.split_stride;
+      if (m0 + BM <= M && n0 + BN <= N) epi_f32_16t<false, true, TM, TN>(acc, outb, p.ldo, mw, nw, lane, M, N);
+      else epi_f32_16t<EPI == EPI_F32_ACCUM, false, TM, TN>(acc, outb, p.ldo, mw, nw, lane, M, N);
+    }
+    __syncthreads();
+  }
+#endif
+}
+
+// Tile configuration of the production kernels (k_gemm4w): 256x256 block
+// tile, K slab 64 in a 2-stage LDS ring, four waves of 128x128, 256-byte LDS
+// swizzle.  The eight-wave k_gemm configuration they replaced is test hook
+// variant 8.
+#define BGPO_TILE4 256, 256, 64, 2, 1
+constexpr int kGemmThreads4 = 256;
 // band heights of the tile walk (see the tile-order comment in k_gemm),
 // measured at the LLaDA head shape: dW and dX fastest with bands of 8, the
 // forward GEMM insensitive between 1 and 8
@@ -523,34 +875,35 @@ hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool sto
   p.group_m = kGroupMFwd;
   if (store_u) {
     p.dZ = ws.dZ; p.ldz = V;
-    k_gemm<EPI_FWDU, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+    k_gemm4w<EPI_FWDU, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   } else {
-    k_gemm<EPI_FWD, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+    k_gemm4w<EPI_FWD, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s) {
+  // dX^T[c][row] = W[c][:] . dZ[row][:], stored transposed: dx_part[row][c]
   GemmParams p = base_params();
-  p.A = ws.dZ; p.lda = V;
-  p.B = W; p.ldb = V;
-  p.N = d; p.K = V; p.dyn_m = 1; p.meta = ws.unit();
+  p.A = W; p.lda = V;
+  p.B = ws.dZ; p.ldb = V;
+  p.M = d; p.K = V; p.dyn_n = 1; p.meta = ws.unit();
   p.dyn_split = 1;
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
-  k_gemm<EPI_F32_STORE, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s) {
   GemmParams p = base_params();
-  p.A = ws.HcT; p.lda = ws.KT;
-  p.B = ws.dZT; p.ldb = ws.KT;
-  p.M = d; p.N = V; p.dyn_k = 1; p.meta = ws.unit();
+  p.A = ws.dZT; p.lda = ws.KT;
+  p.B = ws.HcT; p.ldb = ws.KT;
+  p.M = V; p.N = d; p.dyn_k = 1; p.meta = ws.unit();
   p.group_m = kGroupMdW;
   p.out = dW; p.ldo = V;
-  k_gemm<EPI_F32_ACCUM, BGPO_TILE><<<grid, kGemmThreads, 0, s>>>(p);
+  k_gemm4w<EPI_F32_ACCUM, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -569,13 +922,14 @@ extern "C" int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C,
                                  int32_t K, void* stream) {
   using namespace bgpo;
   if (!A || !B || !C || M <= 0 || N <= 0 || K <= 0 || K % 64) return -1;
+  // the production kernel stores C^T of its operands' product: swap them
   GemmParams p = base_params();
-  p.A = A; p.lda = K; p.B = B; p.ldb = K;
-  p.M = M; p.N = N; p.K = K; p.k_split = K;
+  p.A = B; p.lda = K; p.B = A; p.ldb = K;
+  p.M = N; p.N = M; p.K = K; p.k_split = K;
   p.out = C; p.ldo = N;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -3;
-  k_gemm<EPI_F32_STORE, BGPO_TILE><<<gemm_grid(dev), kGemmThreads, 0, (hipStream_t)stream>>>(p);
+  k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
@@ -621,6 +975,14 @@ extern "C" int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, floa
     case 15: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 128, 5, 1, 1><<<cus, 256, 0, s>>>(p); break;
     case 16: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 4, 1, 1><<<cus, 512, 0, s>>>(p); break;
     case 17: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 5, 1, 1><<<cus, 512, 0, s>>>(p); break;
+    case 18: {   // the production kernel: it stores C^T of its operands' product
+      GemmParams q = p;
+      q.A = B; q.B = A; q.M = N; q.N = M;
+      if (!(flags & 1) && !((flags >> 8) & 0xFF)) q.group_m = 1;
+      else if (flags & 1) q.group_m = N;
+      k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<cus, kGemmThreads4, 0, s>>>(q);
+      break;
+    }
     default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -3;

@@ -20,6 +20,8 @@ constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
 // with 32-bit byte offsets below 2^31, so a bf16 operand's leading dimension
 // must stay at or below this.
 constexpr int64_t kMaxPanelLd = (int64_t(1) << 22) - 1;
+// Padding of the H_c^T / dZ^T leading dimension beyond the row capacity.
+constexpr int64_t kPanelPad = 64;
 
 // Device-resident bookkeeping written by the mask kernel, one record per
 // sample.  Samples are processed in units of up to G consecutive samples whose
