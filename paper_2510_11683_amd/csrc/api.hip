@@ -30,20 +30,22 @@ namespace bgpo {
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 constexpr int64_t kMaxUnit = 8;
+constexpr int64_t kDwUnits = 2;   // units per dW GEMM in the constant-memory mode
 
 size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
                         Workspace* units) {
   const int64_t P = (int64_t)dm.B * dm.L;
   const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
   const int64_t nvt = (dm.V + kVocabTile - 1) / kVocabTile;
-  // samples per unit: up to kMaxUnit while the unit's dZ, dZ^T, H_c and H_c^T
-  // stay within about 20 GB and its 64-row chunks within one grid dimension
-  // of the row kernels.  With every sample retained, the same units (at most
-  // n_t samples each) each keep their own state and all of them form the one
-  // dW batch, so both modes run the same unit compositions.
-  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2 * 2;
+  // samples per unit: up to kMaxUnit while the unit's dZ and H_c and the
+  // dZ^T and H_c^T columns of a dW batch of kDwUnits units stay within about
+  // 32 GB, and the unit's 64-row chunks within one grid dimension of the row
+  // kernels.  With every sample retained, the same units (at most n_t samples
+  // each) each keep their own state and all of them form the one dW batch, so
+  // both modes run the same unit compositions.
+  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2 * (1 + kDwUnits);
   int64_t G = std::max<int64_t>(
-      1, std::min({kMaxUnit, (int64_t(20) << 30) / per_sample, int64_t(65535) * 64 / NP}));
+      1, std::min({kMaxUnit, (int64_t(32) << 30) / per_sample, int64_t(65535) * 64 / NP}));
   if (retain) G = std::min<int64_t>(G, dm.n_t);
   const int64_t n_units = retain ? (dm.n_t + G - 1) / G : 1;
   const int64_t RP = G * NP;
@@ -51,7 +53,12 @@ size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
   // kernel picks each unit's count), within about 4 GB
   const int64_t per_split = RP * dm.d * 4;
   const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t(4) << 30) / per_split));
-  const int64_t dw_batch = n_units;
+  // constant mode: the units of a dW batch keep their dZ^T / H_c^T columns
+  // side by side (the row-major dZ and H_c are per unit), so the fp32 dW is
+  // read and written once per batch; one unit per batch where two would
+  // exceed the panel range
+  const int64_t dw_batch =
+      retain ? n_units : (kDwUnits * RP + kPanelPad <= kMaxPanelLd ? kDwUnits : 1);
   // leading dimension of H_c^T and dZ^T: the dW GEMM reads 256-row panels of
   // both, and with a power-of-two row pitch (32768 rows of bf16 = 64 KB at
   // the benchmark shape) their rows crowd into the same memory channels;
@@ -464,18 +471,28 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
     dbar = ws.dbar;
   }
   const int j_end = prob->j_begin + prob->j_count;
+  int in_batch = 0;        // units already in the current dW batch
+  int prev_used = 0;       // samples of the previous unit (its record is meta[prev_used - 1])
   for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.G) {
     const int n_s = std::min<int>(j_end - j0, (int)ws.G);
+    // a unit after the first of its batch puts its dZ^T / H_c^T columns after
+    // the previous unit's (whose last record the first mask launch reads
+    // before any record is rewritten)
+    const SampleMeta* prev = in_batch ? ws.meta + (prev_used - 1) : nullptr;
     st = run_forward_unit(prob, ws, tm, grid, j0, n_s, act, targets, resp_mask, adv, ell_old,
                           loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, true,
-                          nullptr, dbar, s);
+                          prev, dbar, s);
     if (st != BGPO_OK) return st;
     st = unit_backward(ws, act, j0, prob->j_begin, W_head, dX, dgamma, dm, grid, tm, s);
     if (st != BGPO_OK) return st;
-    // one dW GEMM for the unit: K runs over its rows
-    BGPO_TRY(tm.begin(BGPO_K_DW));
-    BGPO_TRY(launch_gemm_dw(ws, dW, dm.d, dm.V, grid, s));
-    BGPO_TRY(tm.end());
+    prev_used = n_s;
+    // one dW GEMM per batch of units: K runs over all their rows
+    if (++in_batch == (int)ws.dw_batch || j0 + n_s >= j_end) {
+      BGPO_TRY(tm.begin(BGPO_K_DW));
+      BGPO_TRY(launch_gemm_dw(ws, dW, dm.d, dm.V, grid, s));
+      BGPO_TRY(tm.end());
+      in_batch = 0;
+    }
   }
   BGPO_TRY(tm.finish());
   return BGPO_OK;

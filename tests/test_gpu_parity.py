@@ -294,9 +294,10 @@ def test_linearity_and_determinism():
 def test_timing_record_counts_kernel_launches():
     """The optional timing record adds, per kernel class, the elapsed time and
     the number of kernel launches: 10 samples in units of 8 give 2 units; per
-    unit one forward, softmax-gradient, dX and dW GEMM launch, one gather, the
+    unit one forward, softmax-gradient and dX GEMM launch, one gather, the
     three row reductions (target logit, log-sum-exp, per-response terms), and
-    one mask and one dX reduction per sample; the W transpose once per call."""
+    one mask and one dX reduction per sample; one dW GEMM for the batch of
+    both units; the W transpose once per call."""
     w = workloads.TINY.replace(n_t=10)
     r = Runner(w, workloads.generate(w))
     t = lib().Timing()
@@ -304,7 +305,7 @@ def test_timing_record_counts_kernel_launches():
     torch.cuda.synchronize()
     got = {k: n for k, (ms, n) in t.as_dict().items()}
     assert got == {"transpose_w": 1, "mask": 10, "gather": 2, "fwd": 2, "ell": 6,
-                   "softmax_grad": 2, "dx": 2, "dx_reduce": 10, "dw": 2}
+                   "softmax_grad": 2, "dx": 2, "dx_reduce": 10, "dw": 1}
     assert all(ms > 0 for ms, n in t.as_dict().values())
     r.fwd(timing=t)                                     # forward only: no gradient classes
     got2 = {k: n for k, (ms, n) in t.as_dict().items()}
