@@ -39,6 +39,8 @@ int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
  *         16: as 9 with the 256-byte swizzle; 17: as 10 with that swizzle
  *         18: four waves of 128x128 on 16x16x32 MFMAs, K slab 64 in 2 stages,
  *             256-byte swizzle (the production kernel, as bgpo_test_gemm_nt)
+ *         19: as 18 on a 4-stage ring of 32-deep slabs (same LDS, one barrier
+ *             per 32-deep MFMA sub-step instead of per two)
  * flags bit 0: M tiles consecutive in the tile walk (else N tiles);
  *       bit 1: plain workgroup order (no XCD grouping);
  *       bits 8-15: if nonzero, band height (M tiles) of the tile walk;

@@ -557,7 +557,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   using C = Cfg<BM, BN, BK, WM, WN, SWZ>;
   constexpr int NT = C::NT, KCH = C::KCH;
   constexpr int TM = WM / 16, TN = WN / 16;
-  static_assert(C::NWAVES == 4 && BK == 64, "four waves, 64-deep slabs (two sub-steps)");
+  // 64-deep slabs hold two 32-deep MFMA sub-steps between barriers; 32-deep
+  // slabs one, so a ring of the same LDS size has twice the stages
+  static_assert(C::NWAVES == 4 && (BK == 64 || BK == 32), "four waves, 32- or 64-deep slabs");
   __shared__ uint4 smem[STAGES * (BM + BN) * KCH];
   uint4* As = smem;                           // [STAGES][BM][KCH]
   uint4* Bs = smem + STAGES * BM * KCH;       // [STAGES][BN][KCH]
@@ -574,7 +576,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   int64_t k_split = p.k_split;
   if (p.dyn_split) {
     n_split = p.meta->dx_split;
-    k_split = (int64_t)p.meta->dx_kslab * BK;
+    k_split = (int64_t)p.meta->dx_kslab * 64;   // 64-wide slabs: nk even for BK 32
   }
   if (EPI == EPI_F32_ACCUM && K == 0) return;   // nothing to add
   const int tilesM = (M + BM - 1) / BM, tilesN = (N + BN - 1) / BN;
@@ -647,7 +649,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         (void*)(p.B + (int64_t)n0 * p.ldb), (short)0, 0x7FFFFFFF, 0x00020000);
     constexpr int RPI = 64 / KCH;                        // rows per load instruction
     constexpr int A_INS = BM / RPI / C::NWAVES, B_INS = BN / RPI / C::NWAVES;
-    static_assert(A_INS + B_INS == 16, "one slab load per four MFMAs");
+    static_assert(A_INS + B_INS == BK / 4, "one slab load per 256 / BK MFMAs");
     uint32_t a_voff[A_INS], b_voff[B_INS];
 #pragma unroll
     for (int q = 0; q < A_INS; ++q) {
@@ -706,6 +708,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       };
       // one sub-step on fragment set h: its 64 MFMAs, the reads of sub-step
       // (nst, nks) into set 1 - h and, with `loads`, slab lq into stage lst
+      constexpr int LEVERY = TM * TN / NINS;   // MFMAs per slab load
       auto step = [&](int h, int nst, int nks, bool loads, int lq, int lst) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -713,7 +716,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
           for (int j = 0; j < TN; ++j) {
             const int m = i * TN + j;
             BGPO_MFMA16(acc[i][j], fa[h][i], fb[h][j]);
-            if (loads && (m & 3) == 1) issue_one(lq, lst, m >> 2);
+            if (loads && m % LEVERY == 1) issue_one(lq, lst, m / LEVERY);
             if ((m & 3) == 3) rd(fa[1 - h], fb[1 - h], nst, nks, m >> 2);
             __builtin_amdgcn_sched_barrier(0);
           }
@@ -723,17 +726,36 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // every slab, the last one included, runs the same code (the last
       // one's reads and loads fetch data nobody uses), so the accumulators
       // stay in their registers across the whole loop
-      for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt % STAGES;
-        step(0, cur, 1, false, 0, 0);
-        // slab kt + 1 landed (own loads) and, after the barrier, every wave is
-        // done with stage `cur`: refill it with slab kt + S during the second
-        // sub-step, which also reads slab kt + 1's first fragments
-        wait_vmcnt<NINS * (STAGES - 2)>();
-        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-        __builtin_amdgcn_s_barrier();
-        __builtin_amdgcn_sched_barrier(0);
-        step(1, (kt + 1) % STAGES, 0, true, kt + STAGES, cur);
+      if constexpr (BK == 64) {
+        for (int kt = 0; kt < nk; ++kt) {
+          const int cur = kt % STAGES;
+          step(0, cur, 1, false, 0, 0);
+          // slab kt + 1 landed (own loads) and, after the barrier, every wave
+          // is done with stage `cur`: refill it with slab kt + S during the
+          // second sub-step, which also reads slab kt + 1's first fragments
+          wait_vmcnt<NINS * (STAGES - 2)>();
+          __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+          __builtin_amdgcn_s_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+          step(1, (kt + 1) % STAGES, 0, true, kt + STAGES, cur);
+        }
+      } else {
+        // one sub-step per slab; K ranges are multiples of 64, so nk is even
+        // and the fragment sets alternate in a fixed order.  Before slab s:
+        // slab s + 1 landed, every wave is done reading stage s % S (its
+        // fragments were read during slab s - 1), so slab s + S refills it
+        // and has S - 1 sub-steps to land
+        auto sub = [&](int h, int s) {
+          wait_vmcnt<NINS * (STAGES - 2)>();
+          __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+          __builtin_amdgcn_s_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+          step(h, (s + 1) % STAGES, 0, true, s + STAGES, s % STAGES);
+        };
+        for (int kt = 0; kt < nk; kt += 2) {
+          sub(0, kt);
+          sub(1, kt + 1);
+        }
       }
       // drain the ring (outstanding re-loads) before the epilogue may reuse LDS
       __builtin_amdgcn_s_waitcnt(0);
@@ -975,12 +997,16 @@ extern "C" int bgpo_test_gemm_variant(const uint16_t* A, const uint16_t* B, floa
     case 15: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 128, 5, 1, 1><<<cus, 256, 0, s>>>(p); break;
     case 16: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 4, 1, 1><<<cus, 512, 0, s>>>(p); break;
     case 17: k_gemm<EPI_F32_STORE, 256, 256, 32, 128, 64, 5, 1, 1><<<cus, 512, 0, s>>>(p); break;
-    case 18: {   // the production kernel: it stores C^T of its operands' product
+    case 18:     // the production kernel: it stores C^T of its operands' product
+    case 19: {   // the same on a four-stage ring of 32-deep slabs
       GemmParams q = p;
       q.A = B; q.B = A; q.M = N; q.N = M;
       if (!(flags & 1) && !((flags >> 8) & 0xFF)) q.group_m = 1;
       else if (flags & 1) q.group_m = N;
-      k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<cus, kGemmThreads4, 0, s>>>(q);
+      if (variant == 18)
+        k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<cus, kGemmThreads4, 0, s>>>(q);
+      else
+        k_gemm4w<EPI_F32_STORE, 256, 256, 32, 4, 1><<<cus, kGemmThreads4, 0, s>>>(q);
       break;
     }
     default: return -1;

@@ -39,12 +39,13 @@ def _gpu():
 
 # ---------------------------------------------------------------- GEMM core
 
-@pytest.mark.parametrize("core", ["eight_wave_32x32", "four_wave_16x16"])
+@pytest.mark.parametrize("core", ["eight_wave_32x32", "four_wave_16x16", "four_wave_16x16_ring4x32"])
 @pytest.mark.parametrize("M,N,K", [(300, 200, 192), (512, 768, 1024), (257, 1000, 64)])
 def test_gemm_core_matches_fp32_reference(M, N, K, core):
-    """Both GEMM cores (the production four-wave 16x16x32 one through
-    bgpo_test_gemm_nt, the earlier eight-wave 32x32x16 one as variant 8)
-    against exact products."""
+    """The GEMM cores (the production four-wave 16x16x32 one through
+    bgpo_test_gemm_nt, the same on a four-stage ring of 32-deep slabs as
+    variant 19, the earlier eight-wave 32x32x16 one as variant 8) against
+    exact products."""
     g = torch.Generator().manual_seed(M * 7 + N)
     A = torch.randn(M, K, generator=g).to(torch.bfloat16)
     Bm = torch.randn(N, K, generator=g).to(torch.bfloat16)
@@ -53,7 +54,7 @@ def test_gemm_core_matches_fp32_reference(M, N, K, core):
     if core == "four_wave_16x16":
         lib().bgpo_test_gemm_nt(A.cuda(), Bm.cuda(), C)
     else:
-        lib().bgpo_test_gemm_variant(A.cuda(), Bm.cuda(), C, 8)
+        lib().bgpo_test_gemm_variant(A.cuda(), Bm.cuda(), C, 8 if core == "eight_wave_32x32" else 19)
     torch.cuda.synchronize()
     err = (C.cpu().double() - ref).abs().max().item()
     assert err <= 1e-5 * (K ** 0.5) * ref.abs().max().item() + 1e-5, err
