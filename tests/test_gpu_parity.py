@@ -60,6 +60,25 @@ def test_gemm_core_matches_fp32_reference(M, N, K, core):
     assert err <= 1e-5 * (K ** 0.5) * ref.abs().max().item() + 1e-5, err
 
 
+@pytest.mark.parametrize("variant", [8, 18, 19])
+@pytest.mark.parametrize("M,N,K,n_split", [(300, 200, 640, 4), (257, 520, 192, 3), (64, 64, 64, 4)])
+def test_gemm_core_split_k(M, N, K, n_split, variant):
+    """Split-K through the variant hook: slices of a multiple of 64 (the
+    32-deep ring of variant 19 relies on an even slab count per slice), empty
+    trailing slices included (K = 64 in 4 slices); the slices sum to the
+    exact product."""
+    g = torch.Generator().manual_seed(M + 3 * N + K)
+    A = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    Bm = torch.randn(N, K, generator=g).to(torch.bfloat16)
+    ref = A.double() @ Bm.double().T
+    C = torch.full((n_split * M * N,), float("nan"), dtype=torch.float32, device="cuda")
+    lib().bgpo_test_gemm_variant(A.cuda(), Bm.cuda(), C, variant, n_split << 16)
+    torch.cuda.synchronize()
+    got = C.cpu().double().view(n_split, M, N).sum(0)
+    err = (got - ref).abs().max().item()
+    assert err <= 1e-5 * (K ** 0.5) * ref.abs().max().item() + 1e-5, err
+
+
 # ---------------------------------------------------------------- masks
 
 @pytest.mark.parametrize("w", workloads.CONFIGS + (MID,), ids=lambda w: w.name)
