@@ -345,3 +345,30 @@ def test_zero_std_edge_cases():
     W = np.zeros((2, 4))
     ell, rows, lsm = elbo.ell_of_mask(H, W, np.zeros(3, int), np.zeros(3, bool), 0.5)
     assert ell == 0.0 and rows.size == 0
+
+
+# ---------------------------------------------------------------- bf16 widening
+
+def check_bf16_widening(fn=None):
+    """Every one of the 65536 bfloat16 bit patterns widened to float64 equals
+    torch's own bfloat16 -> float64 conversion (NaN patterns give NaN, the
+    two zeros keep their signs), and known values sit at their patterns."""
+    fn = fn or elbo.bf16_to_f64
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    with np.errstate(invalid="ignore"):       # signalling-NaN patterns
+        got = np.asarray(fn(bits), dtype=np.float64)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    assert got.shape == ref.shape
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+    # 1.0 = 0x3F80, -2.0 = 0xC000, the smallest subnormal 2^-133 = 0x0001
+    assert fn(np.array([0x3F80, 0xC000, 0x0001], dtype=np.uint16)).tolist() == [1.0, -2.0, 2.0 ** -133]
+    # a 2-D array keeps its shape
+    with np.errstate(invalid="ignore"):
+        assert np.asarray(fn(bits.reshape(256, 256))).shape == (256, 256)
+
+
+def test_bf16_widening_matches_torch_on_every_pattern():
+    check_bf16_widening()

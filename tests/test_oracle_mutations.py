@@ -22,6 +22,7 @@ ALL_PINS = [
     pins.check_on_policy_equivalence,
     pins.check_bound_equality_cases,
     pins.check_linearity,
+    pins.check_bf16_widening,
 ]
 
 
@@ -50,6 +51,18 @@ def mut_no_max_shift(z):
 
 def mut_no_normaliser(z):
     return z - z.max(axis=1, keepdims=True)
+
+
+def mut_bf16_shift_before_widening(bits):
+    # the shift done in 16 bits drops every bit of the pattern
+    u = (np.asarray(bits, dtype=np.uint16) << np.uint16(16)).astype(np.uint32)
+    return u.view(np.float32).astype(np.float64)
+
+
+def mut_bf16_low_half(bits):
+    # the pattern placed in the low half of the float32 word
+    u = np.asarray(bits, dtype=np.uint16).astype(np.uint32)
+    return u.view(np.float32).astype(np.float64)
 
 
 def mut_swap_branches(d, A, n_t, *rest):
@@ -116,6 +129,8 @@ MUTATIONS = [
     ("backprop_rows", mut_backprop_wrong_target),
     ("backprop_rows", mut_backprop_rows_reversed),
     ("backprop_rows", mut_dx_without_transpose),
+    ("bf16_to_f64", mut_bf16_shift_before_widening),
+    ("bf16_to_f64", mut_bf16_low_half),
 ]
 
 
