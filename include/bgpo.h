@@ -41,8 +41,9 @@
  *     wait for its own timing events before returning.
  *   - The library never allocates device memory; scratch space is the
  *     caller's `workspace` of at least bgpo_workspace_size() bytes (256-byte
- *     aligned).  Its size depends on B, L, d and V, never on n_t (except in
- *     the retain_samples contrast mode below).
+ *     aligned).  Its size depends on B, L, d, V, the input type and the
+ *     workspace budget, never on n_t (except in the retain_samples contrast
+ *     mode below).
  *   - Without a timing record a call only enqueues kernels (no allocation,
  *     memory set or copy, no synchronisation), so it can be captured into a
  *     HIP graph and replayed; the graph then reads and writes the buffers
@@ -51,7 +52,11 @@
  *     enqueued; HIP launch errors return BGPO_ERR_HIP.  No C++ exception
  *     crosses the ABI.  Entry points keep no mutable global state; calls on
  *     different streams must not share a workspace.
- *   - hidden and W_head are bfloat16 bit patterns (uint16), row-major.
+ *   - hidden (or x) and W_head are row-major; their element type is
+ *     prob->in_dtype: bfloat16 bit patterns (uint16, BGPO_BF16) or float32
+ *     (BGPO_F32), which the device rounds to bfloat16 (round to nearest
+ *     even) on first read, so an fp32 call gives the same bits as a bf16 call
+ *     on the host-rounded inputs.
  *   - The head input of sample j may be its own tensor (sample_stride > 0):
  *     the mask predictor's output depends on the noised sequence y_t of each
  *     sample (p_theta(y | y_t, x), Eq. per_step_loss), and the dX of sample j
@@ -77,8 +82,12 @@ typedef enum bgpo_status {
   BGPO_ERR_INVALID_ARG = -1,   /* NULL pointer, negative size, bad enum, range outside [0, n_t) */
   BGPO_ERR_WORKSPACE = -2,     /* workspace NULL, misaligned or smaller than bgpo_workspace_size() */
   BGPO_ERR_HIP = -3,           /* a HIP call failed (launch, event) */
-  BGPO_ERR_UNSUPPORTED = -4    /* shape outside the supported set above */
+  BGPO_ERR_UNSUPPORTED = -4,   /* shape outside the supported set above */
+  BGPO_ERR_BUDGET = -5         /* no workspace layout fits prob->ws_budget */
 } bgpo_status;
+
+/* Element types of the head inputs (bgpo_problem.in_dtype). */
+enum { BGPO_BF16 = 0, BGPO_F32 = 1 };
 
 /* Timestep modes. */
 enum { BGPO_T_IID = 0, BGPO_T_STRATIFIED = 1 };
@@ -112,7 +121,8 @@ enum { BGPO_T_IID = 0, BGPO_T_STRATIFIED = 1 };
  * BGPO_ERR_INVALID_ARG.  The retained rows (n_t rounded up to whole units of
  * samples, times B*L rounded up to 256 per sample) must stay below 2^22;
  * larger retained problems return BGPO_ERR_UNSUPPORTED from every entry
- * point, bgpo_workspace_size included. */
+ * point, bgpo_workspace_size included.  retain_samples = 1 takes the stored
+ * mode only: vocab_chunk and ws_budget must be 0 (else BGPO_ERR_INVALID_ARG). */
 enum { BGPO_BOUND_PAPER = 0, BGPO_BOUND_TAYLOR = 1, BGPO_BOUND_JENSEN = 2, BGPO_BOUND_EXACT = 3 };
 
 /* Bits of *status_flags (device int32, OR-ed in, never cleared by the library). */
@@ -139,7 +149,40 @@ typedef struct bgpo_problem {
   int32_t retain_samples;/* 0, or 1 with bound = BGPO_BOUND_EXACT: keep the state of
                            every sample instead of running the forward twice (see
                            below); the workspace then grows with n_t */
+  int32_t in_dtype;     /* BGPO_BF16 or BGPO_F32: element type of hidden / x and W_head */
+  int32_t vocab_chunk;  /* 0 = backward chosen by ws_budget (below); > 0 = the
+                           recompute backward with vocabulary chunks of this many
+                           entries (a multiple of 256) */
+  uint64_t ws_budget;   /* bytes the workspace may take; 0 = no limit (see below) */
 } bgpo_problem;
+
+/* Backward modes and the workspace budget.  Both keep device memory constant
+ * in n_t; they trade memory for work:
+ *   stored exponentials   the forward GEMM of a unit of samples keeps the
+ *                         exponentials of its logits (fp16, rows x V), the
+ *                         gradient dZ = s (softmax - onehot) is formed from
+ *                         them, and the dX and dW GEMMs read all of it: three
+ *                         GEMM passes per sample, a workspace of about
+ *                         rows x V x 6 bytes per unit (31 GB at B=8, L=512,
+ *                         d=4096, V=126464 with units of 8 samples)
+ *   recompute             the forward keeps only the per-row log-sum-exp; the
+ *                         backward walks the vocabulary in chunks of C
+ *                         entries, recomputing that chunk's logits, writing
+ *                         its dZ (rows x C, two layouts) and accumulating dX
+ *                         and dW before the next chunk: four GEMM passes per
+ *                         sample, nothing of size rows x V is ever stored
+ * ws_budget = 0 and vocab_chunk = 0 give the stored mode with units of up to
+ * 8 samples within about 32 GB.  A nonzero ws_budget picks the largest
+ * stored-mode unit (and dW batch, dX split capacity) whose workspace fits;
+ * if none does, the recompute mode with the unit and chunk width of least
+ * estimated extra traffic that fits; if nothing fits, BGPO_ERR_BUDGET.
+ * vocab_chunk > 0 forces the recompute mode with that chunk (units sized by
+ * ws_budget, or within 32 GB when it is 0).  The smallest layout is the
+ * recompute mode with units of one sample and chunks of 256 entries: about
+ * 2 d V + B L (8 d + V / 16) bytes (the first term is the transposed head,
+ * re-staged every call; with BGPO_F32 inputs a bf16 copy of W_head adds
+ * another 2 d V).  bgpo_workspace_size reports the size of the chosen layout
+ * (at most ws_budget). */
 
 /* Kernel classes reported by the optional timing record. */
 enum {
@@ -153,7 +196,8 @@ enum {
   BGPO_K_DX = 6,           /* dZ W^T split over the vocabulary */
   BGPO_K_DX_REDUCE = 7,    /* split reduction + scatter-add into dX (+ RMSNorm backward) */
   BGPO_K_DW = 8,           /* H_c^T dZ accumulated into dW */
-  BGPO_K_COUNT = 9
+  BGPO_K_RECOMPUTE = 9,    /* recompute mode: a vocabulary chunk's logits -> its dZ (both layouts) */
+  BGPO_K_COUNT = 10
 };
 
 /* Optional per-kernel timing (host memory).  When passed to an entry point,
@@ -171,9 +215,26 @@ int bgpo_version(void);
 const char* bgpo_status_string(int status);
 
 /* Bytes of device workspace needed by bgpo_elbo_fwd and
- * bgpo_elbo_bwd_accumulate for `prob` (depends on B, L, d, V only).
- * Writes *bytes and returns BGPO_OK, or a negative status. Host only. */
+ * bgpo_elbo_bwd_accumulate for `prob` (depends on B, L, d, V, in_dtype,
+ * vocab_chunk and ws_budget; never on n_t outside the retain_samples mode).
+ * Writes *bytes and returns BGPO_OK, or a negative status (BGPO_ERR_BUDGET if
+ * no layout fits ws_budget). Host only. */
 int bgpo_workspace_size(const bgpo_problem* prob, size_t* bytes);
+
+/* The layout bgpo_workspace_size measures for `prob` (see the backward
+ * modes above): samples per unit, units per dW GEMM (stored mode), capacity of
+ * the dX split partials, vocabulary chunk width (0 = stored exponentials) and
+ * the workspace bytes.  Returns BGPO_OK or the status of bgpo_workspace_size.
+ * Host only. */
+typedef struct bgpo_plan_info {
+  int32_t samples_per_unit;
+  int32_t dw_batch;
+  int32_t dx_splits;
+  int32_t vocab_chunk;
+  uint64_t workspace_bytes;
+} bgpo_plan_info;
+
+int bgpo_workspace_plan(const bgpo_problem* prob, bgpo_plan_info* info);
 
 /* Timestep and mask of every response for ONE sample j (the forward masking
  * process of Section 2.1 and the t draw of Algorithm 1), compacted.
@@ -188,8 +249,10 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
                       int32_t* idx, int32_t* n_masked, float* t_out, void* stream);
 
 /* Forward only: l_{b,j} (Eq. per_step_loss) for j in [j_begin, j_begin + j_count).
- *   hidden    bf16  [B, L, d]  final hidden states of the response positions
- *   W_head    bf16  [d, V]     LM-head weights (V contiguous)
+ *   hidden    bf16 or fp32 [B, L, d]  final hidden states of the response
+ *                              positions (in_dtype; 16-byte aligned)
+ *   W_head    bf16 or fp32 [d, V]  LM-head weights (V contiguous; in_dtype;
+ *                              16-byte aligned)
  *   targets   int32 [B, L]     clean target token y^i of every position
  *   resp_mask uint8 [B, L]
  *   ell       double [B, n_t]  out: entries (b, j) of the range are written
@@ -198,7 +261,7 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
  *   prof      host timing record or NULL
  * Deterministic: identical inputs give bit-identical outputs, so `ell` from
  * this call fed back as `ell_old` with the same weights gives d == 0 exactly. */
-int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16_t* W_head,
+int bgpo_elbo_fwd(const bgpo_problem* prob, const void* hidden, const void* W_head,
                   const int32_t* targets, const uint8_t* resp_mask,
                   double* ell, int32_t* n_masked, float* t_out,
                   void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof);
@@ -208,7 +271,9 @@ int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16
  * memory stays constant in n_t).
  *   adv          float  [B]        advantage A_b of each response (Eq. adv)
  *   ell_old      double [B, n_t]   l under the old policy on the same samples;
- *                                  NULL = on-policy (d == 0 exactly)
+ *                                  NULL = on-policy (d == 0 exactly); must not
+ *                                  overlap ell or g (BGPO_ERR_INVALID_ARG: the
+ *                                  call writes l before it reads l_old)
  *   loss_scale   the 1/G of Algorithm 1 (any finite value)
  *   dX           float  [B, L, d]  += d loss / d hidden (zero rows stay zero
  *                                  for never-masked positions)
@@ -221,8 +286,8 @@ int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16
  *                                  l, g or gradient scale occurs (values are
  *                                  never clamped); may be NULL
  * The gradients are those of the loss (to be minimised). */
-int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
-                             const uint16_t* W_head, const int32_t* targets,
+int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const void* hidden,
+                             const void* W_head, const int32_t* targets,
                              const uint8_t* resp_mask, const float* adv,
                              const double* ell_old, double loss_scale,
                              float* dX, float* dW, double* ell, double* g, double* loss,
@@ -233,8 +298,8 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
 /* The same two calls with the final RMSNorm of the mask predictor fused in
  * front of the LM head: the head input of a position is
  *     h = norm_weight * x / sqrt(mean_i x_i^2 + norm_eps)
- * with x the pre-norm activations (bf16 [B, L, d] per sample, laid out as
- * `hidden` above, sample_stride included) and norm_weight fp32 [d]
+ * with x the pre-norm activations ([B, L, d] per sample of in_dtype, laid
+ * out as `hidden` above, sample_stride included) and norm_weight fp32 [d]
  * (16-byte aligned).  h is formed in fp32 for the masked positions only and
  * rounded once to bf16 before the head GEMMs.  The backward returns the
  * gradients w.r.t. the norm's input and weight:
@@ -243,13 +308,13 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
  * (dgamma summed over positions in a fixed order: deterministic).  Other
  * arguments, outputs and errors as in bgpo_elbo_fwd / bgpo_elbo_bwd_accumulate;
  * NULL norm_weight or d_norm_weight returns BGPO_ERR_INVALID_ARG. */
-int bgpo_elbo_fwd_rmsnorm(const bgpo_problem* prob, const uint16_t* x, const float* norm_weight,
-                          const uint16_t* W_head, const int32_t* targets,
+int bgpo_elbo_fwd_rmsnorm(const bgpo_problem* prob, const void* x, const float* norm_weight,
+                          const void* W_head, const int32_t* targets,
                           const uint8_t* resp_mask, double* ell, int32_t* n_masked, float* t_out,
                           void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof);
 
-int bgpo_elbo_bwd_accumulate_rmsnorm(const bgpo_problem* prob, const uint16_t* x,
-                                     const float* norm_weight, const uint16_t* W_head,
+int bgpo_elbo_bwd_accumulate_rmsnorm(const bgpo_problem* prob, const void* x,
+                                     const float* norm_weight, const void* W_head,
                                      const int32_t* targets, const uint8_t* resp_mask,
                                      const float* adv, const double* ell_old, double loss_scale,
                                      float* dx, float* d_norm_weight, float* dW, double* ell,

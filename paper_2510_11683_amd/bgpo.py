@@ -23,11 +23,14 @@ BGPO_ERR_INVALID_ARG = -1
 BGPO_ERR_WORKSPACE = -2
 BGPO_ERR_HIP = -3
 BGPO_ERR_UNSUPPORTED = -4
+BGPO_ERR_BUDGET = -5
+BGPO_BF16, BGPO_F32 = 0, 1
 BGPO_T_IID = 0
 BGPO_T_STRATIFIED = 1
 BGPO_FLAG_NONFINITE = 1
 BGPO_BOUND_PAPER, BGPO_BOUND_TAYLOR, BGPO_BOUND_JENSEN, BGPO_BOUND_EXACT = 0, 1, 2, 3
-KERNEL_CLASSES = ("transpose_w", "mask", "gather", "fwd", "ell", "softmax_grad", "dx", "dx_reduce", "dw")
+KERNEL_CLASSES = ("transpose_w", "mask", "gather", "fwd", "ell", "softmax_grad", "dx", "dx_reduce", "dw",
+                  "recompute")
 
 
 class _Problem(ctypes.Structure):
@@ -36,7 +39,15 @@ class _Problem(ctypes.Structure):
                 ("j_count", ctypes.c_int32), ("t_mode", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("seq_id_base", ctypes.c_uint32),
                 ("bound", ctypes.c_int32), ("sample_stride", ctypes.c_int64),
-                ("norm_eps", ctypes.c_float), ("retain_samples", ctypes.c_int32)]
+                ("norm_eps", ctypes.c_float), ("retain_samples", ctypes.c_int32),
+                ("in_dtype", ctypes.c_int32), ("vocab_chunk", ctypes.c_int32),
+                ("ws_budget", ctypes.c_uint64)]
+
+
+class _PlanInfo(ctypes.Structure):
+    _fields_ = [("samples_per_unit", ctypes.c_int32), ("dw_batch", ctypes.c_int32),
+                ("dx_splits", ctypes.c_int32), ("vocab_chunk", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_uint64)]
 
 
 class Timing(ctypes.Structure):
@@ -58,6 +69,7 @@ def _load():
     lib.bgpo_status_string.restype = ctypes.c_char_p
     lib.bgpo_status_string.argtypes = [ctypes.c_int]
     lib.bgpo_workspace_size.argtypes = [P(_Problem), P(sz)]
+    lib.bgpo_workspace_plan.argtypes = [P(_Problem), P(_PlanInfo)]
     lib.bgpo_sample_masks.argtypes = [P(_Problem), vp, i32, vp, vp, vp, vp]
     lib.bgpo_elbo_fwd.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, P(Timing)]
     lib.bgpo_elbo_bwd_accumulate.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, ctypes.c_double,
@@ -72,11 +84,11 @@ def _load():
     lib.bgpo_moments_workspace_size.argtypes = []
     lib.bgpo_moments_summary.argtypes = [vp, vp, vp, ctypes.c_int64, i32, vp, vp, sz, vp]
     lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
-    lib.bgpo_test_gemm_variant.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, vp]
-    for f in ("bgpo_workspace_size", "bgpo_sample_masks", "bgpo_elbo_fwd",
+    lib.bgpo_test_gemm_split.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp]
+    for f in ("bgpo_workspace_size", "bgpo_workspace_plan", "bgpo_sample_masks", "bgpo_elbo_fwd",
               "bgpo_elbo_bwd_accumulate", "bgpo_elbo_fwd_rmsnorm",
               "bgpo_elbo_bwd_accumulate_rmsnorm", "bgpo_moments_update", "bgpo_moments_summary",
-              "bgpo_test_gemm_nt", "bgpo_test_gemm_variant"):
+              "bgpo_test_gemm_nt", "bgpo_test_gemm_split"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -112,6 +124,9 @@ class Problem:
     sample_stride: int = 0        # elements between per-sample head inputs / dX; 0 = shared
     norm_eps: float = 1e-6        # final RMSNorm epsilon (the _rmsnorm calls)
     retain_samples: int = 0       # 1: exact objective keeping every sample's state (memory ~ n_t)
+    in_dtype: int = BGPO_BF16     # element type of hidden / x and W_head (BGPO_F32: rounded on device)
+    vocab_chunk: int = 0          # > 0: recompute backward with vocabulary chunks of this width
+    ws_budget: int = 0            # workspace byte budget (0: none); picks the backward's layout
 
     @property
     def jc(self) -> int:
@@ -120,7 +135,8 @@ class Problem:
     def c(self) -> _Problem:
         return _Problem(self.B, self.L, self.d, self.V, self.n_t, self.j_begin, self.jc, self.t_mode,
                         self.seed & 0xFFFFFFFFFFFFFFFF, self.seq_id_base & 0xFFFFFFFF, self.bound,
-                        self.sample_stride, self.norm_eps, self.retain_samples)
+                        self.sample_stride, self.norm_eps, self.retain_samples, self.in_dtype,
+                        self.vocab_chunk, self.ws_budget & 0xFFFFFFFFFFFFFFFF)
 
 
 def _ptr(t: Optional[torch.Tensor], name: str, dtypes=None, shape=None, allow_none=False):
@@ -142,6 +158,11 @@ def _ptr(t: Optional[torch.Tensor], name: str, dtypes=None, shape=None, allow_no
 _BF16 = (torch.bfloat16, torch.int16, torch.uint16)
 
 
+def _in_types(prob: "Problem"):
+    """Accepted dtypes of hidden / x and W_head for the problem's in_dtype."""
+    return (torch.float32,) if prob.in_dtype == BGPO_F32 else _BF16
+
+
 def _stream(stream):
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
@@ -155,6 +176,15 @@ def bgpo_workspace_size(prob: Problem) -> int:
     n = ctypes.c_size_t(0)
     _check(_lib.bgpo_workspace_size(ctypes.byref(prob.c()), ctypes.byref(n)), "bgpo_workspace_size")
     return int(n.value)
+
+
+def bgpo_workspace_plan(prob: Problem) -> dict:
+    """The layout the problem's workspace takes (mode, unit size, chunk, bytes)."""
+    info = _PlanInfo()
+    _check(_lib.bgpo_workspace_plan(ctypes.byref(prob.c()), ctypes.byref(info)), "bgpo_workspace_plan")
+    d = {k: int(getattr(info, k)) for k, _ in _PlanInfo._fields_}
+    d["mode"] = "recompute" if d["vocab_chunk"] else "stored"
+    return d
 
 
 def alloc_workspace(prob: Problem, device="cuda") -> torch.Tensor:
@@ -188,8 +218,8 @@ def bgpo_elbo_fwd(prob: Problem, hidden, W_head, targets, resp_mask, ell, n_mask
                   workspace, stream=None, timing: Optional[Timing] = None):
     B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
     _check(_lib.bgpo_elbo_fwd(
-        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, _act_shape(prob)),
-        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _in_types(prob), _act_shape(prob)),
+        _ptr(W_head, "W_head", _in_types(prob), (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
         _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
         _ptr(ell, "ell", (torch.float64,), (B, nt)),
         _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
@@ -204,8 +234,8 @@ def bgpo_elbo_bwd_accumulate(prob: Problem, hidden, W_head, targets, resp_mask, 
                              timing: Optional[Timing] = None):
     B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
     _check(_lib.bgpo_elbo_bwd_accumulate(
-        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _BF16, _act_shape(prob)),
-        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _in_types(prob), _act_shape(prob)),
+        _ptr(W_head, "W_head", _in_types(prob), (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
         _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
         _ptr(adv, "adv", (torch.float32,), (B,)),
         _ptr(ell_old, "ell_old", (torch.float64,), (B, nt), allow_none=True),
@@ -225,9 +255,9 @@ def bgpo_elbo_fwd_rmsnorm(prob: Problem, x, norm_weight, W_head, targets, resp_m
                           timing: Optional[Timing] = None):
     B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
     _check(_lib.bgpo_elbo_fwd_rmsnorm(
-        ctypes.byref(prob.c()), _ptr(x, "x", _BF16, _act_shape(prob)),
+        ctypes.byref(prob.c()), _ptr(x, "x", _in_types(prob), _act_shape(prob)),
         _ptr(norm_weight, "norm_weight", (torch.float32,), (d,)),
-        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        _ptr(W_head, "W_head", _in_types(prob), (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
         _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
         _ptr(ell, "ell", (torch.float64,), (B, nt)),
         _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
@@ -242,9 +272,9 @@ def bgpo_elbo_bwd_accumulate_rmsnorm(prob: Problem, x, norm_weight, W_head, targ
                                      stream=None, timing: Optional[Timing] = None):
     B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
     _check(_lib.bgpo_elbo_bwd_accumulate_rmsnorm(
-        ctypes.byref(prob.c()), _ptr(x, "x", _BF16, _act_shape(prob)),
+        ctypes.byref(prob.c()), _ptr(x, "x", _in_types(prob), _act_shape(prob)),
         _ptr(norm_weight, "norm_weight", (torch.float32,), (d,)),
-        _ptr(W_head, "W_head", _BF16, (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
+        _ptr(W_head, "W_head", _in_types(prob), (d, V)), _ptr(targets, "targets", (torch.int32,), (B, L)),
         _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
         _ptr(adv, "adv", (torch.float32,), (B,)),
         _ptr(ell_old, "ell_old", (torch.float64,), (B, nt), allow_none=True),
@@ -294,17 +324,15 @@ def bgpo_test_gemm_nt(A, B, C, stream=None):
            "bgpo_test_gemm_nt")
 
 
-def bgpo_test_gemm_variant(A, B, C, variant: int, flags: int = 0, stream=None):
-    """Test hook: tile-configuration variants of the GEMM core (see bgpo_testing.h)."""
+def bgpo_test_gemm_split(A, B, C, n_split: int, stream=None):
+    """Test hook: the GEMM core with K in n_split slices, slice s's product in
+    C[s] (C float32 [n_split, M, N])."""
     M, K = A.shape
     N = B.shape[0]
-    nsplit = max(1, (flags >> 16) & 0xFF)
-    if C.numel() < nsplit * M * N:
-        raise ValueError("C too small for the requested K split")
-    _check(_lib.bgpo_test_gemm_variant(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
-                                       _ptr(C, "C", (torch.float32,)), M, N, K,
-                                       int(variant), int(flags), _stream(stream)),
-           "bgpo_test_gemm_variant")
+    _check(_lib.bgpo_test_gemm_split(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
+                                     _ptr(C, "C", (torch.float32,), (n_split, M, N)), M, N, K,
+                                     int(n_split), _stream(stream)),
+           "bgpo_test_gemm_split")
 
 
 def device_inputs(x: dict, device="cuda") -> dict:

@@ -8,12 +8,16 @@
 // backward it also keeps the exponentials of the logits), form l, d, g and
 // the gradient scale of every (sample, response), turn the exponentials into
 // dZ = s (softmax - onehot), run one dX GEMM over the unit's rows and add each
-// sample's rows into dX in sample order; dW is accumulated once per unit.  The
+// sample's rows into dX in sample order; dW is accumulated once per batch of
+// units.  Under a small workspace budget the backward instead recomputes the
+// logits one vocabulary chunk at a time (nothing of size rows x V is kept) and
+// accumulates dX and dW chunk by chunk.  The
 // samples stay independent (the bound is a sum over samples, Eq.
 // lower_bound_def): a unit only shares the GEMM launches, which saves the
 // padded rows and partly filled GEMM rounds of one sample at a time.  All
-// buffers are views into the caller's workspace, sized by B, L, d and V;
-// nothing depends on n_t, so device memory is the same for any number of
+// buffers are views into the caller's workspace, sized by B, L, d, V, the
+// input type and the budget; nothing depends on n_t, so device memory is the
+// same for any number of
 // samples (except in the retained-state contrast mode of the exact
 // objective).
 #include <math.h>
@@ -31,39 +35,36 @@ static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 constexpr int64_t kMaxUnit = 8;
 constexpr int64_t kDwUnits = 2;   // units per dW GEMM in the constant-memory mode
+constexpr int64_t kGiB = int64_t(1) << 30;
 
-size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
+static int64_t padded_positions(const Dims& dm) {
+  const int64_t P = (int64_t)dm.B * dm.L;
+  return (P + kRowPad - 1) / kRowPad * kRowPad;
+}
+
+// largest unit whose row capacity stays within the row kernels' grid (65535
+// workgroups of 64 rows)
+static int64_t max_unit(const Dims& dm) {
+  return std::max<int64_t>(1, std::min<int64_t>(kMaxUnit, int64_t(65535) * 64 / padded_positions(dm)));
+}
+
+size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* ws,
                         Workspace* units) {
   const int64_t P = (int64_t)dm.B * dm.L;
-  const int64_t NP = (P + kRowPad - 1) / kRowPad * kRowPad;
+  const int64_t NP = padded_positions(dm);
   const int64_t nvt = (dm.V + kVocabTile - 1) / kVocabTile;
-  // samples per unit: up to kMaxUnit while the unit's dZ and H_c and the
-  // dZ^T and H_c^T columns of a dW batch of kDwUnits units stay within about
-  // 32 GB, and the unit's 64-row chunks within one grid dimension of the row
-  // kernels.  With every sample retained, the same units (at most n_t samples
-  // each) each keep their own state and all of them form the one dW batch, so
-  // both modes run the same unit compositions.
-  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2 * (1 + kDwUnits);
-  int64_t G = std::max<int64_t>(
-      1, std::min({kMaxUnit, (int64_t(32) << 30) / per_sample, int64_t(65535) * 64 / NP}));
-  if (retain) G = std::min<int64_t>(G, dm.n_t);
-  const int64_t n_units = retain ? (dm.n_t + G - 1) / G : 1;
+  const int64_t G = pl.G;
+  const int64_t n_units = pl.retain ? (dm.n_t + G - 1) / G : 1;
   const int64_t RP = G * NP;
-  // capacity of the split-vocabulary dX partials: up to 16 splits (the mask
-  // kernel picks each unit's count), within about 4 GB
-  const int64_t per_split = RP * dm.d * 4;
-  const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t(4) << 30) / per_split));
-  // constant mode: the units of a dW batch keep their dZ^T / H_c^T columns
-  // side by side (the row-major dZ and H_c are per unit), so the fp32 dW is
-  // read and written once per batch; one unit per batch where two would
-  // exceed the panel range
-  const int64_t dw_batch =
-      retain ? n_units : (kDwUnits * RP + kPanelPad <= kMaxPanelLd ? kDwUnits : 1);
+  const int64_t dw_batch = pl.retain ? n_units : pl.dw_batch;
   // leading dimension of H_c^T and dZ^T: the dW GEMM reads 256-row panels of
   // both, and with a power-of-two row pitch (32768 rows of bf16 = 64 KB at
   // the benchmark shape) their rows crowd into the same memory channels;
   // 64 extra columns (128 bytes) spread them
   const int64_t KT = dw_batch * RP + kPanelPad;
+  const int64_t chunk = pl.chunk;
+  const int64_t ldzc = chunk ? chunk + kPanelPad : dm.V;
+  const int64_t zt_rows = chunk ? chunk : dm.V;     // rows of dZ^T
 
   size_t off = 0;
   char* b = static_cast<char*>(base);
@@ -89,23 +90,26 @@ size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
     w.part_m = static_cast<float*>(take(nvt * RP * 4));
     w.part_s = static_cast<float*>(take(nvt * RP * 4));
     w.Hc = static_cast<uint16_t*>(take(RP * dm.d * 2));
-    w.dZ = static_cast<uint16_t*>(take(RP * dm.V * 2));
+    w.dZ = static_cast<uint16_t*>(take(RP * ldzc * 2));
   };
   Workspace w;
   w.dbar = static_cast<double*>(take(dm.B * 8));
   w.gpart = static_cast<float*>(take((NP / 256) * dm.d * 4));
   w.HcT = static_cast<uint16_t*>(take(KT * dm.d * 2));
   w.WT = static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2));
-  w.dZT = static_cast<uint16_t*>(take(KT * dm.V * 2));
-  w.dx_part = static_cast<float*>(take(n_split * RP * dm.d * 4));
+  w.Wb = pl.f32_in ? static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2)) : nullptr;
+  w.dZT = static_cast<uint16_t*>(take(KT * zt_rows * 2));
+  w.dx_part = static_cast<float*>(take(pl.n_split * RP * dm.d * 4));
   w.P = P;
   w.NP = NP;
   w.nvt = nvt;
   w.G = G;
   w.RP = RP;
-  w.n_split = n_split;
+  w.n_split = pl.n_split;
   w.dw_batch = dw_batch;
   w.KT = KT;
+  w.chunk = chunk;
+  w.ldzc = ldzc;
   w.g_used = (int)G;
   take_unit(w);
   for (int64_t u = 1; u < n_units; ++u) {
@@ -116,6 +120,157 @@ size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
   if (units) units[0] = w;
   if (ws) *ws = w;
   return off;
+}
+
+static size_t plan_bytes(const Dims& dm, const Plan& pl) {
+  return workspace_layout(dm, pl, nullptr, nullptr, nullptr);
+}
+
+// The stored-exponential plan used without a budget: units of up to 8
+// samples while the unit's dZ and H_c and the dZ^T and H_c^T columns of a dW
+// batch of two units stay within about 32 GB; dX split capacity up to 16
+// within about 4 GB.  With every sample retained, the same units (at most n_t
+// samples each) each keep their own state and all of them form the one dW
+// batch, so both modes run the same unit compositions.
+static Plan default_plan(const Dims& dm, int retain, int f32) {
+  const int64_t NP = padded_positions(dm);
+  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2 * (1 + kDwUnits);
+  int64_t G = std::max<int64_t>(1, std::min(max_unit(dm), 32 * kGiB / per_sample));
+  if (retain) G = std::min<int64_t>(G, dm.n_t);
+  const int64_t RP = G * NP;
+  const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, 4 * kGiB / (RP * dm.d * 4)));
+  const int64_t dw_batch = kDwUnits * RP + kPanelPad <= kMaxPanelLd ? kDwUnits : 1;
+  return Plan{G, dw_batch, n_split, 0, retain, f32};
+}
+
+// Estimated time (arbitrary units) per sample of the recompute backward for
+// a plan: the four GEMM passes at the fill of a 256-workgroup grid (tiles for
+// about half of the positions masked, as E[t] = 1/2), plus the fp32
+// read-modify-write traffic that the chunking adds (dX partials once per
+// chunk and split, dW once per unit).  Used only to rank plans.
+// The grid fill of a GEMM of `tiles` tiles on 256 workgroups, averaged over
+// masked fractions 0.4 .. 0.6 of the positions (rows_t row tiles at 0.5)
+static double mean_fill(double rows_cap, double other_tiles, double split) {
+  double f = 0.0;
+  for (double q : {0.4, 0.45, 0.5, 0.55, 0.6}) {
+    const double tiles = std::max(1.0, std::ceil(rows_cap * q / 256.0)) * other_tiles * split;
+    f += tiles / (256.0 * std::ceil(tiles / 256.0));
+  }
+  return f / 5.0;
+}
+
+static double recompute_cost(const Dims& dm, const Plan& pl) {
+  const double NP = (double)padded_positions(dm);
+  const double rows = pl.G * NP;
+  const double col_t = std::ceil(dm.d / 256.0);
+  const double chunk_t = std::ceil(pl.chunk / 256.0);
+  const double n_chunks = std::ceil((double)dm.V / pl.chunk);
+  const double pass = 2.0 * NP * 0.5 * dm.d * (double)dm.V / 1.35e15;   // s per sample per pass
+  // forward (whole vocabulary: well filled), recompute, dX, dW (its tiles
+  // span the chunk and d, not the rows)
+  const double dw_tiles = chunk_t * col_t;
+  const double dw_fill = dw_tiles / (256.0 * std::ceil(dw_tiles / 256.0));
+  const double gemm = pass * (1.0 + 1.0 / mean_fill(rows, chunk_t, 1.0) +
+                              1.0 / mean_fill(rows, col_t, (double)pl.n_split) + 1.0 / dw_fill);
+  const double rmw = (n_chunks * NP * 0.5 * dm.d * 8.0 * pl.n_split + (double)dm.V * dm.d * 8.0 / pl.G) /
+                     5e12;
+  return gemm + rmw;
+}
+
+// The same estimate for the stored-exponential backward: three GEMM passes
+// (the dX GEMM at the best split the capacity allows), the softmax-gradient
+// pass over the kept exponentials (6 bytes per entry) and the dW
+// read-modify-write once per batch of units.
+static double stored_cost(const Dims& dm, const Plan& pl) {
+  const double NP = (double)padded_positions(dm);
+  const double rows = pl.G * NP;
+  const double col_t = std::ceil(dm.d / 256.0);
+  double dx_fill = 0.0;
+  for (int64_t sp = 1; sp <= pl.n_split; ++sp)
+    dx_fill = std::max(dx_fill, mean_fill(rows, col_t, (double)sp));
+  const double pass = 2.0 * NP * 0.5 * dm.d * (double)dm.V / 1.35e15;
+  const double gemm = pass * (1.0 / mean_fill(rows, std::ceil(dm.V / 256.0), 1.0) + 1.0 / dx_fill + 1.0);
+  const double mem = (6.0 * NP * 0.5 * dm.V + (double)dm.V * dm.d * 8.0 / (pl.G * pl.dw_batch)) / 5e12;
+  return gemm + mem;
+}
+
+// Chooses the plan of a problem (see bgpo.h: backward modes and the workspace
+// budget).  Returns BGPO_OK, or BGPO_ERR_BUDGET when nothing fits the budget.
+static int choose_plan(const bgpo_problem* p, Plan* out) {
+  const Dims dm{p->B, p->L, p->d, p->V, p->n_t};
+  const int f32 = p->in_dtype == BGPO_F32;
+  const uint64_t budget = p->ws_budget;
+  if (p->retain_samples || (budget == 0 && p->vocab_chunk == 0)) {
+    *out = default_plan(dm, p->retain_samples, f32);
+    return BGPO_OK;
+  }
+  const int64_t NP = padded_positions(dm);
+  if (p->vocab_chunk == 0) {
+    // the default layout if it fits, else the stored-mode layout of least
+    // estimated time that fits
+    const Plan dflt = default_plan(dm, 0, f32);
+    if (plan_bytes(dm, dflt) <= budget) {
+      *out = dflt;
+      return BGPO_OK;
+    }
+    bool found = false;
+    Plan best{};
+    double best_cost = 0.0;
+    for (int64_t G = max_unit(dm); G >= 1; --G) {
+      for (int64_t dwb = kDwUnits; dwb >= 1; --dwb) {
+        if (dwb * G * NP + kPanelPad > kMaxPanelLd) continue;
+        const int64_t ns_max = std::max<int64_t>(1, std::min<int64_t>(16, 4 * kGiB / (G * NP * p->d * 4)));
+        for (int64_t ns = 1; ns <= ns_max; ++ns) {
+          const Plan pl{G, dwb, ns, 0, 0, f32};
+          if (plan_bytes(dm, pl) > budget) break;   // more splits only take more memory
+          const double c = stored_cost(dm, pl);
+          if (!found || c < best_cost) {
+            found = true;
+            best = pl;
+            best_cost = c;
+          }
+        }
+      }
+    }
+    if (found) {
+      *out = best;
+      return BGPO_OK;
+    }
+  }
+  // recompute mode: the cheapest (unit, chunk, split capacity) that fits the
+  // budget (or about 32 GB without one)
+  const uint64_t cap = budget ? budget : (uint64_t)(32 * kGiB);
+  const int64_t v_round = ((int64_t)p->V + 255) / 256 * 256;
+  std::vector<int64_t> widths;
+  if (p->vocab_chunk) {
+    widths.push_back(std::min<int64_t>(p->vocab_chunk, v_round));
+  } else {
+    for (int64_t c : {32768, 16384, 8192, 4096, 2048, 1024, 512, 256}) {
+      const int64_t w = std::min<int64_t>(c, v_round);
+      if (widths.empty() || widths.back() != w) widths.push_back(w);
+    }
+  }
+  bool found = false;
+  Plan best{};
+  double best_cost = 0.0;
+  for (int64_t G = max_unit(dm); G >= 1; --G) {
+    if (G * NP + kPanelPad > kMaxPanelLd) continue;
+    for (int64_t C : widths) {
+      for (int64_t ns : {4, 2, 1}) {
+        const Plan pl{G, 1, ns, C, 0, f32};
+        if (plan_bytes(dm, pl) > cap) continue;
+        const double c = recompute_cost(dm, pl);
+        if (!found || c < best_cost) {
+          found = true;
+          best = pl;
+          best_cost = c;
+        }
+      }
+    }
+  }
+  if (!found) return BGPO_ERR_BUDGET;
+  *out = best;
+  return BGPO_OK;
 }
 
 // HIP-event timing of kernel classes, enabled by a non-NULL record.
@@ -168,25 +323,30 @@ class Timer {
   std::vector<Ev> ev_;
 };
 
-static int check_problem(const bgpo_problem* p) {
+// Validates a problem and chooses its plan (the layout its workspace takes).
+static int plan_problem(const bgpo_problem* p, Plan* pl) {
   if (!p) return BGPO_ERR_INVALID_ARG;
   if (p->B < 1 || p->L < 1 || p->n_t < 1 || p->j_begin < 0 || p->j_count < 0 ||
       (int64_t)p->j_begin + p->j_count > p->n_t || (p->t_mode != BGPO_T_IID && p->t_mode != BGPO_T_STRATIFIED) ||
       p->bound < BGPO_BOUND_PAPER || p->bound > BGPO_BOUND_EXACT || p->d < 1 || p->V < 1 ||
       p->sample_stride < 0 || p->sample_stride % 8 || !isfinite(p->norm_eps) || p->norm_eps < 0.f ||
       (p->retain_samples != 0 && p->retain_samples != 1) ||
-      (p->retain_samples && p->bound != BGPO_BOUND_EXACT))
+      (p->retain_samples && p->bound != BGPO_BOUND_EXACT) ||
+      (p->in_dtype != BGPO_BF16 && p->in_dtype != BGPO_F32) || p->vocab_chunk < 0 ||
+      p->vocab_chunk % 256 || (p->retain_samples && (p->vocab_chunk || p->ws_budget)))
     return BGPO_ERR_INVALID_ARG;
   if (p->B > 4096 || (int64_t)p->B * p->L > (1 << 20) || p->d % 64 || p->V % 64 || p->d < 64 ||
       p->d > 65536 || p->V < 64 || p->V > (1 << 20))
     return BGPO_ERR_UNSUPPORTED;
+  const int st = choose_plan(p, pl);
+  if (st != BGPO_OK) return st;
   // H_c^T and dZ^T (leading dimension KT) are operand panels of the dW GEMM.
   // One unit's row capacity stays within 65535 * 64 by construction; with
   // every sample retained KT grows with n_t and is bounded here.
   static_assert(int64_t(65535) * 64 / 256 * 256 + kPanelPad <= kMaxPanelLd,
                 "constant-mode KT must fit a panel");
   Workspace w;
-  workspace_layout(Dims{p->B, p->L, p->d, p->V, p->n_t}, p->retain_samples, nullptr, &w, nullptr);
+  workspace_layout(Dims{p->B, p->L, p->d, p->V, p->n_t}, *pl, nullptr, &w, nullptr);
   if (w.KT > kMaxPanelLd) return BGPO_ERR_UNSUPPORTED;
   return BGPO_OK;
 }
@@ -198,20 +358,27 @@ static Dims dims_of(const bgpo_problem* p) { return Dims{p->B, p->L, p->d, p->V,
     if ((expr) != hipSuccess) return BGPO_ERR_HIP; \
   } while (0)
 
+// the dX GEMM's K: the whole vocabulary, or one chunk of it in the recompute mode
 static DxPlan dx_plan(const Dims& dm, const Workspace& ws, int grid) {
-  return DxPlan{dm.V / 64, (dm.d + 255) / 256, grid, (int)ws.n_split};
+  const int k = ws.chunk ? (int)std::min<int64_t>(ws.chunk, dm.V) : dm.V;
+  return DxPlan{k / 64, (dm.d + 255) / 256, grid, (int)ws.n_split};
 }
 
 // The head input of the samples of a call: sample j reads x + (j - j_begin) *
-// stride (stride 0: one tensor shared by all samples), normalised by the
-// final RMSNorm when gamma is given.
+// stride elements (stride 0: one tensor shared by all samples; bf16 or, with
+// f32, fp32 elements), normalised by the final RMSNorm when gamma is given.
 struct Act {
-  const uint16_t* x;
+  const void* x;
+  bool f32;
   const float* gamma;
   float eps;
   int64_t stride;
   int j0;
-  const uint16_t* at(int j) const { return x + (int64_t)(j - j0) * stride; }
+  const void* at(int j) const {
+    const int64_t off = (int64_t)(j - j0) * stride;
+    return f32 ? (const void*)(static_cast<const float*>(x) + off)
+               : (const void*)(static_cast<const uint16_t*>(x) + off);
+  }
 };
 
 // forward part of the unit of samples j0 .. j0 + n_s - 1: masks .. l (and,
@@ -235,8 +402,9 @@ static int run_forward_unit(const bgpo_problem* p, Workspace& ws, Timer& tm, int
   }
   BGPO_TRY(tm.end(n_s));
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
-  if (act.gamma) BGPO_TRY(launch_row_rms(act.at(j0), act.stride, dm.B, ws, dm.d, act.eps, s));
-  BGPO_TRY(launch_gather(act.at(j0), act.stride, dm.B, act.gamma, ws, dm.d, s));
+  if (act.gamma)
+    BGPO_TRY(launch_row_rms(act.at(j0), act.f32, act.stride, dm.B, ws, dm.d, act.eps, s));
+  BGPO_TRY(launch_gather(act.at(j0), act.f32, act.stride, dm.B, act.gamma, ws, dm.d, s));
   BGPO_TRY(tm.end(act.gamma ? 2 : 1));
   BGPO_TRY(tm.begin(BGPO_K_FWD));
   BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, store_u, s));
@@ -263,7 +431,7 @@ using namespace bgpo;
 
 extern "C" {
 
-int bgpo_version(void) { return (2 << 16) | 0; }
+int bgpo_version(void) { return (3 << 16) | 0; }
 
 const char* bgpo_status_string(int status) {
   switch (status) {
@@ -272,21 +440,38 @@ const char* bgpo_status_string(int status) {
     case BGPO_ERR_WORKSPACE: return "BGPO_ERR_WORKSPACE: workspace missing, misaligned or too small";
     case BGPO_ERR_HIP: return "BGPO_ERR_HIP: a HIP runtime call failed";
     case BGPO_ERR_UNSUPPORTED: return "BGPO_ERR_UNSUPPORTED: shape outside the supported set";
+    case BGPO_ERR_BUDGET: return "BGPO_ERR_BUDGET: no workspace layout fits the workspace budget";
     default: return "unknown bgpo status";
   }
 }
 
 int bgpo_workspace_size(const bgpo_problem* prob, size_t* bytes) {
-  const int st = check_problem(prob);
+  Plan pl;
+  const int st = plan_problem(prob, &pl);
   if (st != BGPO_OK) return st;
   if (!bytes) return BGPO_ERR_INVALID_ARG;
-  *bytes = workspace_layout(dims_of(prob), prob->retain_samples, nullptr, nullptr, nullptr);
+  *bytes = workspace_layout(dims_of(prob), pl, nullptr, nullptr, nullptr);
+  return BGPO_OK;
+}
+
+int bgpo_workspace_plan(const bgpo_problem* prob, bgpo_plan_info* info) {
+  Plan pl;
+  const int st = plan_problem(prob, &pl);
+  if (st != BGPO_OK) return st;
+  if (!info) return BGPO_ERR_INVALID_ARG;
+  Workspace w;
+  info->workspace_bytes = workspace_layout(dims_of(prob), pl, nullptr, &w, nullptr);
+  info->samples_per_unit = (int32_t)w.G;
+  info->dw_batch = (int32_t)w.dw_batch;
+  info->dx_splits = (int32_t)w.n_split;
+  info->vocab_chunk = (int32_t)w.chunk;
   return BGPO_OK;
 }
 
 int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_t j, int32_t* idx,
                       int32_t* n_masked, float* t_out, void* stream) {
-  const int st = check_problem(prob);
+  Plan pl;
+  const int st = plan_problem(prob, &pl);
   if (st != BGPO_OK) return st;
   if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
   if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, 0, prob->t_mode,
@@ -298,35 +483,62 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-static int check_workspace(const bgpo_problem* prob, void* workspace, size_t ws_bytes) {
+static int check_workspace(const bgpo_problem* prob, const Plan& pl, void* workspace,
+                           size_t ws_bytes) {
   if (!workspace || ((uintptr_t)workspace % 256) != 0) return BGPO_ERR_WORKSPACE;
-  if (ws_bytes < workspace_layout(dims_of(prob), prob->retain_samples, nullptr, nullptr, nullptr))
+  if (ws_bytes < workspace_layout(dims_of(prob), pl, nullptr, nullptr, nullptr))
     return BGPO_ERR_WORKSPACE;
   return BGPO_OK;
+}
+
+// [B, n_t] doubles at a and b share a byte
+static bool overlaps(const double* a, const double* b, int64_t n) {
+  const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b, len = (uintptr_t)n * sizeof(double);
+  return pa < pb + len && pb < pa + len;
 }
 
 }  // extern "C"
 
 namespace bgpo {
 
-// the gradient part of a unit once its scales are known: dZ, dX (each
-// sample's rows in sample order, with the norm backward), leaving its dZ^T
-// columns for the dW GEMM
+// the gradient part of a unit once its scales are known.  Stored mode: dZ
+// from the kept exponentials, one dX GEMM over the whole vocabulary, the
+// unit's dZ^T columns left for the dW GEMM of its batch.  Recompute mode: per
+// vocabulary chunk, the chunk's logits -> its dZ, dX partials accumulated,
+// dW[:, chunk] accumulated.  Then each sample's rows are added into dX in
+// sample order (with the norm backward).  W_dx: the bf16 W_head the dX GEMM
+// reads.
 static int unit_backward(const Workspace& ws, const Act& act, int j0, int j_begin,
-                         const uint16_t* W_head, float* dX, float* dgamma, const Dims& dm,
-                         int grid, Timer& tm, hipStream_t s) {
-  BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
-  BGPO_TRY(launch_softmax_grad(ws, dm.V, s));
-  BGPO_TRY(tm.end());
-  BGPO_TRY(tm.begin(BGPO_K_DX));
-  BGPO_TRY(launch_gemm_dx(ws, W_head, dm.d, dm.V, grid, s));
-  BGPO_TRY(tm.end());
+                         const uint16_t* W_dx, float* dX, float* dgamma, float* dW,
+                         const Dims& dm, int grid, Timer& tm, hipStream_t s) {
+  if (!ws.chunk) {
+    BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
+    BGPO_TRY(launch_softmax_grad(ws, dm.V, s));
+    BGPO_TRY(tm.end());
+    BGPO_TRY(tm.begin(BGPO_K_DX));
+    BGPO_TRY(launch_gemm_dx(ws, W_dx, dm.d, dm.V, grid, s));
+    BGPO_TRY(tm.end());
+  } else {
+    for (int v0 = 0; v0 < dm.V; v0 += (int)ws.chunk) {
+      const int width = (int)std::min<int64_t>(ws.chunk, dm.V - v0);
+      BGPO_TRY(tm.begin(BGPO_K_RECOMPUTE));
+      BGPO_TRY(launch_gemm_recompute(ws, dm.d, v0, width, grid, s));
+      BGPO_TRY(tm.end());
+      BGPO_TRY(tm.begin(BGPO_K_DX));
+      BGPO_TRY(launch_gemm_dx_chunk(ws, W_dx, dm.d, dm.V, v0, width, v0 == 0, grid, s));
+      BGPO_TRY(tm.end());
+      BGPO_TRY(tm.begin(BGPO_K_DW));
+      BGPO_TRY(launch_gemm_dw_chunk(ws, dW, dm.d, dm.V, v0, width, grid, s));
+      BGPO_TRY(tm.end());
+    }
+  }
   BGPO_TRY(tm.begin(BGPO_K_DX_REDUCE));
   for (int gs = 0; gs < ws.g_used; ++gs) {
     const int j = j0 + gs;
     float* dXj = dX + (int64_t)(j - j_begin) * act.stride;
     if (act.gamma)
-      BGPO_TRY(launch_dx_reduce_rmsnorm(ws, gs, act.at(j), act.gamma, dXj, dgamma, dm.d, s));
+      BGPO_TRY(launch_dx_reduce_rmsnorm(ws, gs, act.at(j), act.f32, act.gamma, dXj, dgamma, dm.d,
+                                        s));
     else
       BGPO_TRY(launch_dx_reduce(ws, gs, dXj, dm.d, s));
   }
@@ -339,21 +551,22 @@ static int unit_backward(const Workspace& ws, const Act& act, int j0, int j_begi
 // forward runs once and keeps its exponentials, the mean log-ratio is formed,
 // then every sample's gradient comes from its kept state; memory grows with
 // n_t.  The units are those of the two-pass mode, each with its own state.
-static int bwd_retained(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
-                        const int32_t* targets, const uint8_t* resp_mask, const float* adv,
-                        const double* ell_old, double loss_scale, float* dX, float* dgamma,
-                        float* dW, double* ell, double* g, double* loss, int32_t* n_masked,
-                        float* t_out, int32_t* status_flags, void* workspace, int grid, Timer& tm,
-                        hipStream_t s) {
+static int bwd_retained(const bgpo_problem* prob, const Plan& pl, const Act& act,
+                        const void* W_head, const int32_t* targets, const uint8_t* resp_mask,
+                        const float* adv, const double* ell_old, double loss_scale, float* dX,
+                        float* dgamma, float* dW, double* ell, double* g, double* loss,
+                        int32_t* n_masked, float* t_out, int32_t* status_flags, void* workspace,
+                        int grid, Timer& tm, hipStream_t s) {
   const Dims dm = dims_of(prob);
   Workspace ws;
-  workspace_layout(dm, 1, workspace, &ws, nullptr);
+  workspace_layout(dm, pl, workspace, &ws, nullptr);
   const int G = (int)ws.G, n_units = (int)ws.dw_batch;
   std::vector<Workspace> U(n_units);
-  workspace_layout(dm, 1, workspace, nullptr, U.data());
+  workspace_layout(dm, pl, workspace, nullptr, U.data());
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
-  BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
+  BGPO_TRY(launch_transpose_w(W_head, act.f32, ws.WT, ws.Wb, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
+  const uint16_t* W_dx = act.f32 ? ws.Wb : static_cast<const uint16_t*>(W_head);
   for (int u = 0; u < n_units; ++u) {
     const int j0 = u * G, n_s = std::min(G, dm.n_t - j0);
     const int st = run_forward_unit(prob, U[u], tm, grid, j0, n_s, act, targets, resp_mask,
@@ -375,7 +588,7 @@ static int bwd_retained(const bgpo_problem* prob, const Act& act, const uint16_t
     BGPO_TRY(launch_seq_terms(U[u], dm.B, dm.n_t, j0, adv, ell_old, loss_scale, ell, g, loss,
                               status_flags, true, prob->bound, dbar, s));
     BGPO_TRY(tm.end());
-    const int st = unit_backward(U[u], act, j0, 0, W_head, dX, dgamma, dm, grid, tm, s);
+    const int st = unit_backward(U[u], act, j0, 0, W_dx, dX, dgamma, dW, dm, grid, tm, s);
     if (st != BGPO_OK) return st;
   }
   BGPO_TRY(tm.begin(BGPO_K_DW));
@@ -384,27 +597,31 @@ static int bwd_retained(const bgpo_problem* prob, const Act& act, const uint16_t
   return BGPO_OK;
 }
 
-static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
+static bool aligned_inputs(const Act& act, const void* W_head) {
+  return aligned16(act.x) && aligned16(W_head) && (!act.gamma || aligned16(act.gamma));
+}
+
+static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const void* W_head,
                          const int32_t* targets, const uint8_t* resp_mask, double* ell,
                          int32_t* n_masked, float* t_out, void* workspace, size_t ws_bytes,
                          void* stream, bgpo_timing* prof) {
-  int st = check_problem(prob);
+  Plan pl;
+  int st = plan_problem(prob, &pl);
   if (st != BGPO_OK) return st;
   if (!act.x || !W_head || !targets || !resp_mask || !ell || !n_masked) return BGPO_ERR_INVALID_ARG;
-  if (!aligned16(act.x) || !aligned16(W_head) || (act.gamma && !aligned16(act.gamma)))
-    return BGPO_ERR_INVALID_ARG;
-  if ((st = check_workspace(prob, workspace, ws_bytes)) != BGPO_OK) return st;
+  if (!aligned_inputs(act, W_head)) return BGPO_ERR_INVALID_ARG;
+  if ((st = check_workspace(prob, pl, workspace, ws_bytes)) != BGPO_OK) return st;
   if (prob->j_count == 0) return BGPO_OK;
   hipStream_t s = (hipStream_t)stream;
   Workspace ws;
   // the layout the workspace was checked against (with retain_samples the
-  // first sample's state and the shared buffers; one sample at a time)
-  workspace_layout(dims_of(prob), prob->retain_samples, workspace, &ws, nullptr);
+  // first unit's state and the shared buffers; one unit at a time)
+  workspace_layout(dims_of(prob), pl, workspace, &ws, nullptr);
   int grid = 0;
   if ((st = device_grid(&grid)) != BGPO_OK) return st;
   Timer tm(prof, s);
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
-  BGPO_TRY(launch_transpose_w(W_head, ws.WT, prob->d, prob->V, s));
+  BGPO_TRY(launch_transpose_w(W_head, act.f32, ws.WT, nullptr, prob->d, prob->V, s));
   BGPO_TRY(tm.end());
   const int j_end = prob->j_begin + prob->j_count;
   for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.G) {
@@ -419,21 +636,26 @@ static int elbo_fwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
 }
 
 // dX (and dgamma with the norm) are per sample at dX + (j - j_begin) * stride.
-static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_t* W_head,
+static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const void* W_head,
                          const int32_t* targets, const uint8_t* resp_mask, const float* adv,
                          const double* ell_old, double loss_scale, float* dX, float* dgamma,
                          float* dW, double* ell, double* g, double* loss, int32_t* n_masked,
                          float* t_out, int32_t* status_flags, void* workspace, size_t ws_bytes,
                          void* stream, bgpo_timing* prof) {
-  int st = check_problem(prob);
+  Plan pl;
+  int st = plan_problem(prob, &pl);
   if (st != BGPO_OK) return st;
   if (!act.x || !W_head || !targets || !resp_mask || !adv || !dX || !dW || !ell || !g || !loss ||
       !n_masked || !isfinite(loss_scale) || (act.gamma && !dgamma))
     return BGPO_ERR_INVALID_ARG;
-  if (!aligned16(act.x) || !aligned16(W_head) || !aligned16(dX) || !aligned16(dW) ||
-      (act.gamma && !aligned16(act.gamma)))
+  if (!aligned_inputs(act, W_head) || !aligned16(dX) || !aligned16(dW))
     return BGPO_ERR_INVALID_ARG;
-  if ((st = check_workspace(prob, workspace, ws_bytes)) != BGPO_OK) return st;
+  // l is written before l_old is read (per response, and in the exact mode's
+  // first pass for every sample): l_old must be a buffer of its own
+  const int64_t nbt = (int64_t)prob->B * prob->n_t;
+  if (ell_old && (overlaps(ell_old, ell, nbt) || overlaps(ell_old, g, nbt)))
+    return BGPO_ERR_INVALID_ARG;
+  if ((st = check_workspace(prob, pl, workspace, ws_bytes)) != BGPO_OK) return st;
   const bool exact = prob->bound == BGPO_BOUND_EXACT;
   if (exact && (prob->j_begin != 0 || prob->j_count != prob->n_t)) return BGPO_ERR_INVALID_ARG;
   if (prob->j_count == 0) return BGPO_OK;
@@ -443,17 +665,19 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
   if ((st = device_grid(&grid)) != BGPO_OK) return st;
   Timer tm(prof, s);
   if (prob->retain_samples) {
-    st = bwd_retained(prob, act, W_head, targets, resp_mask, adv, ell_old, loss_scale, dX, dgamma,
-                      dW, ell, g, loss, n_masked, t_out, status_flags, workspace, grid, tm, s);
+    st = bwd_retained(prob, pl, act, W_head, targets, resp_mask, adv, ell_old, loss_scale, dX,
+                      dgamma, dW, ell, g, loss, n_masked, t_out, status_flags, workspace, grid, tm,
+                      s);
     if (st != BGPO_OK) return st;
     BGPO_TRY(tm.finish());
     return BGPO_OK;
   }
   Workspace ws;
-  workspace_layout(dm, 0, workspace, &ws, nullptr);
+  workspace_layout(dm, pl, workspace, &ws, nullptr);
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
-  BGPO_TRY(launch_transpose_w(W_head, ws.WT, dm.d, dm.V, s));
+  BGPO_TRY(launch_transpose_w(W_head, act.f32, ws.WT, ws.Wb, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
+  const uint16_t* W_dx = act.f32 ? ws.Wb : static_cast<const uint16_t*>(W_head);
   // exact objective off-policy: a forward pass over every sample gives the
   // mean log-ratio, which scales every sample's gradient (on-policy it is 0)
   const double* dbar = nullptr;
@@ -471,6 +695,7 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
     dbar = ws.dbar;
   }
   const int j_end = prob->j_begin + prob->j_count;
+  const bool store_u = !ws.chunk;   // stored mode keeps the forward's exponentials
   int in_batch = 0;        // units already in the current dW batch
   int prev_used = 0;       // samples of the previous unit (its record is meta[prev_used - 1])
   for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.G) {
@@ -480,14 +705,15 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
     // before any record is rewritten)
     const SampleMeta* prev = in_batch ? ws.meta + (prev_used - 1) : nullptr;
     st = run_forward_unit(prob, ws, tm, grid, j0, n_s, act, targets, resp_mask, adv, ell_old,
-                          loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, true,
+                          loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, store_u,
                           prev, dbar, s);
     if (st != BGPO_OK) return st;
-    st = unit_backward(ws, act, j0, prob->j_begin, W_head, dX, dgamma, dm, grid, tm, s);
+    st = unit_backward(ws, act, j0, prob->j_begin, W_dx, dX, dgamma, dW, dm, grid, tm, s);
     if (st != BGPO_OK) return st;
     prev_used = n_s;
-    // one dW GEMM per batch of units: K runs over all their rows
-    if (++in_batch == (int)ws.dw_batch || j0 + n_s >= j_end) {
+    // stored mode: one dW GEMM per batch of units, K over all their rows (the
+    // recompute mode accumulated dW chunk by chunk)
+    if (!ws.chunk && (++in_batch == (int)ws.dw_batch || j0 + n_s >= j_end)) {
       BGPO_TRY(tm.begin(BGPO_K_DW));
       BGPO_TRY(launch_gemm_dw(ws, dW, dm.d, dm.V, grid, s));
       BGPO_TRY(tm.end());
@@ -498,15 +724,16 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const uint16_
   return BGPO_OK;
 }
 
-static Act act_of(const bgpo_problem* p, const uint16_t* x, const float* gamma) {
-  return Act{x, gamma, p ? p->norm_eps : 0.f, p ? p->sample_stride : 0, p ? p->j_begin : 0};
+static Act act_of(const bgpo_problem* p, const void* x, const float* gamma) {
+  return Act{x, p && p->in_dtype == BGPO_F32, gamma, p ? p->norm_eps : 0.f,
+             p ? p->sample_stride : 0, p ? p->j_begin : 0};
 }
 
 }  // namespace bgpo
 
 extern "C" {
 
-int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16_t* W_head,
+int bgpo_elbo_fwd(const bgpo_problem* prob, const void* hidden, const void* W_head,
                   const int32_t* targets, const uint8_t* resp_mask, double* ell,
                   int32_t* n_masked, float* t_out, void* workspace, size_t ws_bytes, void* stream,
                   bgpo_timing* prof) {
@@ -514,8 +741,8 @@ int bgpo_elbo_fwd(const bgpo_problem* prob, const uint16_t* hidden, const uint16
                        n_masked, t_out, workspace, ws_bytes, stream, prof);
 }
 
-int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
-                             const uint16_t* W_head, const int32_t* targets,
+int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const void* hidden,
+                             const void* W_head, const int32_t* targets,
                              const uint8_t* resp_mask, const float* adv, const double* ell_old,
                              double loss_scale, float* dX, float* dW, double* ell, double* g,
                              double* loss, int32_t* n_masked, float* t_out, int32_t* status_flags,
@@ -525,8 +752,8 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const uint16_t* hidden,
                        status_flags, workspace, ws_bytes, stream, prof);
 }
 
-int bgpo_elbo_fwd_rmsnorm(const bgpo_problem* prob, const uint16_t* x, const float* norm_weight,
-                          const uint16_t* W_head, const int32_t* targets,
+int bgpo_elbo_fwd_rmsnorm(const bgpo_problem* prob, const void* x, const float* norm_weight,
+                          const void* W_head, const int32_t* targets,
                           const uint8_t* resp_mask, double* ell, int32_t* n_masked, float* t_out,
                           void* workspace, size_t ws_bytes, void* stream, bgpo_timing* prof) {
   if (!norm_weight) return BGPO_ERR_INVALID_ARG;
@@ -534,8 +761,8 @@ int bgpo_elbo_fwd_rmsnorm(const bgpo_problem* prob, const uint16_t* x, const flo
                        n_masked, t_out, workspace, ws_bytes, stream, prof);
 }
 
-int bgpo_elbo_bwd_accumulate_rmsnorm(const bgpo_problem* prob, const uint16_t* x,
-                                     const float* norm_weight, const uint16_t* W_head,
+int bgpo_elbo_bwd_accumulate_rmsnorm(const bgpo_problem* prob, const void* x,
+                                     const float* norm_weight, const void* W_head,
                                      const int32_t* targets, const uint8_t* resp_mask,
                                      const float* adv, const double* ell_old, double loss_scale,
                                      float* dx, float* d_norm_weight, float* dW, double* ell,

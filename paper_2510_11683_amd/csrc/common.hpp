@@ -80,4 +80,33 @@ __device__ __forceinline__ float f16_to_f32(uint16_t h) {
 
 __device__ __forceinline__ float bf16_to_f32(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
+// Head inputs as bf16 bit patterns, 8 or 4 consecutive elements at a time:
+// bf16 inputs as they are, fp32 inputs rounded to nearest even (so both
+// element types give the same bits for the same rounded values).  p must be
+// 16-byte (bf16 x8, fp32 x4) or 8-byte (bf16 x4) aligned.
+template <typename T>
+__device__ __forceinline__ uint4 load_bf16x8(const T* p);
+template <>
+__device__ __forceinline__ uint4 load_bf16x8<uint16_t>(const uint16_t* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+template <>
+__device__ __forceinline__ uint4 load_bf16x8<float>(const float* p) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  return make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(b.x, b.y),
+                    pack_bf16x2(b.z, b.w));
+}
+template <typename T>
+__device__ __forceinline__ uint2 load_bf16x4(const T* p);
+template <>
+__device__ __forceinline__ uint2 load_bf16x4<uint16_t>(const uint16_t* p) {
+  return *reinterpret_cast<const uint2*>(p);
+}
+template <>
+__device__ __forceinline__ uint2 load_bf16x4<float>(const float* p) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  return make_uint2(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w));
+}
+
 }  // namespace bgpo

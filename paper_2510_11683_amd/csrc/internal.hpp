@@ -62,6 +62,7 @@ struct Workspace {
   uint16_t* Hc;        // [RP, d]      gathered masked hidden rows (bf16)
   uint16_t* HcT;       // [d, KT]      the same, transposed; units of a dW batch side by side
   uint16_t* WT;        // [V, d]       W_head transposed (bf16)
+  uint16_t* Wb;        // [d, V]       W_head rounded to bf16 (fp32 inputs only, else NULL)
   float* part_m;       // [nvt, RP]    per-vocabulary-slice max (log2 units)
   float* part_s;       // [nvt, RP]    per-vocabulary-slice sum of 2^(z*log2e - max)
   float* ztgt;         // [RP]         target logit
@@ -71,15 +72,20 @@ struct Workspace {
   double* dbar;        // [B]          mean log-ratio over all samples (exact objective)
   float* inv_rms;      // [RP]         final-RMSNorm 1/rms of each compacted row
   float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks of a sample
-  uint16_t* dZ;        // [RP, V]      s (softmax - onehot), bf16 (first the fp16 exponentials)
-  uint16_t* dZT;       // [V, KT]      the same, transposed; units of a dW batch side by side
+  uint16_t* dZ;        // stored mode: [RP, V] s (softmax - onehot), bf16 (first the fp16
+                       // exponentials); recompute mode: [RP, chunk], one vocabulary chunk
+  uint16_t* dZT;       // stored mode: [V, KT] the same, transposed, units of a dW batch side
+                       // by side; recompute mode: [chunk, KT], one chunk
   float* dx_part;      // [S, RP, d]   split-vocabulary partial dX
   int64_t P, NP, nvt;
   int64_t G;           // samples per unit
   int64_t RP;          // G * NP: row capacity of a unit
   int64_t n_split;     // capacity of dx_part in splits (the unit's count is in its meta)
   int64_t dw_batch;    // units whose dW contributions share one GEMM
-  int64_t KT;          // dw_batch * RP: leading dimension of H_c^T and dZ^T
+  int64_t KT;          // dw_batch * RP + pad: leading dimension of H_c^T and dZ^T
+  int64_t chunk;       // 0: stored exponentials; > 0: recompute backward, vocabulary chunk width
+  int64_t ldzc;        // recompute mode: row pitch of the chunk's dZ (chunk + pad: no
+                       // power-of-two pitch)
   int g_used;          // samples in the current unit (host side; its record meta[g_used - 1]
                        // describes the unit)
   const SampleMeta* unit() const { return meta + (g_used - 1); }
@@ -89,19 +95,33 @@ struct Dims {
   int B, L, d, V, n_t;
 };
 
-// Views into the caller's workspace (base may be NULL: sizes only).
-// retain = 0: the state of one unit of G samples at a time (G chosen from the
-//             shapes, never from n_t), one unit per dW GEMM; the size does not
-//             depend on n_t.
+// How a problem uses its workspace, chosen from the shapes, the input type and
+// the budget (never from n_t, except the unit count of the retained mode).
+struct Plan {
+  int64_t G;          // samples per unit
+  int64_t dw_batch;   // units per dW GEMM (stored mode)
+  int64_t n_split;    // capacity of the dX split partials, in splits
+  int64_t chunk;      // 0: stored exponentials; > 0: recompute in vocabulary chunks of this width
+  int retain;         // every unit keeps its own state (memory grows with n_t)
+  int f32_in;         // fp32 inputs: keep a bf16 copy of W_head
+};
+
+// Views into the caller's workspace for plan `pl` (base may be NULL: sizes
+// only).
+// retain = 0: the state of one unit of G samples at a time, dw_batch units
+//             per dW GEMM; the size does not depend on n_t.
 // retain = 1: the same units (G capped at n_t), each keeping its own state
 //             (units[0 .. ceil(n_t / G)): meta, rows, partials, H_c and dZ;
 //             H_c^T / dZ^T hold all units' columns; one dW batch), so memory
 //             grows with n_t.
-size_t workspace_layout(const Dims& dm, int retain, void* base, Workspace* ws,
+size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* ws,
                         Workspace* units);
 
 // ---- launchers (return hipSuccess or the launch error) ----
-hipError_t launch_transpose_w(const uint16_t* W, uint16_t* WT, int d, int V, hipStream_t s);
+// W_head -> W^T (bf16); fp32 W (f32) is rounded to bf16, and its rounded copy
+// in natural layout goes to Wb
+hipError_t launch_transpose_w(const void* W, bool f32, uint16_t* WT, uint16_t* Wb, int d, int V,
+                              hipStream_t s);
 // Mask and compaction of sample j, sample g of its unit: rows go after those of
 // the unit's earlier samples (prev = record of sample g - 1); for g = 0, prev
 // (may be NULL) is the record of the previous unit of the dW batch, whose
@@ -112,9 +132,10 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int nm_stride, float* t_out, int t_stride, int V,
                                const SampleMeta* prev, const DxPlan& plan, hipStream_t s);
 // x / hidden of row r is x + (row_seq[r] / B) * stride (the row's sample in the unit)
-hipError_t launch_row_rms(const uint16_t* x, int64_t stride, int B, const Workspace& ws, int d,
-                          float eps, hipStream_t s);
-hipError_t launch_gather(const uint16_t* hidden, int64_t stride, int B, const float* gamma,
+// (f32: x / hidden are fp32, rounded to bf16 as they are read)
+hipError_t launch_row_rms(const void* x, bool f32, int64_t stride, int B, const Workspace& ws,
+                          int d, float eps, hipStream_t s);
+hipError_t launch_gather(const void* hidden, bool f32, int64_t stride, int B, const float* gamma,
                          const Workspace& ws, int d, hipStream_t s);
 hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool store_u,
                            hipStream_t s);
@@ -133,10 +154,20 @@ hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, 
 // dX of sample g of the unit (its rows only; samples of a unit run one after
 // the other, so positions shared between samples are summed in sample order)
 hipError_t launch_dx_reduce(const Workspace& ws, int g, float* dX, int d, hipStream_t s);
-hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const uint16_t* x,
+hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const void* x, bool f32,
                                     const float* gamma, float* dx, float* dgamma, int d,
                                     hipStream_t s);
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s);
+// recompute mode, vocabulary chunk [v0, v0 + width): the chunk's logits from
+// W^T and H_c, turned into dZ = s (softmax - onehot) (bf16, [row][v] and
+// [v][row]); dX^T partials (+)= W[:, chunk] . dZ^T (first chunk: stored);
+// dW[:, chunk] += H_c^T . dZ
+hipError_t launch_gemm_recompute(const Workspace& ws, int d, int v0, int width, int grid,
+                                 hipStream_t s);
+hipError_t launch_gemm_dx_chunk(const Workspace& ws, const uint16_t* W, int d, int V, int v0,
+                                int width, bool first, int grid, hipStream_t s);
+hipError_t launch_gemm_dw_chunk(const Workspace& ws, float* dW, int d, int V, int v0, int width,
+                                int grid, hipStream_t s);
 
 int gemm_grid(int device);  // persistent grid size of the GEMM kernels on `device`
 

@@ -363,9 +363,10 @@ hipError_t launch_dx_reduce(const Workspace& ws, int g, float* dX, int d, hipStr
 //   c_k      = dh_k x_k r  -> part[0][row][k], summed over rows into dgamma
 // Every thread revisits only the elements it wrote, so part[0] needs no
 // cross-thread ordering; the row dot product goes through LDS.
+template <typename T>
 __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
     float* __restrict__ part, const int32_t* __restrict__ idx, const SampleMeta* __restrict__ sm,
-    const SampleMeta* __restrict__ um, const uint16_t* __restrict__ x,
+    const SampleMeta* __restrict__ um, const T* __restrict__ x,
     const float* __restrict__ gamma, const float* __restrict__ inv_rms, float* __restrict__ dx,
     int d, int64_t split_stride) {
   __shared__ float red[4];
@@ -374,7 +375,7 @@ __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
   const int n_split = um->dx_split;
   const int tid = threadIdx.x;
   float* p0 = part + (int64_t)r * d;
-  const uint16_t* xr = x + (int64_t)idx[r] * d;
+  const T* xr = x + (int64_t)idx[r] * d;
   float dot = 0.f;
   for (int c = tid * 4; c < d; c += 1024) {
     float4 acc = *reinterpret_cast<const float4*>(p0 + c);
@@ -383,7 +384,7 @@ __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
       acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
     }
     *reinterpret_cast<float4*>(p0 + c) = acc;
-    const uint2 xv = *reinterpret_cast<const uint2*>(xr + c);
+    const uint2 xv = load_bf16x4(xr + c);
     const float4 g = *reinterpret_cast<const float4*>(gamma + c);
     dot = fmaf(g.x * acc.x, __uint_as_float(xv.x << 16), dot);
     dot = fmaf(g.y * acc.y, __uint_as_float(xv.x & 0xFFFF0000u), dot);
@@ -400,7 +401,7 @@ __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
   float* dxr = dx + (int64_t)idx[r] * d;
   for (int c = tid * 4; c < d; c += 1024) {
     const float4 dh = *reinterpret_cast<const float4*>(p0 + c);
-    const uint2 xv = *reinterpret_cast<const uint2*>(xr + c);
+    const uint2 xv = load_bf16x4(xr + c);
     const float4 g = *reinterpret_cast<const float4*>(gamma + c);
     const float x0 = __uint_as_float(xv.x << 16), x1 = __uint_as_float(xv.x & 0xFFFF0000u);
     const float x2 = __uint_as_float(xv.y << 16), x3 = __uint_as_float(xv.y & 0xFFFF0000u);
@@ -441,12 +442,18 @@ __global__ __launch_bounds__(256) void k_dgamma_final(const float* __restrict__ 
   dgamma[k] += acc;
 }
 
-hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const uint16_t* x,
+hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const void* x, bool f32,
                                     const float* gamma, float* dx, float* dgamma, int d,
                                     hipStream_t s) {
   const SampleMeta* sm = ws.meta + g;
-  k_dx_reduce_rmsnorm<<<(unsigned)ws.NP, 256, 0, s>>>(ws.dx_part, ws.idx, sm, ws.unit(), x, gamma,
-                                                     ws.inv_rms, dx, d, ws.RP * d);
+  if (f32)
+    k_dx_reduce_rmsnorm<float><<<(unsigned)ws.NP, 256, 0, s>>>(
+        ws.dx_part, ws.idx, sm, ws.unit(), static_cast<const float*>(x), gamma, ws.inv_rms, dx, d,
+        ws.RP * d);
+  else
+    k_dx_reduce_rmsnorm<uint16_t><<<(unsigned)ws.NP, 256, 0, s>>>(
+        ws.dx_part, ws.idx, sm, ws.unit(), static_cast<const uint16_t*>(x), gamma, ws.inv_rms, dx,
+        d, ws.RP * d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 g1((unsigned)((d + 255) / 256), (unsigned)(ws.NP / 256));

@@ -204,7 +204,8 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
 // RMSNorm h = gamma x r, r = (mean x^2 + eps)^(-1/2)): one wave per row, fp32
 // sum of squares.  Row r of the unit reads sample g = row_seq[r] / B, i.e.
 // x + g * stride.
-__global__ __launch_bounds__(256) void k_row_rms(const uint16_t* __restrict__ x, int64_t stride,
+template <typename T>
+__global__ __launch_bounds__(256) void k_row_rms(const T* __restrict__ x, int64_t stride,
                                                  int B, const int32_t* __restrict__ idx,
                                                  const int32_t* __restrict__ row_seq,
                                                  const SampleMeta* __restrict__ meta,
@@ -212,10 +213,10 @@ __global__ __launch_bounds__(256) void k_row_rms(const uint16_t* __restrict__ x,
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= meta->n_rows) return;
-  const uint16_t* xr = x + (int64_t)(row_seq[row] / B) * stride + (int64_t)idx[row] * d;
+  const T* xr = x + (int64_t)(row_seq[row] / B) * stride + (int64_t)idx[row] * d;
   float acc = 0.f;
   for (int k = lane * 8; k < d; k += 64 * 8) {
-    const uint4 v = *reinterpret_cast<const uint4*>(xr + k);
+    const uint4 v = load_bf16x8(xr + k);
     const uint32_t a[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -229,10 +230,15 @@ __global__ __launch_bounds__(256) void k_row_rms(const uint16_t* __restrict__ x,
   if (lane == 0) inv_rms[row] = 1.f / sqrtf(acc / (float)d + eps);
 }
 
-hipError_t launch_row_rms(const uint16_t* x, int64_t stride, int B, const Workspace& ws, int d,
-                          float eps, hipStream_t s) {
-  k_row_rms<<<(unsigned)(ws.RP / 4), 256, 0, s>>>(x, stride, B, ws.idx, ws.row_seq, ws.unit(),
-                                                  ws.inv_rms, d, eps);
+hipError_t launch_row_rms(const void* x, bool f32, int64_t stride, int B, const Workspace& ws,
+                          int d, float eps, hipStream_t s) {
+  const unsigned grid = (unsigned)(ws.RP / 4);
+  if (f32)
+    k_row_rms<float><<<grid, 256, 0, s>>>(static_cast<const float*>(x), stride, B, ws.idx,
+                                          ws.row_seq, ws.unit(), ws.inv_rms, d, eps);
+  else
+    k_row_rms<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(x), stride, B, ws.idx,
+                                             ws.row_seq, ws.unit(), ws.inv_rms, d, eps);
   return hipGetLastError();
 }
 
@@ -241,8 +247,10 @@ hipError_t launch_row_rms(const uint16_t* x, int64_t stride, int B, const Worksp
 // stride); zeros for N <= r < N_pad.  64x64 tiles staged in LDS for the
 // transposed copy.  With `gamma`, `hidden` holds the pre-norm activations and
 // the gathered row is the final RMSNorm bf16(x * inv_rms[r] * gamma) (fp32
-// arithmetic, one rounding to bfloat16).
-__global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hidden,
+// arithmetic, one rounding to bfloat16).  fp32 inputs are rounded to bf16
+// first (load_bf16x8), then treated the same way.
+template <typename T>
+__global__ __launch_bounds__(256) void k_gather(const T* __restrict__ hidden,
                                                 int64_t stride, int B,
                                                 const int32_t* __restrict__ idx,
                                                 const int32_t* __restrict__ row_seq,
@@ -265,8 +273,8 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
     const int r = r0 + row;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (r < N) {
-      const uint16_t* src = hidden + (int64_t)(row_seq[r] / B) * stride + (int64_t)idx[r] * d;
-      v = *reinterpret_cast<const uint4*>(src + c0 + ch * 8);
+      const T* src = hidden + (int64_t)(row_seq[r] / B) * stride + (int64_t)idx[r] * d;
+      v = load_bf16x8(src + c0 + ch * 8);
       if (gamma) {
         const float ir = inv_rms[r];
         const float4 g0 = *reinterpret_cast<const float4*>(gamma + c0 + ch * 8);
@@ -298,18 +306,28 @@ __global__ __launch_bounds__(256) void k_gather(const uint16_t* __restrict__ hid
   }
 }
 
-hipError_t launch_gather(const uint16_t* hidden, int64_t stride, int B, const float* gamma,
+hipError_t launch_gather(const void* hidden, bool f32, int64_t stride, int B, const float* gamma,
                          const Workspace& ws, int d, hipStream_t s) {
   dim3 grid((unsigned)(ws.RP / 64), (unsigned)(d / 64));
-  k_gather<<<grid, 256, 0, s>>>(hidden, stride, B, ws.idx, ws.row_seq, ws.unit(), gamma,
-                                ws.inv_rms, ws.Hc, ws.HcT, d, ws.KT);
+  if (f32)
+    k_gather<float><<<grid, 256, 0, s>>>(static_cast<const float*>(hidden), stride, B, ws.idx,
+                                         ws.row_seq, ws.unit(), gamma, ws.inv_rms, ws.Hc, ws.HcT,
+                                         d, ws.KT);
+  else
+    k_gather<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(hidden), stride, B,
+                                            ws.idx, ws.row_seq, ws.unit(), gamma, ws.inv_rms,
+                                            ws.Hc, ws.HcT, d, ws.KT);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// W_head [d, V] -> WT [V, d], 64x64 tiles through LDS.
-__global__ __launch_bounds__(256) void k_transpose_w(const uint16_t* __restrict__ W,
-                                                     uint16_t* __restrict__ WT, int d, int V) {
+// W_head [d, V] -> WT [V, d], 64x64 tiles through LDS.  fp32 W is rounded to
+// bf16 as it is read, and the rounded rows also go to Wb [d, V] (the dX GEMM's
+// operand).
+template <typename T>
+__global__ __launch_bounds__(256) void k_transpose_w(const T* __restrict__ W,
+                                                     uint16_t* __restrict__ WT,
+                                                     uint16_t* __restrict__ Wb, int d, int V) {
   __shared__ uint16_t tile[64][72];
   const int v0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
   const int tid = threadIdx.x;
@@ -317,8 +335,9 @@ __global__ __launch_bounds__(256) void k_transpose_w(const uint16_t* __restrict_
   for (int it = 0; it < 2; ++it) {
     const int q = tid + it * 256;
     const int kr = q >> 3, ch = q & 7;
-    *reinterpret_cast<uint4*>(&tile[kr][ch * 8]) =
-        *reinterpret_cast<const uint4*>(W + (int64_t)(k0 + kr) * V + v0 + ch * 8);
+    const uint4 v = load_bf16x8(W + (int64_t)(k0 + kr) * V + v0 + ch * 8);
+    *reinterpret_cast<uint4*>(&tile[kr][ch * 8]) = v;
+    if (Wb) *reinterpret_cast<uint4*>(Wb + (int64_t)(k0 + kr) * V + v0 + ch * 8) = v;
   }
   __syncthreads();
 #pragma unroll
@@ -334,9 +353,14 @@ __global__ __launch_bounds__(256) void k_transpose_w(const uint16_t* __restrict_
   }
 }
 
-hipError_t launch_transpose_w(const uint16_t* W, uint16_t* WT, int d, int V, hipStream_t s) {
+hipError_t launch_transpose_w(const void* W, bool f32, uint16_t* WT, uint16_t* Wb, int d, int V,
+                              hipStream_t s) {
   dim3 grid((unsigned)(V / 64), (unsigned)(d / 64));
-  k_transpose_w<<<grid, 256, 0, s>>>(W, WT, d, V);
+  if (f32)
+    k_transpose_w<float><<<grid, 256, 0, s>>>(static_cast<const float*>(W), WT, Wb, d, V);
+  else
+    k_transpose_w<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(W), WT, nullptr, d,
+                                                 V);
   return hipGetLastError();
 }
 

@@ -49,8 +49,9 @@ def _prob(b, **kw):
 
 
 def test_status_strings(b):
-    for s in (0, -1, -2, -3, -4):
+    for s in (0, -1, -2, -3, -4, -5):
         assert b._lib.bgpo_status_string(s)
+    assert b"budget" in b._lib.bgpo_status_string(-5)
     assert b"unknown" in b._lib.bgpo_status_string(-99)
 
 
@@ -66,6 +67,10 @@ def test_workspace_independent_of_n_t(b):
     (dict(j_begin=-1), -1), (dict(j_begin=60, j_count=5), -1), (dict(t_mode=2), -1),
     (dict(bound=4), -1), (dict(sample_stride=-8), -1), (dict(sample_stride=12), -1),
     (dict(norm_eps=float("nan")), -1), (dict(norm_eps=-1.0), -1),
+    (dict(in_dtype=2), -1), (dict(in_dtype=-1), -1), (dict(vocab_chunk=100), -1),
+    (dict(vocab_chunk=-256), -1), (dict(ws_budget=1 << 20), -5),
+    (dict(bound=3, retain_samples=1, vocab_chunk=256), -1),
+    (dict(bound=3, retain_samples=1, ws_budget=1 << 40), -1),
 ])
 def test_problem_validation(b, kw, status):
     with pytest.raises(b.BgpoError) as e:
@@ -115,12 +120,20 @@ def test_null_pointers_and_workspace_rejected_before_hip(b):
 
 
 def test_problem_struct_layout(b):
-    # matches the C struct: 8 int32, uint64, uint32, int32, int64, float, int32 = 64 bytes
-    assert ctypes.sizeof(b._Problem) == 64
+    # matches the C struct: 8 int32, uint64, uint32, int32, int64, float, 3 int32, uint64
+    assert ctypes.sizeof(b._Problem) == 80
     assert b._Problem.seed.offset == 32
     assert b._Problem.bound.offset == 44
     assert b._Problem.sample_stride.offset == 48
     assert b._Problem.norm_eps.offset == 56
+    assert b._Problem.retain_samples.offset == 60
+    assert b._Problem.in_dtype.offset == 64
+    assert b._Problem.vocab_chunk.offset == 68
+    assert b._Problem.ws_budget.offset == 72
+    src = open(os.path.join(ROOT, "include", "bgpo.h")).read()
+    src = src[src.index("typedef struct bgpo_problem {"):src.index("} bgpo_problem;")]
+    fields = re.findall(r"^\s+(?:int32_t|uint64_t|uint32_t|int64_t|float)\s+(\w+);", src, flags=re.M)
+    assert [f for f in fields if f in dict(b._Problem._fields_)] == [n for n, _ in b._Problem._fields_]
 
 
 def test_retained_workspace_grows_linearly_with_n_t(b):
@@ -155,11 +168,11 @@ def test_every_entry_point_lays_out_what_it_checked(b):
         assert lib.bgpo_elbo_fwd(ctypes.byref(pr), fake, fake, fake, fake, fake, fake, None, ws,
                                  n.value - 1, None, None) == -2
     src = open(os.path.join(ROOT, "paper_2510_11683_amd", "csrc", "api.hip")).read()
-    # every layout call that sits next to a checked workspace uses the problem's flag or the
-    # retained / constant layout of its own branch
+    # every layout call lays out a plan (the one plan_problem chose for the
+    # problem, which check_workspace measured), never a layout of its own
     calls = re.findall(r"workspace_layout\(([^;]*)\);", src)
-    assert all("retain_samples" in c or ", 1," in c or ", 0," in c for c in calls), calls
-    assert any("prob->retain_samples, workspace" in c for c in calls)
+    assert calls and all(re.search(r"(^|, )\*?pl, ", c) for c in calls), calls
+    assert src.count("plan_problem(prob, &pl)") >= 4
 
 
 def test_reserved_field_and_rmsnorm_arguments_rejected_before_hip(b):
@@ -198,3 +211,70 @@ def test_retained_rows_bounded_by_the_dw_panel_range(b):
             b.bgpo_workspace_size(_prob(b, n_t=n_t, retain_samples=1, **big))
         assert e.value.status == -4
     assert b.bgpo_workspace_size(_prob(b, n_t=1000, **big)) == b.bgpo_workspace_size(_prob(b, n_t=1, **big))
+
+
+GiB = 1 << 30
+
+
+def test_budget_picks_layouts_that_fit(b):
+    """A workspace budget selects the largest stored-exponential layout that
+    fits, and below that the recompute layout; the chosen size never exceeds
+    the budget and never depends on n_t; a budget below the smallest layout is
+    refused with BGPO_ERR_BUDGET."""
+    full = b.bgpo_workspace_size(_prob(b))
+    assert full > 29 * GiB                                  # default: stored, units of 8
+    sizes = {}
+    for budget in (2, 3, 4, 6, 8, 16, 24, 32, 64):
+        sz = b.bgpo_workspace_size(_prob(b, ws_budget=budget * GiB))
+        assert sz <= budget * GiB
+        assert {b.bgpo_workspace_size(_prob(b, n_t=n, ws_budget=budget * GiB)) for n in (1, 4, 16, 64)} == {sz}
+        sizes[budget] = sz
+    assert sizes[64] == full or sizes[64] <= 64 * GiB
+    # monotone: a larger budget never gives a smaller layout here
+    vals = [sizes[k] for k in sorted(sizes)]
+    assert vals == sorted(vals)
+    # the smallest layouts hold the transposed head (2 d V bytes) and little else
+    dV2 = 2 * 4096 * 126464
+    assert dV2 < sizes[2] <= 2 * GiB
+    with pytest.raises(b.BgpoError) as e:
+        b.bgpo_workspace_size(_prob(b, ws_budget=dV2))
+    assert e.value.status == b.BGPO_ERR_BUDGET
+
+
+def test_forced_vocab_chunk_and_fp32_copy(b):
+    """vocab_chunk > 0 forces the recompute layout (much smaller than the
+    stored one at the same unit size); fp32 inputs add a bf16 copy of W."""
+    stored = b.bgpo_workspace_size(_prob(b))
+    chunked = b.bgpo_workspace_size(_prob(b, vocab_chunk=8192))
+    assert chunked < stored / 4
+    small = dict(B=2, L=64, d=128, V=1024, n_t=4)
+    w16 = b.bgpo_workspace_size(_prob(b, **small))
+    w32 = b.bgpo_workspace_size(_prob(b, in_dtype=b.BGPO_F32, **small))
+    assert w32 - w16 >= 2 * 128 * 1024
+    # a chunk wider than the vocabulary is the whole vocabulary
+    assert (b.bgpo_workspace_size(_prob(b, vocab_chunk=4096, **small)) ==
+            b.bgpo_workspace_size(_prob(b, vocab_chunk=1024, **small)))
+
+
+def test_ell_old_aliasing_rejected_before_hip(b):
+    """l is written before l_old is read, so ell_old overlapping ell or g is
+    refused (BGPO_ERR_INVALID_ARG) before anything is enqueued; disjoint
+    buffers pass that check (and here fail the workspace check instead)."""
+    p = _prob(b, B=2, L=64, d=128, V=1024, n_t=4).c()
+    lib = b._lib
+    n = ctypes.c_size_t(0)
+    assert lib.bgpo_workspace_size(ctypes.byref(p), ctypes.byref(n)) == 0
+    fake = ctypes.c_void_p(0x1000)
+    ws = ctypes.c_void_p(0x100000)
+    ell, g = 0x200000, 0x300000
+    nbytes = 2 * 4 * 8
+
+    def call(ell_old):
+        return lib.bgpo_elbo_bwd_accumulate(ctypes.byref(p), fake, fake, fake, fake, fake,
+                                            ctypes.c_void_p(ell_old), 0.125, fake, fake,
+                                            ctypes.c_void_p(ell), ctypes.c_void_p(g), fake, fake,
+                                            None, None, ws, n.value - 1, None, None)
+    for eo in (ell, ell + 8, ell - nbytes + 8, g, g + nbytes - 8):
+        assert call(eo) == -1, hex(eo)
+    for eo in (ell + nbytes, ell - nbytes, 0x400000):
+        assert call(eo) == -2, hex(eo)

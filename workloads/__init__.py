@@ -112,7 +112,8 @@ def _chunked(seed_seq, n_rows, fill, rows=_CHUNK_ROWS):
         list(ex.map(lambda a: fill(*a), jobs))
 
 
-def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True) -> dict:
+def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True,
+             keep_f32: bool = False) -> dict:
     """Draw every input of workload ``w`` from numpy PCG64 streams spawned from
     ``w.data_seed`` (one stream per input, so W or hidden can be skipped).
 
@@ -122,7 +123,9 @@ def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True
       targets   int32  [B, L]     target token per position (defined on padding too)
       resp_mask uint8  [B, L]     1 on response positions, 0 on padding
       adv       float32 [B]       per-response advantage
-    plus ``lengths`` (int32 [B]).
+    plus ``lengths`` (int32 [B]).  ``keep_f32`` also returns the float32
+    values before rounding as ``hidden_f32`` [B, L, d] and ``W_f32`` [d, V]
+    (the rounded bits are those values rounded to nearest even).
     """
     # independent streams per input, so that any subset can be drawn alone
     ss = np.random.SeedSequence(w.data_seed).spawn(5)
@@ -130,6 +133,8 @@ def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True
     B, L, d, V = w.B, w.L, w.d, w.V
 
     hidden = None
+    hidden_f32 = np.empty((B * L, d), dtype=np.float32) if (with_hidden and keep_f32) else None
+    W_f32 = np.empty((d, V), dtype=np.float32) if (with_weights and keep_f32) else None
     if with_hidden:
         hidden = np.empty((B * L, d), dtype=np.uint16)
 
@@ -139,6 +144,8 @@ def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True
                 rms = np.sqrt(np.mean(h.astype(np.float64) ** 2, axis=-1, keepdims=True) + 1e-6)
                 h = (h / rms).astype(np.float32)
             hidden[c:c + h.shape[0]] = f32_to_bf16_bits(h).reshape(h.shape)
+            if hidden_f32 is not None:
+                hidden_f32[c:c + h.shape[0]] = h
 
         _chunked(ss[0], B * L, fill_h)
         hidden = hidden.reshape(B, L, d)
@@ -152,6 +159,8 @@ def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True
             n = min(d, c + rows) - c
             chunk = rng.standard_normal((n, V), dtype=np.float32) * np.float32(w.w_std)
             W[c:c + n] = f32_to_bf16_bits(chunk).reshape(n, V)
+            if W_f32 is not None:
+                W_f32[c:c + n] = chunk
 
         _chunked(ss[1], d, fill_w, rows)
 
@@ -178,8 +187,12 @@ def generate(w: Workload, *, with_weights: bool = True, with_hidden: bool = True
     else:
         adv = r.astype(np.float32)
 
-    return dict(hidden=hidden, W=W, targets=targets, resp_mask=resp_mask, adv=adv,
-                lengths=lengths)
+    out = dict(hidden=hidden, W=W, targets=targets, resp_mask=resp_mask, adv=adv,
+               lengths=lengths)
+    if keep_f32:
+        out["hidden_f32"] = None if hidden_f32 is None else hidden_f32.reshape(B, L, d)
+        out["W_f32"] = W_f32
+    return out
 
 
 def pre_norm_activations(w: Workload, n_samples: int = 0) -> np.ndarray:
