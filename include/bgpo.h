@@ -50,7 +50,8 @@
  *     that were passed at capture time.
  *   - Host-detectable errors return a negative bgpo_status before anything is
  *     enqueued; HIP launch errors return BGPO_ERR_HIP.  No C++ exception
- *     crosses the ABI.  Entry points keep no mutable global state; calls on
+ *     crosses the ABI.  Entry points keep no mutable global state (except
+ *     the static scratch of bgpo_elbo_bwd_accumulate_noalloc); calls on
  *     different streams must not share a workspace.
  *   - hidden (or x) and W_head are row-major; their element type is
  *     prob->in_dtype: bfloat16 bit patterns (uint16, BGPO_BF16) or float32
@@ -294,6 +295,32 @@ int bgpo_elbo_bwd_accumulate(const bgpo_problem* prob, const void* hidden,
                              int32_t* n_masked, float* t_out, int32_t* status_flags,
                              void* workspace, size_t ws_bytes, void* stream,
                              bgpo_timing* prof);
+
+/* bgpo_elbo_bwd_accumulate without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  The workspace is a static device
+ * array of bgpo_noalloc_scratch_bytes() bytes (128 MiB) inside the library,
+ * one per device, held until the process ends; the call allocates nothing.
+ * The layout is the one bgpo_workspace_size gives for `prob` with ws_budget
+ * set to the scratch size (or to prob->ws_budget if that is smaller), so the
+ * results are bit-identical to bgpo_elbo_bwd_accumulate with that budget.
+ * Problems whose smallest layout exceeds the scratch return BGPO_ERR_BUDGET
+ * before anything is enqueued (at the LLaDA head shape the transposed head
+ * alone is 1 GB, so only smaller heads fit); retain_samples = 1 returns
+ * BGPO_ERR_INVALID_ARG.  Every call on a device shares that device's array:
+ * calls that overlap in time on one device (other streams, other threads)
+ * race and must be serialised by the caller.  No state carries over from one
+ * call to the next (every kernel writes the scratch it reads). */
+int bgpo_elbo_bwd_accumulate_noalloc(const bgpo_problem* prob, const void* hidden,
+                                     const void* W_head, const int32_t* targets,
+                                     const uint8_t* resp_mask, const float* adv,
+                                     const double* ell_old, double loss_scale, float* dX,
+                                     float* dW, double* ell, double* g, double* loss,
+                                     int32_t* n_masked, float* t_out, int32_t* status_flags,
+                                     void* stream);
+
+/* Size in bytes of the static scratch array of bgpo_elbo_bwd_accumulate_noalloc. */
+size_t bgpo_noalloc_scratch_bytes(void);
 
 /* The same two calls with the final RMSNorm of the mask predictor fused in
  * front of the LM head: the head input of a position is

@@ -79,6 +79,11 @@ def _load():
     lib.bgpo_elbo_bwd_accumulate_rmsnorm.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp, vp,
                                                      ctypes.c_double, vp, vp, vp, vp, vp, vp, vp,
                                                      vp, vp, vp, sz, vp, P(Timing)]
+    lib.bgpo_elbo_bwd_accumulate_noalloc.argtypes = [P(_Problem), vp, vp, vp, vp, vp, vp,
+                                                     ctypes.c_double, vp, vp, vp, vp, vp, vp, vp,
+                                                     vp, vp]
+    lib.bgpo_noalloc_scratch_bytes.restype = sz
+    lib.bgpo_noalloc_scratch_bytes.argtypes = []
     lib.bgpo_moments_update.argtypes = [vp, vp, vp, ctypes.c_int64, i32, vp]
     lib.bgpo_moments_workspace_size.restype = sz
     lib.bgpo_moments_workspace_size.argtypes = []
@@ -86,7 +91,7 @@ def _load():
     lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
     lib.bgpo_test_gemm_split.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp]
     for f in ("bgpo_workspace_size", "bgpo_workspace_plan", "bgpo_sample_masks", "bgpo_elbo_fwd",
-              "bgpo_elbo_bwd_accumulate", "bgpo_elbo_fwd_rmsnorm",
+              "bgpo_elbo_bwd_accumulate", "bgpo_elbo_bwd_accumulate_noalloc", "bgpo_elbo_fwd_rmsnorm",
               "bgpo_elbo_bwd_accumulate_rmsnorm", "bgpo_moments_update", "bgpo_moments_summary",
               "bgpo_test_gemm_nt", "bgpo_test_gemm_split"):
         getattr(lib, f).restype = ctypes.c_int
@@ -248,6 +253,32 @@ def bgpo_elbo_bwd_accumulate(prob: Problem, hidden, W_head, targets, resp_mask, 
         _ptr(status_flags, "status_flags", (torch.int32,), (1,), allow_none=True),
         _ptr(workspace, "workspace", (torch.uint8,)), workspace.numel(), _stream(stream),
         ctypes.byref(timing) if timing is not None else None), "bgpo_elbo_bwd_accumulate")
+
+
+def bgpo_elbo_bwd_accumulate_noalloc(prob: Problem, hidden, W_head, targets, resp_mask, adv,
+                                     ell_old, loss_scale: float, dX, dW, ell, g, loss, n_masked,
+                                     t_out, status_flags, stream=None):
+    """bgpo_elbo_bwd_accumulate on the library's static scratch (no workspace)."""
+    B, L, d, V, nt = prob.B, prob.L, prob.d, prob.V, prob.n_t
+    _check(_lib.bgpo_elbo_bwd_accumulate_noalloc(
+        ctypes.byref(prob.c()), _ptr(hidden, "hidden", _in_types(prob), _act_shape(prob)),
+        _ptr(W_head, "W_head", _in_types(prob), (d, V)),
+        _ptr(targets, "targets", (torch.int32,), (B, L)),
+        _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)),
+        _ptr(adv, "adv", (torch.float32,), (B,)),
+        _ptr(ell_old, "ell_old", (torch.float64,), (B, nt), allow_none=True),
+        float(loss_scale),
+        _ptr(dX, "dX", (torch.float32,), _act_shape(prob)), _ptr(dW, "dW", (torch.float32,), (d, V)),
+        _ptr(ell, "ell", (torch.float64,), (B, nt)), _ptr(g, "g", (torch.float64,), (B, nt)),
+        _ptr(loss, "loss", (torch.float64,), (1,)),
+        _ptr(n_masked, "n_masked", (torch.int32,), (B, nt)),
+        _ptr(t_out, "t_out", (torch.float32,), (B, nt), allow_none=True),
+        _ptr(status_flags, "status_flags", (torch.int32,), (1,), allow_none=True),
+        _stream(stream)), "bgpo_elbo_bwd_accumulate_noalloc")
+
+
+def bgpo_noalloc_scratch_bytes() -> int:
+    return int(_lib.bgpo_noalloc_scratch_bytes())
 
 
 def bgpo_elbo_fwd_rmsnorm(prob: Problem, x, norm_weight, W_head, targets, resp_mask, ell,

@@ -24,6 +24,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "../../include/bgpo.h"
@@ -776,3 +777,56 @@ int bgpo_elbo_bwd_accumulate_rmsnorm(const bgpo_problem* prob, const void* x,
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The backward without a caller workspace: its workspace is a static device
+// array of kScratchBytes (each device the library runs on holds its own copy
+// until the process ends).  The array's name is a host-side stand-in, so the
+// device address of each device's copy is looked up once, with that device
+// current, and only that address is handed to the kernels.
+namespace bgpo {
+
+constexpr size_t kScratchBytes = size_t(128) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];
+
+// device address of the current device's scratch array (NULL on failure)
+static void* scratch_of_current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace bgpo
+
+extern "C" size_t bgpo_noalloc_scratch_bytes(void) { return bgpo::kScratchBytes; }
+
+extern "C" int bgpo_elbo_bwd_accumulate_noalloc(
+    const bgpo_problem* prob, const void* hidden, const void* W_head, const int32_t* targets,
+    const uint8_t* resp_mask, const float* adv, const double* ell_old, double loss_scale,
+    float* dX, float* dW, double* ell, double* g, double* loss, int32_t* n_masked, float* t_out,
+    int32_t* status_flags, void* stream) {
+  using namespace bgpo;
+  if (!prob) return BGPO_ERR_INVALID_ARG;
+  if (prob->retain_samples) return BGPO_ERR_INVALID_ARG;   // memory grows with n_t
+  // the problem's layout within the scratch array: its own budget if smaller
+  bgpo_problem p = *prob;
+  if (p.ws_budget == 0 || p.ws_budget > kScratchBytes) p.ws_budget = kScratchBytes;
+  Plan pl;
+  const int st = plan_problem(&p, &pl);
+  if (st != BGPO_OK) return st;   // BGPO_ERR_BUDGET: the problem needs more than the scratch
+  void* ws = scratch_of_current_device();
+  if (!ws) return BGPO_ERR_HIP;
+  return elbo_bwd_impl(&p, act_of(&p, hidden, nullptr), W_head, targets, resp_mask, adv, ell_old,
+                       loss_scale, dX, nullptr, dW, ell, g, loss, n_masked, t_out, status_flags,
+                       ws, kScratchBytes, stream, nullptr);
+}

@@ -278,3 +278,23 @@ def test_ell_old_aliasing_rejected_before_hip(b):
         assert call(eo) == -1, hex(eo)
     for eo in (ell + nbytes, ell - nbytes, 0x400000):
         assert call(eo) == -2, hex(eo)
+
+
+def test_noalloc_refuses_problems_beyond_its_scratch_before_hip(b):
+    """The allocation-free backward plans the problem within its static
+    scratch (128 MiB): a problem whose smallest layout is larger (the LLaDA
+    head: W^T alone is 1 GB) is refused with BGPO_ERR_BUDGET, a retained-state
+    problem with BGPO_ERR_INVALID_ARG, before any HIP call."""
+    lib = b._lib
+    assert b.bgpo_noalloc_scratch_bytes() == 128 << 20
+    fake = ctypes.c_void_p(0x1000)
+
+    def call(p):
+        return lib.bgpo_elbo_bwd_accumulate_noalloc(ctypes.byref(p.c()), *([fake] * 6), 0.125,
+                                                    *([fake] * 8), None)
+    assert call(_prob(b)) == b.BGPO_ERR_BUDGET
+    assert call(_prob(b, bound=3, retain_samples=1, B=2, L=64, d=128, V=1024, n_t=4)) == -1
+    assert call(_prob(b, B=0)) == -1
+    # a small problem fits the scratch: its plan under that budget exists
+    small = _prob(b, B=4, L=200, d=576, V=4288, n_t=3, ws_budget=128 << 20)
+    assert b.bgpo_workspace_plan(small)["workspace_bytes"] <= 128 << 20
