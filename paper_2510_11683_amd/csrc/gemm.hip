@@ -166,37 +166,44 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   int64_t k_split = p.k_split;
   if (p.dyn_split) {
     n_split = p.meta->dx_split;
-    k_split = (int64_t)p.meta->dx_kslab * 64;   // 64-wide slabs: nk even for BK 32
+    k_split = (int64_t)p.meta->dx_kslab * 64;   // whole 64-deep slabs
   }
   if (EPI == EPI_F32_ACCUM && K == 0) return;   // nothing to add
-  const int tilesM = (M + BM - 1) / BM, tilesN = (N + BN - 1) / BN;
-  const int64_t total = (int64_t)tilesM * tilesN * n_split;
-  const int G = gridDim.x;
-  const int w = blockIdx.x;
-  const int xcd_slot = G % 8 == 0 ? (w % 8) * (G / 8) + w / 8 : w;
+  // The tile walk in 32-bit wave-uniform (scalar) arithmetic: tile counts
+  // stay below 2^30 for every launch (tiles of M and N below 2^12 and 2^14,
+  // at most 16 splits; the test hook checks its own).
+  const uint32_t tilesM = __builtin_amdgcn_readfirstlane((M + BM - 1) / BM);
+  const uint32_t tilesN = __builtin_amdgcn_readfirstlane((N + BN - 1) / BN);
+  const uint32_t per_split = tilesM * tilesN;
+  const uint32_t total = __builtin_amdgcn_readfirstlane(per_split * (uint32_t)n_split);
+  const uint32_t GM = __builtin_amdgcn_readfirstlane(max(1, min(p.group_m, (int)tilesM)));
+  const uint32_t band_tiles = GM * tilesN;
+  const uint32_t G = gridDim.x;
+  const uint32_t w = blockIdx.x;
+  const uint32_t xcd_slot = G % 8 == 0 ? (w % 8) * (G / 8) + w / 8 : w;
 
-  for (int64_t base = 0; base < total; base += G) {
-    const int64_t t = base + xcd_slot;
-    if (t >= total) continue;
-    // the lane index, re-derived every tile: addresses computed from it are
-    // then not hoisted out of the tile loop (with all 256 AGPRs holding
-    // accumulators, such hoisted values would be spilled)
-    int lane_t = tid & 63;
-    asm volatile("" : "+v"(lane_t));
+  for (uint32_t t = xcd_slot; t < total; t += G) {
+    // the lane index, recomputed every tile from the execution mask (volatile
+    // asm, so neither it nor the addresses formed from it are hoisted out of
+    // the tile loop: with all 256 AGPRs holding accumulators, hoisted values
+    // are spilled, and their reload at the loop head waits for every
+    // outstanding store of the previous tile)
+    int lane_t;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane_t));
     const int lane = lane_t;
     int mt, nt, split;
     {
       // bands of GM M tiles walk along N: 32 consecutive tiles (one XCD's
       // share of a round) cover GM M tiles x 32 / GM N tiles
-      const int64_t per_split = (int64_t)tilesM * tilesN;
-      split = (int)(t / per_split);
-      const int64_t r = t - (int64_t)split * per_split;
-      const int GM = max(1, min(p.group_m, tilesM));
-      const int64_t band = r / ((int64_t)GM * tilesN);
-      const int gm = min(GM, tilesM - (int)band * GM);
-      const int64_t idx = r - band * GM * tilesN;
-      mt = (int)band * GM + (int)(idx % gm);
-      nt = (int)(idx / gm);
+      const uint32_t sp = __builtin_amdgcn_readfirstlane(t / per_split);
+      const uint32_t r = t - sp * per_split;
+      const uint32_t band = __builtin_amdgcn_readfirstlane(r / band_tiles);
+      const uint32_t gm = min(GM, tilesM - band * GM);
+      const uint32_t idx = r - band * band_tiles;
+      const uint32_t q = __builtin_amdgcn_readfirstlane(idx / gm);
+      split = (int)sp;
+      mt = (int)(band * GM + (idx - q * gm));
+      nt = (int)q;
     }
     const int m0 = mt * BM, n0 = nt * BN;
     const int64_t kb = (int64_t)split * k_split;
@@ -368,6 +375,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // one 16-row column block of the wave tile at a time, so that only its
       // 32 values per lane are live outside the accumulators
       const int vt = mw / WM;
+      // the wave's partial rows (vt is wave-uniform: a scalar base, 32-bit
+      // per-lane offsets)
+      float* const pm = p.part_m + (int64_t)vt * p.ldp;
+      float* const ps = p.part_s + (int64_t)vt * p.ldp;
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         float mx = -INFINITY;
@@ -400,8 +411,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         st += __shfl_xor(st, 32, 64);
         const int n = n0 + nl;
         if (lane < 16 && mw < M && n < n_valid) {
-          p.part_m[(int64_t)vt * p.ldp + n] = mref;
-          p.part_s[(int64_t)vt * p.ldp + n] = st;
+          pm[(uint32_t)n] = mref;
+          ps[(uint32_t)n] = st;
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -642,6 +653,7 @@ extern "C" int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C,
                                  int32_t K, void* stream) {
   using namespace bgpo;
   if (!A || !B || !C || M <= 0 || N <= 0 || K <= 0 || K % 64) return -1;
+  if ((int64_t)((M + 255) / 256) * ((N + 255) / 256) >= (int64_t(1) << 30)) return -1;
   // the production kernel stores C^T of its operands' product: swap them
   GemmParams p = base_params();
   p.A = B; p.lda = K; p.B = A; p.ldb = K;
@@ -659,6 +671,7 @@ extern "C" int bgpo_test_gemm_split(const uint16_t* A, const uint16_t* B, float*
   using namespace bgpo;
   if (!A || !B || !C || M <= 0 || N <= 0 || K <= 0 || K % 64 || n_split < 1 || n_split > 255)
     return -1;
+  if ((int64_t)((M + 255) / 256) * ((N + 255) / 256) * n_split >= (int64_t(1) << 30)) return -1;
   // slice s covers K range [s * ks, min(K, (s + 1) * ks)) with ks a multiple
   // of 64; trailing slices can be empty (their block is stored as zeros)
   GemmParams p = base_params();
