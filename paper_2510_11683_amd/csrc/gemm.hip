@@ -162,6 +162,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   if (p.dyn_m) { M = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_n) { N = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_k) K = p.meta->col_end;    // batched dW: all samples' columns (multiple of 64)
+  // first dZ^T column of the unit (EPI_DZ), read once into a scalar register
+  const int zt_col = EPI == EPI_DZ ? __builtin_amdgcn_readfirstlane(p.meta->col_off) : 0;
   int n_split = p.n_split;
   int64_t k_split = p.k_split;
   if (p.dyn_split) {
@@ -490,14 +492,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // dZ^T: lane l of an instruction takes vocabulary row ml = 64 k + l of
       // the tile (64 lanes read 128 contiguous bytes of one staged row: no
       // bank conflicts), wave w the 8-row chunks 8 w .. 8 w + 7; each lane
-      // assembles 8 consecutive rows into one 16-byte store
-      uint16_t* zt = p.dZT + p.meta->col_off + n0;
+      // assembles 8 consecutive rows into one 16-byte store.  Consecutive
+      // stores of a lane fill consecutive 16-byte pieces of the same dZ^T
+      // row, so every 128-byte line is complete after eight of them (wider
+      // per-lane reads that spread a lane's stores over four rows left four
+      // times as many partly written lines open, overflowing the L2).
       int lm = lane;
       asm volatile("" : "+v"(lm));
 #pragma unroll
       for (int k = 0; k < BM / 64; ++k) {
         const int ml = 64 * k + lm;
         const int cw = ((ml >> 3) << 4) + (ml & 7) * 2;   // chunk base (before the XOR) and offset
+        uint16_t* const zt = p.dZT + (int64_t)(m0 + ml) * p.ldzt + zt_col + n0;
+        const bool row_live = m0 + ml < M;
 #pragma unroll
         for (int c = 0; c < ROWS_PER_WAVE / 8; ++c) {
           const int r0 = wave * ROWS_PER_WAVE + 8 * c;
@@ -509,9 +516,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
             const uint32_t b = *reinterpret_cast<const uint16_t*>(stage + rb * 512 + (cw ^ ((rb & 31) << 4)));
             wv[t] = a | (b << 16);
           }
-          if (m0 + ml < M && n0 + r0 < N)
-            *reinterpret_cast<uint4*>(zt + (int64_t)(m0 + ml) * p.ldzt + r0) =
-                make_uint4(wv[0], wv[1], wv[2], wv[3]);
+          if (row_live) *reinterpret_cast<uint4*>(zt + r0) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
         }
       }
     } else {
