@@ -31,7 +31,7 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 WORKLOADS = {w.name: w for w in workloads.CONFIGS}
 DEFAULT = workloads.LLADA_L512_NT64.name
-GEMM_CLASSES = ("fwd", "dx", "dw")
+GEMM_CLASSES = ("fwd", "recompute", "dx", "dw")
 TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "hbm_traffic_llada_head_B8_L512_nt64.json")
 
 
@@ -112,32 +112,105 @@ class Telemetry:
                 "samples": len(self.sclk)}
 
 
-def cpu_baseline(w: workloads.Workload, x: dict, budget_s: float = 20.0) -> dict:
-    """Time the float64 oracle's literal per-sample form (Algorithm 1 inner loop)
-    on sample j = 0 for the first responses of the batch, adding responses until
-    the time budget is spent."""
-    from oracle import elbo
+def blas_info() -> dict:
+    """BLAS library numpy runs on (threadpoolctl) and its thread count."""
     try:
         from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 0) for i in threadpool_info()), default=0)
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                return {"vendor": i.get("internal_api"), "version": i.get("version"),
+                        "threads": i.get("num_threads"), "architecture": i.get("architecture")}
     except Exception:
-        threads = 0
+        pass
+    return {"vendor": None, "version": None, "threads": None}
+
+
+def _oracle_tokens_per_s(w, x, js, budget_s, max_responses=None):
+    """The literal float64 oracle (Algorithm 1 inner loop) on samples `js`,
+    one response at a time, until `budget_s` of host time is spent (at least
+    one response per sample).  Returns (tokens, seconds, [(j, responses)])."""
+    from oracle import elbo
+    tokens, secs, done = 0, 0.0, []
+    per_j = budget_s / len(js)
+    for j in js:
+        nb, t_j = 0, 0.0
+        while nb < (max_responses or w.B) and (nb == 0 or t_j < per_j):
+            b = nb
+            p = elbo.Problem(1, w.L, w.d, w.V, w.n_t, j_begin=j, j_count=1, seed=w.philox_seed,
+                             seq_id_base=w.seq_id_base + b, t_mode=w.t_mode)
+            t0 = time.perf_counter()
+            r = elbo.elbo_literal(p, x["hidden"][b:b + 1], x["W"], x["targets"][b:b + 1],
+                                  x["resp_mask"][b:b + 1], x["adv"][b:b + 1])
+            t_j += time.perf_counter() - t0
+            tokens += int(r.n_masked.sum())
+            nb += 1
+        secs += t_j
+        done.append((j, nb))
+    return tokens, secs, done
+
+
+def cpu_baseline(w: workloads.Workload, x: dict, budget_s: float = 20.0,
+                 single_thread_s: float = 15.0) -> dict:
+    """The float64 oracle's literal per-sample form timed on this host: samples
+    j = 0 and 1 of the workload on all BLAS threads (responses added until the
+    budget is spent), and one response of sample j = 0 of the B=8, L=256
+    workload on one BLAS thread."""
+    blas = blas_info()
     cores = len(os.sched_getaffinity(0))
-    tokens, secs, nb = 0, 0.0, 0
-    while nb < w.B and secs < budget_s:
-        b = nb
-        p = elbo.Problem(1, w.L, w.d, w.V, w.n_t, j_begin=0, j_count=1, seed=w.philox_seed,
-                         seq_id_base=w.seq_id_base + b, t_mode=w.t_mode)
-        t0 = time.perf_counter()
-        r = elbo.elbo_literal(p, x["hidden"][b:b + 1], x["W"], x["targets"][b:b + 1],
-                              x["resp_mask"][b:b + 1], x["adv"][b:b + 1])
-        secs += time.perf_counter() - t0
-        tokens += int(r.n_masked.sum())
-        nb += 1
-    return {"value": tokens / secs, "unit": "masked tokens/s", "cores": threads or cores,
-            "kind": "oracle",
-            "sample": f"literal float64 oracle, MC sample j=0 of responses 0..{nb - 1} "
-                      f"({tokens} masked tokens, fwd+bwd incl. full dW), {secs:.1f} s"}
+    tokens, secs, done = _oracle_tokens_per_s(w, x, (0, 1), budget_s)
+    out = {"value": tokens / secs, "unit": "masked tokens/s", "cores": blas["threads"] or cores,
+           "kind": "oracle", "blas": blas, "host_cpus": cores,
+           "sample": f"literal float64 oracle, MC samples j=0,1 of {w.name} "
+                     f"(responses per sample: {dict(done)}; {tokens} masked tokens, fwd+bwd incl. "
+                     f"full dW), {secs:.1f} s on {blas['threads'] or cores} BLAS threads"}
+    if single_thread_s > 0:
+        try:
+            from threadpoolctl import threadpool_limits
+            w2 = workloads.LLADA_L256
+            x2 = x if w2.name == w.name else workloads.generate(w2)
+            with threadpool_limits(1):
+                t2, s2, _ = _oracle_tokens_per_s(w2, x2, (0,), single_thread_s, max_responses=1)
+            out["single_thread"] = {"value": t2 / s2, "unit": "masked tokens/s", "threads": 1,
+                                    "sample": f"{w2.name} j=0, response 0: {t2} masked tokens, "
+                                              f"{s2:.1f} s"}
+        except ImportError:
+            out["single_thread"] = None
+    return out
+
+
+def cpu_plan(out_path=None):
+    """The oracle's literal form on samples j = 0 and 1 of every LLaDA-shaped
+    workload with the full batch (all responses), on all BLAS threads, plus
+    one response of the B=8, L=256 workload's sample j = 0 on one thread; one
+    JSON line per measurement (host only, minutes of CPU time)."""
+    from oracle import elbo
+    blas = blas_info()
+    rows = []
+    for w in workloads.CONFIGS[1:]:
+        x = workloads.generate(w)
+        for j in (0, 1):
+            p = elbo.Problem(w.B, w.L, w.d, w.V, w.n_t, j_begin=j, j_count=1, seed=w.philox_seed,
+                             seq_id_base=w.seq_id_base, t_mode=w.t_mode)
+            t0 = time.perf_counter()
+            r = elbo.elbo_literal(p, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"])
+            secs = time.perf_counter() - t0
+            tok = int(r.n_masked.sum())
+            row = {"workload": w.name, "j": j, "masked_tokens": tok, "seconds": secs,
+                   "value": tok / secs, "unit": "masked tokens/s", "threads": blas["threads"],
+                   "blas": blas}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+    from threadpoolctl import threadpool_limits
+    w = workloads.LLADA_L256
+    x = workloads.generate(w)
+    with threadpool_limits(1):
+        tok, secs, _ = _oracle_tokens_per_s(w, x, (0,), 0.0, max_responses=1)
+    row = {"workload": w.name, "j": 0, "responses": 1, "masked_tokens": tok, "seconds": secs,
+           "value": tok / secs, "unit": "masked tokens/s", "threads": 1, "blas": blas}
+    rows.append(row)
+    print(json.dumps(row), flush=True)
+    if out_path:
+        json.dump(rows, open(out_path, "w"), indent=1)
 
 
 def main():
@@ -147,12 +220,27 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default=DEFAULT, choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-budget", type=float, default=20.0,
+                    help="seconds of host time for the oracle on samples j = 0, 1")
+    ap.add_argument("--cpu-single-thread", type=float, default=12.0,
+                    help="seconds for the one-thread oracle figure (0: skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the per-sample + final-RMSNorm variant measurement")
+    ap.add_argument("--ws-budget-gib", type=float, default=0.0,
+                    help="workspace budget of the timed step (0: the default layout)")
+    ap.add_argument("--vocab-chunk", type=int, default=0,
+                    help="force the recompute backward with this vocabulary chunk")
+    ap.add_argument("--no-budget-sweep", action="store_true",
+                    help="skip the workspace-budget sweep")
+    ap.add_argument("--cpu-plan", metavar="OUT_JSON", nargs="?", const="",
+                    help="only time the CPU oracle on samples j = 0, 1 of every LLaDA workload "
+                         "(full batch) and exit")
     args = ap.parse_args()
+    if args.cpu_plan is not None:
+        cpu_plan(args.cpu_plan or None)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -167,7 +255,11 @@ def main():
     dev = bgpo.device_inputs(x)
     B, L, d, V, nt = w.B, w.L, w.d, w.V, w.n_t
     prob = bgpo.Problem(B, L, d, V, nt, seed=w.philox_seed, seq_id_base=w.seq_id_base,
-                        t_mode=w.t_mode)
+                        t_mode=w.t_mode, ws_budget=int(args.ws_budget_gib * GiB),
+                        vocab_chunk=args.vocab_chunk)
+    plan = bgpo.bgpo_workspace_plan(prob)
+    # peak memory against n_t first, with nothing else allocated but the inputs
+    mem_vs_nt = memory_vs_n_t(w, prob, dev, x)
     ws = bgpo.alloc_workspace(prob)
     dX = torch.zeros(B, L, d, dtype=torch.float32, device="cuda")
     dW = torch.zeros(d, V, dtype=torch.float32, device="cuda")
@@ -182,14 +274,6 @@ def main():
         bgpo.bgpo_elbo_bwd_accumulate(p, dev["hidden"], dev["W"], dev["targets"],
                                       dev["resp_mask"], dev["adv"], None, 1.0 / 8, dX, dW, ell, g,
                                       loss, nm, tt, flags, ws, timing=timing)
-
-    # peak device memory with a single sample vs all n_t samples (same workspace)
-    torch.cuda.synchronize()
-    torch.cuda.reset_peak_memory_stats()
-    step(bgpo.Problem(B, L, d, V, nt, j_begin=0, j_count=1, seed=w.philox_seed,
-                      seq_id_base=w.seq_id_base, t_mode=w.t_mode))
-    torch.cuda.synchronize()
-    peak_one = torch.cuda.max_memory_allocated()
 
     for _ in range(args.warmup):
         step(prob)
@@ -209,7 +293,6 @@ def main():
         wall = time.perf_counter() - wall0
     telemetry = tel.summary()
     ms = start.elapsed_time(end) / args.steps
-    peak_all = torch.cuda.max_memory_allocated()
     tokens = int(nm.sum().item())                        # masked tokens per step
     value = tokens / (ms / 1e3)
 
@@ -252,9 +335,12 @@ def main():
             e["algorithmic_hbm_frac"] = e["algorithmic_gbs"] / PEAK_HBM_GBS
     dom = max((k for k in per_kernel if k in GEMM_CLASSES), key=lambda k: per_kernel[k]["ms_per_step"])
     achieved = per_kernel[dom]["tflops"]
-    # three GEMM passes per sample (forward logits, dX, dW): the backward reuses
-    # the forward's exponentials, so the executed MFMA work is the useful 6 d V
-    exec_flops = 6.0 * d * V * value
+    # GEMM passes per sample: forward logits, dX, dW (stored mode: the
+    # backward reuses the forward's exponentials, so executed = useful 6 d V),
+    # plus the chunked logits recompute in the recompute mode (8 d V executed)
+    passes = sum(1 for k in GEMM_CLASSES if k in per_kernel)
+    exec_flops = 2.0 * passes * d * V * value
+    useful_flops = 6.0 * d * V * value
 
     out = {
         "metric": "masked tokens/sec fwd+bwd per MC sample; % bf16 MFMA peak; peak mem vs n_t",
@@ -275,17 +361,18 @@ def main():
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": hbm_traffic(dom, w.name)},
-        "gemm_passes_per_sample": len(GEMM_CLASSES),
-        "mfma_frac_6dV": exec_flops / (PEAK_BF16_TFLOPS * 1e12),
+        "backward_plan": plan,
+        "gemm_passes_per_sample": passes,
+        "mfma_frac_executed": exec_flops / (PEAK_BF16_TFLOPS * 1e12),
+        "mfma_frac_6dV": useful_flops / (PEAK_BF16_TFLOPS * 1e12),
         "kernels": per_kernel,
         "telemetry": telemetry,
         # the same MFMA fraction against the peak at the mean engine clock measured
-        "mfma_frac_6dV_at_measured_clock": (
+        "mfma_frac_executed_at_measured_clock": (
             exec_flops / (PEAK_BF16_TFLOPS * 1e12 * telemetry["sclk_mhz_mean"] / 2400.0)
             if telemetry.get("sclk_mhz_mean") else None),
         "wall_s_timed": wall,
-        "peak_mem_bytes": {"n_t_1": peak_one, f"n_t_{nt}": peak_all,
-                           "workspace": bgpo.bgpo_workspace_size(prob)},
+        "peak_mem_vs_n_t": mem_vs_nt,
         "status_flags": int(flags.item()),
         "input_gen_s": gen_s,
     }
@@ -293,12 +380,142 @@ def main():
         out["variants"] = {"per_sample_rmsnorm": per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens),
                            "exact_objective_off_policy": exact_objective_leg(w, prob, dev, ws, args,
                                                                              tokens)}
-        del ws
-        torch.cuda.empty_cache()
+    # the remaining legs allocate their own workspaces and buffers
+    del ws, dX, dW, ell, g, loss, nm, tt
+    torch.cuda.empty_cache()
+    if not args.no_budget_sweep and args.ws_budget_gib == 0 and args.vocab_chunk == 0:
+        out["budget_sweep"] = budget_sweep_leg(w, dev)
+    if not args.no_variants:
         out["variants"]["exact_objective_retained"] = retained_memory_leg(w, prob, dev)
+        out["mask_compaction_2p20"] = mask_scaling_leg()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, x, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(w, x, args.cpu_budget, args.cpu_single_thread)
     print(json.dumps(out))
+
+
+GiB = 1 << 30
+
+
+def _call_buffers(w, nt):
+    import torch
+    f = dict(device="cuda")
+    return dict(dX=torch.zeros(w.B, w.L, w.d, dtype=torch.float32, **f),
+                dW=torch.zeros(w.d, w.V, dtype=torch.float32, **f),
+                ell=torch.zeros(w.B, nt, dtype=torch.float64, **f),
+                g=torch.zeros(w.B, nt, dtype=torch.float64, **f),
+                loss=torch.zeros(1, dtype=torch.float64, **f),
+                nm=torch.zeros(w.B, nt, dtype=torch.int32, **f),
+                flags=torch.zeros(1, dtype=torch.int32, **f))
+
+
+def _bwd(bgpo, p, dev, o, ws):
+    bgpo.bgpo_elbo_bwd_accumulate(p, dev["hidden"], dev["W"], dev["targets"], dev["resp_mask"],
+                                  dev["adv"], None, 1.0 / 8, o["dX"], o["dW"], o["ell"], o["g"],
+                                  o["loss"], o["nm"], None, o["flags"], ws)
+
+
+def memory_vs_n_t(w, prob, dev, x, n_ts=(1, 4, 16, 64)):
+    """Peak device memory of one backward call over all n_t samples, for
+    several n_t at the step's layout: torch's peak of everything allocated
+    (inputs, outputs, gradients, workspace) and the drop of free device
+    memory (hipMemGetInfo) across the call, which would show any allocation
+    inside the library."""
+    import dataclasses
+    import torch
+    from paper_2510_11683_amd import bgpo
+    res = {"n_t": list(n_ts), "workspace_bytes": [], "peak_mem_bytes": [],
+           "mem_get_info_drop_during_call": [], "inputs_bytes": sum(t.numel() * t.element_size()
+                                                                   for t in dev.values())}
+    for n in n_ts:
+        p = dataclasses.replace(prob, n_t=n)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        ws = bgpo.alloc_workspace(p)
+        o = _call_buffers(w, n)
+        torch.cuda.synchronize()
+        free0 = torch.cuda.mem_get_info()[0]
+        _bwd(bgpo, p, dev, o, ws)
+        torch.cuda.synchronize()
+        free1 = torch.cuda.mem_get_info()[0]
+        res["workspace_bytes"].append(ws.numel())
+        res["peak_mem_bytes"].append(torch.cuda.max_memory_allocated())
+        res["mem_get_info_drop_during_call"].append(free0 - free1)
+        del ws, o
+    torch.cuda.empty_cache()
+    return res
+
+
+def budget_sweep_leg(w, dev, budgets_gib=(2, 4, 8, 16, 32), n_ts=(1, 64)):
+    """Masked tokens/s and peak device memory of one backward call over all
+    samples under each workspace budget (the layout it picks: stored
+    exponentials with smaller units, or the recompute backward), for
+    n_t = 1 and the workload's n_t."""
+    import torch
+    from paper_2510_11683_amd import bgpo
+    out = []
+    for bg in budgets_gib:
+        for n in n_ts:
+            n = min(n, w.n_t) if n != 1 else 1
+            p = bgpo.Problem(w.B, w.L, w.d, w.V, n, seed=w.philox_seed, seq_id_base=w.seq_id_base,
+                             t_mode=w.t_mode, ws_budget=bg * GiB)
+            try:
+                plan = bgpo.bgpo_workspace_plan(p)
+            except bgpo.BgpoError as e:
+                out.append({"budget_gib": bg, "n_t": n, "error": str(e)})
+                continue
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+            torch.cuda.reset_peak_memory_stats()
+            ws = bgpo.alloc_workspace(p)
+            o = _call_buffers(w, n)
+            _bwd(bgpo, p, dev, o, ws)                    # warm-up
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = 3 if n == 1 else 1
+            a.record()
+            for _ in range(reps):
+                _bwd(bgpo, p, dev, o, ws)
+            b.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(b) / reps
+            tokens = int(o["nm"].sum().item())
+            out.append({"budget_gib": bg, "n_t": n, "plan": plan, "ms_per_call": ms,
+                        "masked_tokens": tokens, "value": tokens / (ms / 1e3),
+                        "peak_mem_bytes": torch.cuda.max_memory_allocated(),
+                        "status_flags": int(o["flags"].item())})
+            del ws, o
+    torch.cuda.empty_cache()
+    return out
+
+
+def mask_scaling_leg(B=4096, L=256, reps=5):
+    """Mask draw + stable compaction of one sample at the B*L = 2^20 limit:
+    the single-workgroup kernel (bgpo_sample_masks) against the multi-block
+    passes the library uses above 65536 positions (test hook), HIP events."""
+    import torch
+    from paper_2510_11683_amd import bgpo
+    p = bgpo.Problem(B, L, 64, 64, 4, seed=0xB6B0D000)
+    resp = torch.ones(B, L, dtype=torch.uint8, device="cuda")
+    idx = torch.empty(B * L, dtype=torch.int32, device="cuda")
+    nm = torch.empty(B, dtype=torch.int32, device="cuda")
+    res = {"B": B, "L": L}
+    for name, fn in (("single_workgroup", lambda j: bgpo.bgpo_sample_masks(p, resp, j, idx, nm)),
+                     ("multi_block", lambda j: bgpo.bgpo_test_mask_multiblock(p, resp, j, idx, nm))):
+        fn(0)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for r in range(reps):
+            fn(r % 4)
+        b.record()
+        torch.cuda.synchronize()
+        us = 1e3 * a.elapsed_time(b) / reps
+        n = int(nm.sum().item())
+        # resp_mask read + one 4-byte index per masked position written
+        res[name] = {"us_per_sample": us, "masked": n,
+                     "gbs": (B * L + 4 * n) / (us * 1e-6) / 1e9}
+    return res
 
 
 def retained_memory_leg(w, prob, dev, n_ts=(1, 4, 16)):

@@ -4,7 +4,10 @@
 #ifndef BGPO_TESTING_H_
 #define BGPO_TESTING_H_
 
+#include <stddef.h>
 #include <stdint.h>
+
+#include "bgpo.h"
 
 #ifdef __cplusplus
 extern "C" {
@@ -27,6 +30,17 @@ int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
  * shape rules and return codes as bgpo_test_gemm_nt. */
 int bgpo_test_gemm_split(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
                          int32_t K, int32_t n_split, void* stream);
+
+/* The multi-block form of the mask and compaction step (the three passes the
+ * library uses above 65536 positions: mask words with per-block counts, a
+ * one-block scan of the counts, a scatter), run at any size, with the same
+ * arguments and outputs as bgpo_sample_masks; `scratch` is device memory of
+ * at least bgpo_test_mask_scratch_bytes(prob) bytes, 256-byte aligned
+ * (BGPO_ERR_WORKSPACE otherwise). */
+size_t bgpo_test_mask_scratch_bytes(const bgpo_problem* prob);
+int bgpo_test_mask_multiblock(const bgpo_problem* prob, const uint8_t* resp_mask, int32_t j,
+                              int32_t* idx, int32_t* n_masked, float* t_out, void* scratch,
+                              size_t scratch_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -90,10 +90,13 @@ def _load():
     lib.bgpo_moments_summary.argtypes = [vp, vp, vp, ctypes.c_int64, i32, vp, vp, sz, vp]
     lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
     lib.bgpo_test_gemm_split.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp]
+    lib.bgpo_test_mask_scratch_bytes.restype = sz
+    lib.bgpo_test_mask_scratch_bytes.argtypes = [P(_Problem)]
+    lib.bgpo_test_mask_multiblock.argtypes = [P(_Problem), vp, i32, vp, vp, vp, vp, sz, vp]
     for f in ("bgpo_workspace_size", "bgpo_workspace_plan", "bgpo_sample_masks", "bgpo_elbo_fwd",
               "bgpo_elbo_bwd_accumulate", "bgpo_elbo_bwd_accumulate_noalloc", "bgpo_elbo_fwd_rmsnorm",
               "bgpo_elbo_bwd_accumulate_rmsnorm", "bgpo_moments_update", "bgpo_moments_summary",
-              "bgpo_test_gemm_nt", "bgpo_test_gemm_split"):
+              "bgpo_test_gemm_nt", "bgpo_test_gemm_split", "bgpo_test_mask_multiblock"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -205,6 +208,23 @@ def bgpo_sample_masks(prob: Problem, resp_mask, j: int, idx, n_masked, t_out=Non
                                   _ptr(n_masked, "n_masked", (torch.int32,), (B,)),
                                   _ptr(t_out, "t_out", (torch.float32,), (B,), allow_none=True),
                                   _stream(stream)), "bgpo_sample_masks")
+
+
+def bgpo_test_mask_multiblock(prob: Problem, resp_mask, j: int, idx, n_masked, t_out=None,
+                              stream=None):
+    """Test hook: the multi-block mask passes (any size); allocates their scratch."""
+    B, L = prob.B, prob.L
+    pc = prob.c()
+    scratch = torch.empty(int(_lib.bgpo_test_mask_scratch_bytes(ctypes.byref(pc))) + 256,
+                          dtype=torch.uint8, device=resp_mask.device)
+    _check(_lib.bgpo_test_mask_multiblock(
+        ctypes.byref(pc), _ptr(resp_mask, "resp_mask", (torch.uint8,), (B, L)), int(j),
+        _ptr(idx, "idx", (torch.int32,), (B * L,)),
+        _ptr(n_masked, "n_masked", (torch.int32,), (B,)),
+        _ptr(t_out, "t_out", (torch.float32,), (B,), allow_none=True),
+        _ptr(scratch, "scratch", (torch.uint8,)), scratch.numel(), _stream(stream)),
+        "bgpo_test_mask_multiblock")
+    return scratch
 
 
 def _act_shape(prob: Problem):

@@ -88,6 +88,7 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
     w.lp = static_cast<float*>(take(RP * 4));
     w.row_scale = static_cast<float*>(take(RP * 4));
     w.inv_rms = static_cast<float*>(take(RP * 4));
+    w.mask_scratch = take(mask_scratch_bytes(dm.B, dm.L));
     w.part_m = static_cast<float*>(take(nvt * RP * 4));
     w.part_s = static_cast<float*>(take(nvt * RP * 4));
     w.Hc = static_cast<uint16_t*>(take(RP * dm.d * 2));
@@ -399,7 +400,8 @@ static int run_forward_unit(const bgpo_problem* p, Workspace& ws, Timer& tm, int
     BGPO_TRY(launch_mask_compact(resp, targets, dm.B, dm.L, dm.n_t, j, gs, p->t_mode, p->seed,
                                  p->seq_id_base, &ws, nullptr, n_masked + j, dm.n_t,
                                  t_out ? t_out + j : nullptr, dm.n_t, dm.V,
-                                 gs ? ws.meta + (gs - 1) : prev_unit, dx_plan(dm, ws, grid), s));
+                                 gs ? ws.meta + (gs - 1) : prev_unit, dx_plan(dm, ws, grid),
+                                 ws.mask_scratch, false, s));
   }
   BGPO_TRY(tm.end(n_s));
   BGPO_TRY(tm.begin(BGPO_K_GATHER));
@@ -477,7 +479,8 @@ int bgpo_sample_masks(const bgpo_problem* prob, const uint8_t* resp_mask, int32_
   if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
   if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, 0, prob->t_mode,
                           prob->seed, prob->seq_id_base, nullptr, idx, n_masked, 1, t_out, 1,
-                          prob->V, nullptr, DxPlan{1, 1, 1, 1}, (hipStream_t)stream) != hipSuccess)
+                          prob->V, nullptr, DxPlan{1, 1, 1, 1}, nullptr, false,
+                          (hipStream_t)stream) != hipSuccess)
     return BGPO_ERR_HIP;
   return BGPO_OK;
 }
@@ -829,4 +832,29 @@ extern "C" int bgpo_elbo_bwd_accumulate_noalloc(
   return elbo_bwd_impl(&p, act_of(&p, hidden, nullptr), W_head, targets, resp_mask, adv, ell_old,
                        loss_scale, dX, nullptr, dW, ell, g, loss, n_masked, t_out, status_flags,
                        ws, kScratchBytes, stream, nullptr);
+}
+
+// ---- test hook: the multi-block mask passes at any size ----
+extern "C" size_t bgpo_test_mask_scratch_bytes(const bgpo_problem* prob) {
+  return prob ? bgpo::mask_scratch_bytes(prob->B, prob->L) : 0;
+}
+
+extern "C" int bgpo_test_mask_multiblock(const bgpo_problem* prob, const uint8_t* resp_mask,
+                                         int32_t j, int32_t* idx, int32_t* n_masked,
+                                         float* t_out, void* scratch, size_t scratch_bytes,
+                                         void* stream) {
+  using namespace bgpo;
+  Plan pl;
+  const int st = plan_problem(prob, &pl);
+  if (st != BGPO_OK) return st;
+  if (!resp_mask || !idx || !n_masked || j < 0 || j >= prob->n_t) return BGPO_ERR_INVALID_ARG;
+  if (!scratch || ((uintptr_t)scratch % 256) != 0 ||
+      scratch_bytes < mask_scratch_bytes(prob->B, prob->L))
+    return BGPO_ERR_WORKSPACE;
+  if (launch_mask_compact(resp_mask, nullptr, prob->B, prob->L, prob->n_t, j, 0, prob->t_mode,
+                          prob->seed, prob->seq_id_base, nullptr, idx, n_masked, 1, t_out, 1,
+                          prob->V, nullptr, DxPlan{1, 1, 1, 1}, scratch, true,
+                          (hipStream_t)stream) != hipSuccess)
+    return BGPO_ERR_HIP;
+  return BGPO_OK;
 }

@@ -71,6 +71,7 @@ struct Workspace {
   float* row_scale;    // [RP]         gradient scale s of each row (0 for padding)
   double* dbar;        // [B]          mean log-ratio over all samples (exact objective)
   float* inv_rms;      // [RP]         final-RMSNorm 1/rms of each compacted row
+  void* mask_scratch;  // mask_scratch_bytes(B, L): the multi-block mask passes
   float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks of a sample
   uint16_t* dZ;        // stored mode: [RP, V] s (softmax - onehot), bf16 (first the fp16
                        // exponentials); recompute mode: [RP, chunk], one vocabulary chunk
@@ -130,7 +131,13 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
                                int j, int g, int t_mode, uint64_t seed, uint32_t seq_base,
                                const Workspace* ws, int32_t* idx_out, int32_t* n_masked_out,
                                int nm_stride, float* t_out, int t_stride, int V,
-                               const SampleMeta* prev, const DxPlan& plan, hipStream_t s);
+                               const SampleMeta* prev, const DxPlan& plan, void* scratch,
+                               bool force_multi, hipStream_t s);
+// scratch bytes the multi-block mask passes need (mask words, block counts and
+// offsets, timesteps); with scratch NULL the single-workgroup kernel runs, and
+// with scratch the multi-block passes run above 65536 positions (or always,
+// with force_multi)
+size_t mask_scratch_bytes(int B, int L);
 // x / hidden of row r is x + (row_seq[r] / B) * stride (the row's sample in the unit)
 // (f32: x / hidden are fp32, rounded to bf16 as they are read)
 hipError_t launch_row_rms(const void* x, bool f32, int64_t stride, int B, const Workspace& ws,

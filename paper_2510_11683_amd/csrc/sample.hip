@@ -13,6 +13,9 @@ namespace bgpo {
 
 constexpr int kMaskThreads = 1024;
 constexpr int kMaxB = 4096;
+// the single-workgroup mask kernel takes problems up to this many positions;
+// larger ones go through the multi-block passes below
+constexpr int64_t kSingleBlockPositions = 65536;
 
 // Philox words for position p = b*L + i are taken from counter (i>>2, seq, j, 0);
 // consecutive positions of one response share a counter block, so a thread
@@ -23,9 +26,12 @@ struct MaskWalker {
   int cached_b = -1, cached_blk = -1;
   u32x4 w;
   __device__ bool masked(const uint8_t* resp, const uint32_t* sT, int64_t p) {
+    return resp[p] ? test(sT, p) : false;
+  }
+  // the Philox test of response position p (resp_mask[p] != 0 assumed)
+  __device__ bool test(const uint32_t* sT, int64_t p) {
     const int b = (int)(p / L);
     const int i = (int)(p - (int64_t)b * L);
-    if (!resp[p]) return false;
     const int blk = i >> 2;
     if (blk != cached_blk || b != cached_b) {
       w = philox4x32_10(u32x4{(uint32_t)blk, seq_base + (uint32_t)b, (uint32_t)j, 0u}, k0, k1);
@@ -76,6 +82,23 @@ struct MaskOut {
   int row_cap;           // rows the unit holds (padding is written up to it)
 };
 
+// The record of a sample whose `total` masked rows follow row0 rows of its
+// unit, with the unit's columns from col0.
+__device__ void write_record(SampleMeta* m, int row0, int col0, int total, const DxPlan& plan) {
+  if (!m) return;
+  const int rows = row0 + total;
+  const int rows_pad = (rows + kRowPad - 1) / kRowPad * kRowPad;
+  m->n_rows = rows;
+  m->n_rows_pad = rows_pad;
+  m->col_off = col0;
+  m->col_end = col0 + (rows + 63) / 64 * 64;
+  m->s_rows = total;
+  m->s_row_off = row0;
+  choose_dx_split(rows_pad / kRowPad, plan, &m->dx_split, &m->dx_kslab);
+}
+
+// Single-workgroup form (up to kSingleBlockPositions positions): timesteps in
+// LDS, every thread a contiguous run of positions, one block-wide scan.
 __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
     const uint8_t* __restrict__ resp, const int32_t* __restrict__ targets, int B, int L, int n_t,
     int j, int g, int t_mode, uint32_t k0, uint32_t k1, uint32_t seq_base, MaskOut out,
@@ -157,16 +180,7 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
   }
   if (tid == 0) {
     if (out.seg_off) out.seg_off[B] = rows;
-    if (out.meta) {
-      SampleMeta* m = out.meta;
-      m->n_rows = rows;
-      m->n_rows_pad = rows_pad;
-      m->col_off = col0;
-      m->col_end = col0 + (rows + 63) / 64 * 64;
-      m->s_rows = total;
-      m->s_row_off = row0;
-      choose_dx_split(rows_pad / kRowPad, plan, &m->dx_split, &m->dx_kslab);
-    }
+    write_record(out.meta, row0, col0, total, plan);
   }
   // padding rows up to the next row tile (a later sample of the unit
   // overwrites them with its own rows)
@@ -177,11 +191,167 @@ __global__ __launch_bounds__(kMaskThreads) void k_mask_compact(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Multi-block form for large B*L: the same masks (the same Philox words and
+// integer test), in three passes that each spread over the whole GPU:
+//   k_mask_bits     one 32-bit mask word per thread (32 consecutive positions),
+//                   one count per block of kMbPositions positions
+//   k_mask_scan     one block: exclusive scan of the block counts, the
+//                   per-response offsets (block offset + popcounts of the
+//                   words before the response's first position), counts,
+//                   the sample's record and the padding rows
+//   k_mask_scatter  every set bit in ascending position order to its row
+// so the compacted order and every count equal the single-block form's.
+constexpr int kMbThreads = 256;
+constexpr int kMbPositions = kMbThreads * 32;   // positions per block
+
+__global__ __launch_bounds__(256) void k_timesteps(int B, int n_t, int j, int t_mode, uint32_t k0,
+                                                   uint32_t k1, uint32_t seq_base,
+                                                   uint32_t* __restrict__ t24,
+                                                   float* __restrict__ t_out, int t_stride) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= B) return;
+  const uint32_t T = timestep_t24(k0, k1, seq_base + (uint32_t)b, j, n_t, t_mode);
+  t24[b] = T;
+  if (t_out) t_out[(int64_t)b * t_stride] = (float)T * (1.0f / 16777216.0f);
+}
+
+// exclusive prefix of v over the block's 256 threads (and the block total)
+__device__ __forceinline__ int block_exclusive_sum(int v, int* s_wave, int* total) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int u = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += u;
+  }
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int base = incl - v;
+  for (int q = 0; q < wave; ++q) base += s_wave[q];
+  *total = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
+  return base;
+}
+
+__global__ __launch_bounds__(kMbThreads) void k_mask_bits(
+    const uint8_t* __restrict__ resp, const uint32_t* __restrict__ t24, int L, int64_t P, int j,
+    uint32_t k0, uint32_t k1, uint32_t seq_base, uint32_t* __restrict__ bits,
+    int32_t* __restrict__ wprefix, int32_t* __restrict__ blk_count) {
+  __shared__ int s_wave[kMbThreads / 64];
+  const int tid = threadIdx.x;
+  const int64_t w = (int64_t)blockIdx.x * kMbThreads + tid;
+  uint32_t word = 0;
+  const int64_t p0 = w * 32;
+  if (p0 < P) {
+    // the word's 32 response-mask bytes in two 16-byte loads (resp_mask rows
+    // are contiguous; a word that crosses P reads byte by byte)
+    uint8_t r[32];
+    if (p0 + 32 <= P && (((uintptr_t)(resp + p0)) & 15) == 0) {
+      *reinterpret_cast<uint4*>(r) = *reinterpret_cast<const uint4*>(resp + p0);
+      *reinterpret_cast<uint4*>(r + 16) = *reinterpret_cast<const uint4*>(resp + p0 + 16);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 32; ++e) r[e] = p0 + e < P ? resp[p0 + e] : 0;
+    }
+    MaskWalker mw{k0, k1, seq_base, L, j};
+#pragma unroll
+    for (int e = 0; e < 32; ++e)
+      if (r[e] && mw.test(t24, p0 + e)) word |= 1u << e;
+    bits[w] = word;
+  }
+  int total;
+  const int pre = block_exclusive_sum(__popc(word), s_wave, &total);
+  if (p0 < P) wprefix[w] = pre;
+  if (tid == 0) blk_count[blockIdx.x] = total;
+}
+
+constexpr int kMbMaxBlocks = (1 << 20) / kMbPositions;   // B*L <= 2^20
+
+// masked positions before position pos < P: the block's offset, the word's
+// prefix within its block, the word's bits below pos
+__device__ __forceinline__ int masked_before(const uint32_t* bits, const int32_t* wprefix,
+                                             const int32_t* blk_off, int64_t pos) {
+  const int64_t w = pos / 32;
+  return blk_off[w / kMbThreads] + wprefix[w] +
+         __popc(bits[w] & ((1u << (int)(pos - w * 32)) - 1u));
+}
+
+__global__ __launch_bounds__(1024) void k_mask_scan(
+    const uint32_t* __restrict__ bits, const int32_t* __restrict__ wprefix,
+    const int32_t* __restrict__ blk_count,
+    int32_t* __restrict__ blk_off, int nblk, int B, int L, int g, MaskOut out,
+    int32_t* __restrict__ nm_out, int nm_stride, const SampleMeta* prev, DxPlan plan) {
+  __shared__ int s_total;
+  __shared__ int32_t s_off[kMbMaxBlocks];
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    int acc = 0;
+    for (int q = 0; q < nblk; ++q) {
+      s_off[q] = acc;
+      blk_off[q] = acc;   // for the scatter pass
+      acc += blk_count[q];
+    }
+    s_total = acc;
+  }
+  __syncthreads();
+  const int total = s_total;
+  const int row0 = (g > 0 && prev) ? prev->n_rows : 0;
+  const int col0 = prev ? (g > 0 ? prev->col_off : prev->col_end) : 0;
+  for (int b = tid; b < B; b += 1024) {
+    const int s0 = masked_before(bits, wprefix, s_off, (int64_t)b * L);
+    const int s1 = b + 1 < B ? masked_before(bits, wprefix, s_off, (int64_t)(b + 1) * L) : total;
+    if (nm_out) nm_out[(int64_t)b * nm_stride] = s1 - s0;
+    if (out.seg_off) out.seg_off[b] = row0 + s0;
+  }
+  const int rows = row0 + total;
+  const int rows_pad = (rows + kRowPad - 1) / kRowPad * kRowPad;
+  if (tid == 0) {
+    if (out.seg_off) out.seg_off[B] = rows;
+    write_record(out.meta, row0, col0, total, plan);
+  }
+  const int pad_end = min(rows_pad, out.row_cap);
+  for (int r = rows + tid; r < pad_end; r += 1024) {
+    if (out.row_tgt) out.row_tgt[r] = 0;
+    if (out.row_seq) out.row_seq[r] = 0;
+  }
+}
+
+__global__ __launch_bounds__(kMbThreads) void k_mask_scatter(
+    const uint32_t* __restrict__ bits, const int32_t* __restrict__ wprefix,
+    const int32_t* __restrict__ blk_off, const int32_t* __restrict__ targets, int B, int L,
+    int64_t P, int g, int V, MaskOut out, const SampleMeta* prev) {
+  const int64_t w = (int64_t)blockIdx.x * kMbThreads + threadIdx.x;
+  if (w * 32 >= P) return;
+  const uint32_t word = bits[w];
+  const int row0 = (g > 0 && prev) ? prev->n_rows : 0;
+  int r = row0 + blk_off[blockIdx.x] + wprefix[w];
+  uint32_t m = word;
+  while (m) {
+    const int e = __builtin_ctz(m);
+    m &= m - 1;
+    const int64_t p = w * 32 + e;
+    if (out.idx) out.idx[r] = (int32_t)p;
+    if (out.row_tgt) {
+      const int y = targets[p];
+      out.row_tgt[r] = y < 0 ? 0 : (y >= V ? V - 1 : y);
+    }
+    if (out.row_seq) out.row_seq[r] = g * B + (int)(p / L);
+    ++r;
+  }
+}
+
+size_t mask_scratch_bytes(int B, int L) {
+  const int64_t P = (int64_t)B * L;
+  const int64_t words = (P + 31) / 32, nblk = (P + kMbPositions - 1) / kMbPositions;
+  return (size_t)(words * 8 + nblk * 8 + (int64_t)B * 4 + 4 * 256);
+}
+
 hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int B, int L, int n_t,
                                int j, int g, int t_mode, uint64_t seed, uint32_t seq_base,
                                const Workspace* ws, int32_t* idx_out, int32_t* n_masked_out,
                                int nm_stride, float* t_out, int t_stride, int V,
-                               const SampleMeta* prev, const DxPlan& plan, hipStream_t s) {
+                               const SampleMeta* prev, const DxPlan& plan, void* scratch,
+                               bool force_multi, hipStream_t s) {
   MaskOut out{idx_out, nullptr, nullptr, nullptr, nullptr, nullptr, 0};
   if (ws) {
     out.idx = ws->idx;
@@ -192,10 +362,38 @@ hipError_t launch_mask_compact(const uint8_t* resp, const int32_t* targets, int 
     out.meta = ws->meta + g;
     out.row_cap = (int)ws->RP;
   }
-  k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, g, t_mode,
-                                            (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
-                                            seq_base, out, n_masked_out, nm_stride, t_out,
-                                            t_stride, V, prev, plan);
+  const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+  const int64_t P = (int64_t)B * L;
+  if ((P <= kSingleBlockPositions && !force_multi) || !scratch) {
+    k_mask_compact<<<1, kMaskThreads, 0, s>>>(resp, targets, B, L, n_t, j, g, t_mode, k0, k1,
+                                              seq_base, out, n_masked_out, nm_stride, t_out,
+                                              t_stride, V, prev, plan);
+    return hipGetLastError();
+  }
+  // scratch: mask words, block counts and offsets, and (without a unit) the
+  // sample's timesteps
+  char* sc = static_cast<char*>(scratch);
+  const int64_t words = (P + 31) / 32, nblk = (P + kMbPositions - 1) / kMbPositions;
+  const int64_t wbytes = (words * 4 + 255) / 256 * 256;
+  uint32_t* bits = reinterpret_cast<uint32_t*>(sc);
+  int32_t* wprefix = reinterpret_cast<int32_t*>(sc + wbytes);
+  int32_t* blk_count = reinterpret_cast<int32_t*>(sc + 2 * wbytes);
+  int32_t* blk_off = blk_count + nblk;
+  uint32_t* t24 = out.t24 ? out.t24
+                          : reinterpret_cast<uint32_t*>(sc + 2 * wbytes +
+                                                        (nblk * 8 + 255) / 256 * 256);
+  k_timesteps<<<(unsigned)((B + 255) / 256), 256, 0, s>>>(B, n_t, j, t_mode, k0, k1, seq_base, t24,
+                                                          t_out, t_stride);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_mask_bits<<<(unsigned)nblk, kMbThreads, 0, s>>>(resp, t24, L, P, j, k0, k1, seq_base, bits,
+                                                    wprefix, blk_count);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  k_mask_scan<<<1, 1024, 0, s>>>(bits, wprefix, blk_count, blk_off, (int)nblk, B, L, g, out,
+                                 n_masked_out, nm_stride, prev, plan);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  k_mask_scatter<<<(unsigned)nblk, kMbThreads, 0, s>>>(bits, wprefix, blk_off, targets, B, L, P,
+                                                       g, V, out, prev);
   return hipGetLastError();
 }
 

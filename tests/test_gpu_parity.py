@@ -100,6 +100,41 @@ def test_masks_bit_exact(w):
         assert (idx[n:].cpu().numpy() == -7).all()                       # untouched tail
 
 
+@pytest.mark.parametrize("B,L,lengths,j", [
+    (2, 64, None, 0), (8, 512, None, 3), (3, 5000, (1, 5000), 1), (37, 1, None, 0),
+    (4096, 256, (1, 256), 0), (4096, 256, None, 1), (1, 1 << 20, None, 2), (2048, 512, (300, 512), 5)],
+    ids=["B2_L64", "B8_L512", "B3_L5000_ragged", "B37_L1", "B4096_L256_ragged", "B4096_L256",
+         "B1_L2p20", "B2048_L512_ragged"])
+def test_mask_multiblock_bit_exact(B, L, lengths, j):
+    """The multi-block mask passes (used above 65536 positions, forced here at
+    every size) give the oracle's compacted positions, counts and timesteps
+    bit for bit, up to B*L = 2^20 positions (several blocks, ragged responses,
+    single-position responses, one response spanning every block)."""
+    w = workloads.TINY.replace(B=B, L=L, n_t=8, lengths=lengths, data_seed=2300 + B,
+                               philox_seed=0xB6B0C000 + B * 7 + L)
+    x = workloads.generate(w, with_weights=False, with_hidden=False)
+    resp = torch.from_numpy(x["resp_mask"]).cuda()
+    p = problem(w)
+    op = _oracle_problem(w)
+    idx = torch.full((B * L,), -7, dtype=torch.int32, device="cuda")
+    nm = torch.zeros(B, dtype=torch.int32, device="cuda")
+    t = torch.zeros(B, dtype=torch.float32, device="cuda")
+    lib().bgpo_test_mask_multiblock(p, resp, j, idx, nm, t)
+    T, tt, m, oidx = elbo.sample_masks(op, x["resp_mask"], j)
+    torch.cuda.synchronize()
+    n = int(nm.sum())
+    assert n == oidx.size
+    assert np.array_equal(idx[:n].cpu().numpy(), oidx)
+    assert np.array_equal(nm.cpu().numpy(), m.sum(axis=1))
+    assert np.array_equal(t.cpu().numpy().astype(np.float64), tt)
+    assert (idx[n:].cpu().numpy() == -7).all()
+    if B * L <= 65536:    # the single-workgroup kernel gives the same
+        idx2 = torch.full((B * L,), -7, dtype=torch.int32, device="cuda")
+        lib().bgpo_sample_masks(p, resp, j, idx2, nm, t)
+        torch.cuda.synchronize()
+        assert torch.equal(idx, idx2)
+
+
 # ---------------------------------------------------------------- ELBO head
 
 def _check_against_oracle(w, out, ref, js, adv, ell_old=None, loss_scale=1.0 / 8, bound=0):
