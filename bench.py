@@ -234,6 +234,8 @@ def main():
                     help="force the recompute backward with this vocabulary chunk")
     ap.add_argument("--no-budget-sweep", action="store_true",
                     help="skip the workspace-budget sweep")
+    ap.add_argument("--no-memory-leg", action="store_true",
+                    help="skip the peak-memory-against-n_t calls (profiling runs)")
     ap.add_argument("--cpu-plan", metavar="OUT_JSON", nargs="?", const="",
                     help="only time the CPU oracle on samples j = 0, 1 of every LLaDA workload "
                          "(full batch) and exit")
@@ -259,7 +261,7 @@ def main():
                         vocab_chunk=args.vocab_chunk)
     plan = bgpo.bgpo_workspace_plan(prob)
     # peak memory against n_t first, with nothing else allocated but the inputs
-    mem_vs_nt = memory_vs_n_t(w, prob, dev, x)
+    mem_vs_nt = None if args.no_memory_leg else memory_vs_n_t(w, prob, dev, x)
     ws = bgpo.alloc_workspace(prob)
     dX = torch.zeros(B, L, d, dtype=torch.float32, device="cuda")
     dW = torch.zeros(d, V, dtype=torch.float32, device="cuda")
