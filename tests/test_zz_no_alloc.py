@@ -66,3 +66,35 @@ def test_noalloc_matches_workspace_entry_point_twice_then_smaller():
         for k in ref:
             assert np.array_equal(got[k], ref[k]), (w.name, k)
         assert np.abs(got["dW"]).max() > 0 and got["flags"][0] == 0
+
+
+def test_noalloc_under_graph_capture():
+    """The allocation-free backward under HIP graph capture (the callers it is
+    for): captured after one eager call, replayed twice with eager zeroing in
+    between; every replay gives the workspace entry point's bits."""
+    from test_gpu_parity import MID
+    b = lib()
+    w = MID.replace(n_t=3)
+    x = workloads.generate(w)
+    ell_old = np.random.default_rng(52).normal(-400.0, 30.0, (w.B, w.n_t))
+    ref = _run(w, x, ell_old, noalloc=False)
+    p = problem(w, ws_budget=b.bgpo_noalloc_scratch_bytes())
+    dev, o = _buffers(w, x)
+    eo = torch.from_numpy(ell_old).cuda()
+    args = (dev["hidden"], dev["W"], dev["targets"], dev["resp_mask"], dev["adv"], eo, 0.25,
+            o["dX"], o["dW"], o["ell"], o["g"], o["loss"], o["nm"], o["t"], o["flags"])
+    b.bgpo_elbo_bwd_accumulate_noalloc(p, *args)          # the device's scratch address, once
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        b.bgpo_elbo_bwd_accumulate_noalloc(p, *args)
+        b.bgpo_elbo_bwd_accumulate_noalloc(p, *args)       # accumulates twice, as _run does
+    for _ in range(2):
+        for k in ("dX", "dW", "loss", "ell", "g", "nm", "t", "flags"):
+            o[k].zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = {k: v.cpu().numpy() for k, v in o.items()}
+        for k in ref:
+            assert np.array_equal(got[k], ref[k]), k
