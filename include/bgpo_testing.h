@@ -13,10 +13,12 @@
 extern "C" {
 #endif
 
-/* The bf16 MFMA GEMM core of the production kernels alone, used to test it in
- * isolation:
+/* The bf16 MFMA GEMM core of the production kernels alone (the kernel of the
+ * dX GEMM, in its operand layouts), used to test it in isolation:
  *   C[m][n] = sum_k A[m][k] * B[n][k]   (fp32 result, fp32 accumulation)
- * A bf16 [M, K], B bf16 [N, K], C float [M, N], all row-major device memory.
+ * A bf16 M x K in the library's K-slab-major operand layout (element (m, k)
+ * at index ((k / 64) M + m) 64 + k % 64, i.e. [K/64][M][64]); B bf16 [N, K]
+ * row-major; C float [M, N] row-major; all device memory.
  * Requires M, N >= 1 and K a positive multiple of 64.  Returns 0, -1 (invalid
  * argument) or -3 (HIP error).  Enqueued on `stream` (hipStream_t). */
 int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,

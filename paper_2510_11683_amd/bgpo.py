@@ -367,20 +367,22 @@ def bgpo_moments_summary(mean, m2, ref, count: int, out, workspace, stream=None)
 
 
 def bgpo_test_gemm_nt(A, B, C, stream=None):
-    """Test hook: C[m, n] = sum_k A[m, k] B[n, k] through the MFMA GEMM core."""
-    M, K = A.shape
-    N = B.shape[0]
-    _check(_lib.bgpo_test_gemm_nt(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
+    """Test hook: C[m, n] = sum_k A[m, k] B[n, k] through the MFMA GEMM core of
+    the dX GEMM, in its operand layouts: A K-slab-major [K/64, M, 64]
+    (element (m, k) at [k // 64, m, k % 64]), B row-major [N, K]."""
+    S, M, _ = A.shape
+    N, K = B.shape
+    _check(_lib.bgpo_test_gemm_nt(_ptr(A, "A", _BF16, (K // 64, M, 64)), _ptr(B, "B", _BF16, (N, K)),
                                   _ptr(C, "C", (torch.float32,), (M, N)), M, N, K, _stream(stream)),
            "bgpo_test_gemm_nt")
 
 
 def bgpo_test_gemm_split(A, B, C, n_split: int, stream=None):
     """Test hook: the GEMM core with K in n_split slices, slice s's product in
-    C[s] (C float32 [n_split, M, N])."""
-    M, K = A.shape
-    N = B.shape[0]
-    _check(_lib.bgpo_test_gemm_split(_ptr(A, "A", _BF16), _ptr(B, "B", _BF16, (N, K)),
+    C[s] (C float32 [n_split, M, N]); A, B as in bgpo_test_gemm_nt."""
+    S, M, _ = A.shape
+    N, K = B.shape
+    _check(_lib.bgpo_test_gemm_split(_ptr(A, "A", _BF16, (K // 64, M, 64)), _ptr(B, "B", _BF16, (N, K)),
                                      _ptr(C, "C", (torch.float32,), (n_split, M, N)), M, N, K,
                                      int(n_split), _stream(stream)),
            "bgpo_test_gemm_split")

@@ -58,14 +58,10 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
   const int64_t n_units = pl.retain ? (dm.n_t + G - 1) / G : 1;
   const int64_t RP = G * NP;
   const int64_t dw_batch = pl.retain ? n_units : pl.dw_batch;
-  // leading dimension of H_c^T and dZ^T: the dW GEMM reads 256-row panels of
-  // both, and with a power-of-two row pitch (32768 rows of bf16 = 64 KB at
-  // the benchmark shape) their rows crowd into the same memory channels;
-  // 64 extra columns (128 bytes) spread them
-  const int64_t KT = dw_batch * RP + kPanelPad;
+  // columns of H_c^T and dZ^T (the rows of a dW batch)
+  const int64_t KT = dw_batch * RP;
   const int64_t chunk = pl.chunk;
-  const int64_t ldzc = chunk ? chunk + kPanelPad : dm.V;
-  const int64_t zt_rows = chunk ? chunk : dm.V;     // rows of dZ^T
+  const int64_t zt_rows = chunk ? chunk : dm.V;     // vocabulary ids of dZ (columns) and dZ^T (rows)
 
   size_t off = 0;
   char* b = static_cast<char*>(base);
@@ -92,7 +88,7 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
     w.part_m = static_cast<float*>(take(nvt * RP * 4));
     w.part_s = static_cast<float*>(take(nvt * RP * 4));
     w.Hc = static_cast<uint16_t*>(take(RP * dm.d * 2));
-    w.dZ = static_cast<uint16_t*>(take(RP * ldzc * 2));
+    w.dZ = static_cast<uint16_t*>(take(RP * zt_rows * 2));
   };
   Workspace w;
   w.dbar = static_cast<double*>(take(dm.B * 8));
@@ -111,7 +107,6 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
   w.dw_batch = dw_batch;
   w.KT = KT;
   w.chunk = chunk;
-  w.ldzc = ldzc;
   w.g_used = (int)G;
   take_unit(w);
   for (int64_t u = 1; u < n_units; ++u) {
@@ -141,7 +136,7 @@ static Plan default_plan(const Dims& dm, int retain, int f32) {
   if (retain) G = std::min<int64_t>(G, dm.n_t);
   const int64_t RP = G * NP;
   const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, 4 * kGiB / (RP * dm.d * 4)));
-  const int64_t dw_batch = kDwUnits * RP + kPanelPad <= kMaxPanelLd ? kDwUnits : 1;
+  const int64_t dw_batch = kDwUnits * RP <= kMaxColumns ? kDwUnits : 1;
   return Plan{G, dw_batch, n_split, 0, retain, f32};
 }
 
@@ -220,7 +215,7 @@ static int choose_plan(const bgpo_problem* p, Plan* out) {
     double best_cost = 0.0;
     for (int64_t G = max_unit(dm); G >= 1; --G) {
       for (int64_t dwb = kDwUnits; dwb >= 1; --dwb) {
-        if (dwb * G * NP + kPanelPad > kMaxPanelLd) continue;
+        if (dwb * G * NP > kMaxColumns) continue;
         const int64_t ns_max = std::max<int64_t>(1, std::min<int64_t>(16, 4 * kGiB / (G * NP * p->d * 4)));
         for (int64_t ns = 1; ns <= ns_max; ++ns) {
           const Plan pl{G, dwb, ns, 0, 0, f32};
@@ -256,7 +251,7 @@ static int choose_plan(const bgpo_problem* p, Plan* out) {
   Plan best{};
   double best_cost = 0.0;
   for (int64_t G = max_unit(dm); G >= 1; --G) {
-    if (G * NP + kPanelPad > kMaxPanelLd) continue;
+    if (G * NP > kMaxColumns) continue;
     for (int64_t C : widths) {
       for (int64_t ns : {4, 2, 1}) {
         const Plan pl{G, 1, ns, C, 0, f32};
@@ -342,14 +337,15 @@ static int plan_problem(const bgpo_problem* p, Plan* pl) {
     return BGPO_ERR_UNSUPPORTED;
   const int st = choose_plan(p, pl);
   if (st != BGPO_OK) return st;
-  // H_c^T and dZ^T (leading dimension KT) are operand panels of the dW GEMM.
-  // One unit's row capacity stays within 65535 * 64 by construction; with
-  // every sample retained KT grows with n_t and is bounded here.
-  static_assert(int64_t(65535) * 64 / 256 * 256 + kPanelPad <= kMaxPanelLd,
-                "constant-mode KT must fit a panel");
+  // H_c^T and dZ^T hold KT columns (32-bit column offsets in the sample
+  // records).  One unit's row capacity stays within 65535 * 64 by
+  // construction; with every sample retained KT grows with n_t and is
+  // bounded here.
+  static_assert(int64_t(65535) * 64 / 256 * 256 * kDwUnits <= kMaxColumns,
+                "constant-mode KT must fit the column range");
   Workspace w;
   workspace_layout(Dims{p->B, p->L, p->d, p->V, p->n_t}, *pl, nullptr, &w, nullptr);
-  if (w.KT > kMaxPanelLd) return BGPO_ERR_UNSUPPORTED;
+  if (w.KT > kMaxColumns) return BGPO_ERR_UNSUPPORTED;
   return BGPO_OK;
 }
 

@@ -1,12 +1,19 @@
 // The bf16 MFMA GEMM core for gfx950 and its epilogues.
 //
 // Every contraction of the ELBO head is written in one "NT" form,
-//     C[m][n] = sum_k A[m][k] * B[n][k]      (A, B row-major, K contiguous),
+//     C[m][n] = sum_k A[m][k] * B[n][k]      (K contiguous in both),
 // so both operands load as 16-byte K-contiguous vectors that match the MFMA
 // operand layouts directly:
 //   forward               Z^T[v][row] = WT[v][:] . Hc[row][:]     (K = d)
 //   dX (split over V)     dX^T[c][row] = W[c][:] . dZ[row][:]     (K = V)
 //   dW                    dW^T[v][c]  += dZT[v][:] . HcT[c][:]    (K = rows)
+// Operand layouts: the head weights (WT, and W in the dX GEMM) are
+// row-major; the per-unit operands (Hc, dZ, dZT, HcT) are K-slab-major:
+// element (r, k) of a matrix with R rows per slab sits at
+// ((k / 64) R + r) 64 + k % 64, so the 64-deep slab of a 256-row panel that
+// one pipeline stage loads is 32 KB of contiguous memory.  (Row-major, with
+// rows V or the row count long, each slab of a panel touched 256 rows far
+// apart, and the loads ran slower.)
 // The logits are produced as Z^T (vocabulary along M) so that each lane holds
 // vocabulary entries of few rows: the per-row max / sum-exp reductions are
 // in-lane plus lane swaps.  dX and dW are produced transposed and stored
@@ -36,9 +43,9 @@ enum EpiKind { EPI_FWD = 0, EPI_FWDU = 1, EPI_F32_STORE = 2, EPI_F32_ACCUM = 3, 
 
 struct GemmParams {
   const uint16_t* A;
-  int64_t lda;
+  int64_t lda;               // row-major A: elements per row; slab-major A: rows per slab
   const uint16_t* B;
-  int64_t ldb;
+  int64_t ldb;               // rows per slab (B is always slab-major)
   int M, N, K;               // static extents
   int dyn_m, dyn_n, dyn_k;   // extents taken from the device sample metadata
   int dyn_split;             // K split taken from the metadata (dX)
@@ -53,10 +60,10 @@ struct GemmParams {
   float* part_m;             // FWD: per-128-vocabulary-slice (max, sum) partials [M/WM][ldp]
   float* part_s;
   int64_t ldp;
-  uint16_t* dZ;              // FWDU: exponentials u, [rows][ldz]; DZ: the chunk's dZ [rows][ldz]
-  int64_t ldz;
-  uint16_t* dZT;             // DZ: the chunk's dZ^T [v][ldzt] (columns from the unit's col_off)
-  int64_t ldzt;
+  uint16_t* dZ;              // FWDU: exponentials u; DZ: the chunk's dZ (slab-major, ldz rows
+  int64_t ldz;               // per slab)
+  uint16_t* dZT;             // DZ: the chunk's dZ^T (slab-major, ldzt rows per slab; columns
+  int64_t ldzt;              // from the unit's col_off)
   const float* lse2;         // DZ: per-row log2-sum-exp2, gradient scale and target id
   const float* rscale;
   const int32_t* rtgt;
@@ -141,7 +148,7 @@ __device__ __forceinline__ void epi_f32_16t(const f32x4 (&acc)[TM][TN], float* o
   }
 }
 
-template <int EPI, int BM, int BN, int BK, int STAGES>
+template <int EPI, bool SLAB_A, int BM, int BN, int BK, int STAGES>
 __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
 #if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature
   constexpr int WM = 128, WN = 128;
@@ -150,6 +157,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   constexpr int TM = WM / 16, TN = WN / 16;
   // 64-deep slabs hold two 32-deep MFMA sub-steps between barriers
   static_assert(C::NWAVES == 4 && BK == 64, "four waves, 64-deep slabs");
+  // A is slab-major in the dW GEMM (dZ^T), row-major (W^T, W) in the others;
+  // B is always slab-major
+  constexpr bool kSlabA = SLAB_A;
   __shared__ uint4 smem[STAGES * (BM + BN) * KCH];
   uint4* As = smem;                           // [STAGES][BM][KCH]
   uint4* Bs = smem + STAGES * BM * KCH;       // [STAGES][BN][KCH]
@@ -242,11 +252,17 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
 
     // Operand panels as buffer resources; each load instruction moves 64
     // lanes x 16 bytes straight into LDS, the XOR swizzle applied on the
-    // global side; rows past the matrix are clamped to its last row.
-    const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.A + (int64_t)m0 * p.lda), (short)0, 0x7FFFFFFF, 0x00020000);
-    const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.B + (int64_t)n0 * p.ldb), (short)0, 0x7FFFFFFF, 0x00020000);
+    // global side; rows past the matrix are clamped to its last row.  A
+    // row-major panel is one descriptor with the slab's K offset as the
+    // scalar offset; a slab-major panel gets a descriptor per slab (its
+    // slabs lie rows-per-slab x 128 bytes apart, beyond 32-bit offsets), with
+    // rows 128 bytes apart inside it.
+    const char* const a_tile = reinterpret_cast<const char*>(p.A + (int64_t)m0 * (kSlabA ? 64 : p.lda));
+    const char* const b_tile = reinterpret_cast<const char*>(p.B + (int64_t)n0 * 64);
+    const int64_t a_slab = p.lda * 128, b_slab = p.ldb * 128;   // bytes per slab (slab-major)
+    const int a_row = kSlabA ? 128 : (int)p.lda * 2;            // bytes per row
+    const __amdgpu_buffer_rsrc_t a_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)a_tile, (short)0, 0x7FFFFFFF, 0x00020000);
     constexpr int RPI = 64 / KCH;                        // rows per load instruction
     constexpr int A_INS = BM / RPI / C::NWAVES, B_INS = BN / RPI / C::NWAVES;
     static_assert(A_INS + B_INS == BK / 4, "one slab load per 256 / BK MFMAs");
@@ -256,14 +272,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       const int g = wave * A_INS + q, row = g * RPI + lane / KCH;
       const int c = (lane % KCH) ^ C::swz(row);
       const int rr = min(m0 + row, M - 1) - m0;
-      a_voff[q] = (uint32_t)(rr * p.lda * 2 + c * 16);
+      a_voff[q] = (uint32_t)(rr * a_row + c * 16);
     }
 #pragma unroll
     for (int q = 0; q < B_INS; ++q) {
       const int g = wave * B_INS + q, row = g * RPI + lane / KCH;
       const int c = (lane % KCH) ^ C::swz(row);
       const int rr = min(n0 + row, N - 1) - n0;
-      b_voff[q] = (uint32_t)(rr * p.ldb * 2 + c * 16);
+      b_voff[q] = (uint32_t)(rr * 128 + c * 16);
     }
     if (nk > 0) {
       // S-stage ring of K slabs: slab q lives in stage q % S,
@@ -272,16 +288,25 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       constexpr int NINS = A_INS + B_INS;
       auto issue_one = [&](int q, int stage, int e) {   // load instruction e of slab q
         const int qc = min(q, nk - 1);
-        const int soff = (int)((kb + (int64_t)qc * BK) * 2);
+        const int64_t ks = kb / BK + qc;                  // slab index in K
         if (e < A_INS) {
           uint4* dst = As + stage * BM * KCH + (wave * A_INS + e) * 64;
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              a_rsrc, (__attribute__((address_space(3))) void*)dst, 16, a_voff[e], soff, 0, 0);
+          if constexpr (kSlabA) {
+            const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(a_tile + ks * a_slab), (short)0, 0x7FFFFFFF, 0x00020000);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                r, (__attribute__((address_space(3))) void*)dst, 16, a_voff[e], 0, 0, 0);
+          } else {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                a_rsrc, (__attribute__((address_space(3))) void*)dst, 16, a_voff[e],
+                (int)(ks * BK * 2), 0, 0);
+          }
         } else {
           uint4* dst = Bs + stage * BN * KCH + (wave * B_INS + e - A_INS) * 64;
+          const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+              (void*)(b_tile + ks * b_slab), (short)0, 0x7FFFFFFF, 0x00020000);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              b_rsrc, (__attribute__((address_space(3))) void*)dst, 16, b_voff[e - A_INS], soff,
-              0, 0);
+              r, (__attribute__((address_space(3))) void*)dst, 16, b_voff[e - A_INS], 0, 0, 0);
         }
       };
 #pragma unroll
@@ -307,9 +332,13 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         }
       };
       // one sub-step on fragment set h: its 64 MFMAs, the reads of sub-step
-      // (nst, nks) into set 1 - h and, with `loads`, slab lq into stage lst
+      // (nst, nks) into set 1 - h and, with `loads`, slab lq into stage lst.
+      // The sub-step before a barrier issues its 16 reads after every third
+      // of its first 48 MFMAs, so that the reads are complete when the wave
+      // reaches the barrier's wait (measured 1 % faster than reads spread to
+      // the last MFMA); the other sub-step reads after every fourth.
       constexpr int LEVERY = TM * TN / NINS;   // MFMAs per slab load
-      auto step = [&](int h, int nst, int nks, bool loads, int lq, int lst) {
+      auto step = [&](int h, int nst, int nks, bool loads, int lq, int lst, bool pre) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -317,7 +346,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
             const int m = i * TN + j;
             BGPO_MFMA16(acc[i][j], fa[h][i], fb[h][j]);
             if (loads && m % LEVERY == 1) issue_one(lq, lst, m / LEVERY);
-            if ((m & 3) == 3) rd(fa[1 - h], fb[1 - h], nst, nks, m >> 2);
+            if (pre) {
+              if (m % 3 == 0 && m / 3 < TM + TN) rd(fa[1 - h], fb[1 - h], nst, nks, m / 3);
+            } else if ((m & 3) == 3) {
+              rd(fa[1 - h], fb[1 - h], nst, nks, m >> 2);
+            }
             __builtin_amdgcn_sched_barrier(0);
           }
       };
@@ -328,7 +361,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // stay in their registers across the whole loop
       for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt % STAGES;
-        step(0, cur, 1, false, 0, 0);
+        step(0, cur, 1, false, 0, 0, true);
         // slab kt + 1 landed (own loads) and, after the barrier, every wave
         // is done with stage `cur`: refill it with slab kt + S during the
         // second sub-step, which also reads slab kt + 1's first fragments
@@ -336,7 +369,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
-        step(1, (kt + 1) % STAGES, 0, true, kt + STAGES, cur);
+        step(1, (kt + 1) % STAGES, 0, true, kt + STAGES, cur, false);
       }
       // drain the ring (outstanding re-loads) before the epilogue may reuse LDS
       __builtin_amdgcn_s_waitcnt(0);
@@ -370,7 +403,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // EPI_FWDU stages the tile's exponentials in LDS (free once the ring is
       // drained; 256 rows x 256 vocabulary ids x fp16 = the ring's 128 KB) as
       // [row][vocabulary], 16-byte chunk c of row r at chunk c ^ (r mod 32),
-      // and then writes whole rows (two 512-byte rows per instruction).
+      // and then writes whole rows (two rows of 256 ids per instruction, each
+      // four 128-byte lines of the slab-major dZ).
       char* stage_u = reinterpret_cast<char*>(smem);
       static_assert(!kStore || (BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2),
                     "staging tile: 512-byte rows that fit the ring");
@@ -433,7 +467,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
           const int m = m0 + 8 * (pc ^ (row & 31));
           const uint4 v = *reinterpret_cast<const uint4*>(stage_u + row * 512 + pc * 16);
           if (n0 + row < N && m < M)
-            *reinterpret_cast<uint4*>(p.dZ + (int64_t)(n0 + row) * p.ldz + m) = v;
+            *reinterpret_cast<uint4*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + n0 + row) * 64 + (m & 63)) = v;
         }
       }
     } else if constexpr (EPI == EPI_DZ) {
@@ -445,8 +479,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // gradient scale of the response's bound term); padding rows get exact
       // zeros.  The bf16 tile is staged in LDS as [row][vocabulary] (16-byte
       // chunk c of row r at chunk c ^ (r mod 32), as the exponentials above),
-      // written as whole 512-byte rows of dZ[row][m] (the dX GEMM's operand)
-      // and read back down its columns for dZ^T[m][row] (the dW GEMM's).
+      // written as whole rows of dZ (the dX GEMM's operand) and read back
+      // down its columns for dZ^T (the dW GEMM's), both slab-major.
       char* stage = reinterpret_cast<char*>(smem);
       static_assert(BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2,
                     "staging tile: 512-byte rows that fit the ring");
@@ -487,23 +521,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         const int m = m0 + 8 * (pc ^ (row & 31));
         const uint4 v = *reinterpret_cast<const uint4*>(stage + row * 512 + pc * 16);
         if (n0 + row < N && m < M)
-          *reinterpret_cast<uint4*>(p.dZ + (int64_t)(n0 + row) * p.ldz + m) = v;
+          *reinterpret_cast<uint4*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + n0 + row) * 64 + (m & 63)) = v;
       }
       // dZ^T: lane l of an instruction takes vocabulary row ml = 64 k + l of
       // the tile (64 lanes read 128 contiguous bytes of one staged row: no
       // bank conflicts), wave w the 8-row chunks 8 w .. 8 w + 7; each lane
-      // assembles 8 consecutive rows into one 16-byte store.  Consecutive
-      // stores of a lane fill consecutive 16-byte pieces of the same dZ^T
-      // row, so every 128-byte line is complete after eight of them (wider
-      // per-lane reads that spread a lane's stores over four rows left four
-      // times as many partly written lines open, overflowing the L2).
+      // assembles 8 consecutive rows into one 16-byte store.  A wave's 64
+      // rows are one 64-column slab of dZ^T, so a lane's eight stores fill
+      // the 128-byte line of its vocabulary row in that slab (wider per-lane
+      // reads that spread a lane's stores over four rows left four times as
+      // many partly written lines open, overflowing the L2).
       int lm = lane;
       asm volatile("" : "+v"(lm));
 #pragma unroll
       for (int k = 0; k < BM / 64; ++k) {
         const int ml = 64 * k + lm;
         const int cw = ((ml >> 3) << 4) + (ml & 7) * 2;   // chunk base (before the XOR) and offset
-        uint16_t* const zt = p.dZT + (int64_t)(m0 + ml) * p.ldzt + zt_col + n0;
+        static_assert(ROWS_PER_WAVE == 64, "one dZ^T column slab per wave");
+        uint16_t* const zt = p.dZT + ((int64_t)((zt_col + n0) / 64 + wave) * p.ldzt + m0 + ml) * 64;
         const bool row_live = m0 + ml < M;
 #pragma unroll
         for (int c = 0; c < ROWS_PER_WAVE / 8; ++c) {
@@ -516,7 +551,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
             const uint32_t b = *reinterpret_cast<const uint16_t*>(stage + rb * 512 + (cw ^ ((rb & 31) << 4)));
             wv[t] = a | (b << 16);
           }
-          if (row_live) *reinterpret_cast<uint4*>(zt + r0) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+          if (row_live) *reinterpret_cast<uint4*>(zt + 8 * c) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
         }
       }
     } else {
@@ -557,16 +592,16 @@ hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool sto
                            hipStream_t s) {
   GemmParams p = base_params();
   p.A = ws.WT; p.lda = d;
-  p.B = ws.Hc; p.ldb = d;
+  p.B = ws.Hc; p.ldb = ws.RP;
   p.M = V; p.K = d; p.dyn_n = 1; p.meta = ws.unit();
   p.k_split = d;
   p.part_m = ws.part_m; p.part_s = ws.part_s; p.ldp = ws.RP;
   p.group_m = kGroupMFwd;
   if (store_u) {
-    p.dZ = ws.dZ; p.ldz = V;
-    k_gemm4w<EPI_FWDU, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    p.dZ = ws.dZ; p.ldz = ws.RP;
+    k_gemm4w<EPI_FWDU, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   } else {
-    k_gemm4w<EPI_FWD, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    k_gemm4w<EPI_FWD, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   }
   return hipGetLastError();
 }
@@ -576,23 +611,23 @@ hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, 
   // dX^T[c][row] = W[c][:] . dZ[row][:], stored transposed: dx_part[row][c]
   GemmParams p = base_params();
   p.A = W; p.lda = V;
-  p.B = ws.dZ; p.ldb = V;
+  p.B = ws.dZ; p.ldb = ws.RP;
   p.M = d; p.K = V; p.dyn_n = 1; p.meta = ws.unit();
   p.dyn_split = 1;
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
-  k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s) {
   GemmParams p = base_params();
-  p.A = ws.dZT; p.lda = ws.KT;
-  p.B = ws.HcT; p.ldb = ws.KT;
+  p.A = ws.dZT; p.lda = V;
+  p.B = ws.HcT; p.ldb = d;
   p.M = V; p.N = d; p.dyn_k = 1; p.meta = ws.unit();
   p.group_m = kGroupMdW;
   p.out = dW; p.ldo = V;
-  k_gemm4w<EPI_F32_ACCUM, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  k_gemm4w<EPI_F32_ACCUM, true, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -601,14 +636,14 @@ hipError_t launch_gemm_recompute(const Workspace& ws, int d, int v0, int width, 
   // Z^T[v][row] for the chunk's ids v0 .. v0 + width - 1, epilogue -> dZ, dZ^T
   GemmParams p = base_params();
   p.A = ws.WT + (int64_t)v0 * d; p.lda = d;
-  p.B = ws.Hc; p.ldb = d;
+  p.B = ws.Hc; p.ldb = ws.RP;
   p.M = width; p.K = d; p.dyn_n = 1; p.meta = ws.unit();
   p.k_split = d;
   p.group_m = kGroupMFwd;
   p.lse2 = ws.lse2; p.rscale = ws.row_scale; p.rtgt = ws.row_tgt; p.v0 = v0;
-  p.dZ = ws.dZ; p.ldz = ws.ldzc;
-  p.dZT = ws.dZT; p.ldzt = ws.KT;
-  k_gemm4w<EPI_DZ, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  p.dZ = ws.dZ; p.ldz = ws.RP;
+  p.dZT = ws.dZT; p.ldzt = ws.chunk;
+  k_gemm4w<EPI_DZ, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -618,15 +653,15 @@ hipError_t launch_gemm_dx_chunk(const Workspace& ws, const uint16_t* W, int d, i
   // the chunk as the unit's record says; the first chunk stores the partials
   GemmParams p = base_params();
   p.A = W + v0; p.lda = V;
-  p.B = ws.dZ; p.ldb = ws.ldzc;
+  p.B = ws.dZ; p.ldb = ws.RP;
   p.M = d; p.K = width; p.dyn_n = 1; p.meta = ws.unit();
   p.dyn_split = 1;
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
   if (first)
-    k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   else
-    k_gemm4w<EPI_F32_ACCUM, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    k_gemm4w<EPI_F32_ACCUM, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -634,12 +669,12 @@ hipError_t launch_gemm_dw_chunk(const Workspace& ws, float* dW, int d, int V, in
                                 int grid, hipStream_t s) {
   // dW^T[v0 + m][c] += dZ^T[m][:] . H_c^T[c][:] (K = the unit's rows)
   GemmParams p = base_params();
-  p.A = ws.dZT; p.lda = ws.KT;
-  p.B = ws.HcT; p.ldb = ws.KT;
+  p.A = ws.dZT; p.lda = ws.chunk;
+  p.B = ws.HcT; p.ldb = d;
   p.M = width; p.N = d; p.dyn_k = 1; p.meta = ws.unit();
   p.group_m = kGroupMdW;
   p.out = dW + v0; p.ldo = V;
-  k_gemm4w<EPI_F32_ACCUM, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  k_gemm4w<EPI_F32_ACCUM, true, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -653,7 +688,8 @@ int gemm_grid(int device) {
 
 }  // namespace bgpo
 
-// ---- test hook: the GEMM core alone, C[m][n] = sum_k A[m][k] B[n][k] in fp32 ----
+// ---- test hook: the GEMM core alone (the dX GEMM's kernel: A slab-major, B
+// row-major), C[m][n] = sum_k A[m][k] B[n][k] in fp32 ----
 extern "C" int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
                                  int32_t K, void* stream) {
   using namespace bgpo;
@@ -661,12 +697,12 @@ extern "C" int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C,
   if ((int64_t)((M + 255) / 256) * ((N + 255) / 256) >= (int64_t(1) << 30)) return -1;
   // the production kernel stores C^T of its operands' product: swap them
   GemmParams p = base_params();
-  p.A = B; p.lda = K; p.B = A; p.ldb = K;
+  p.A = B; p.lda = K; p.B = A; p.ldb = M;
   p.M = N; p.N = M; p.K = K; p.k_split = K;
   p.out = C; p.ldo = N;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -3;
-  k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
+  k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
@@ -680,13 +716,13 @@ extern "C" int bgpo_test_gemm_split(const uint16_t* A, const uint16_t* B, float*
   // slice s covers K range [s * ks, min(K, (s + 1) * ks)) with ks a multiple
   // of 64; trailing slices can be empty (their block is stored as zeros)
   GemmParams p = base_params();
-  p.A = B; p.lda = K; p.B = A; p.ldb = K;
+  p.A = B; p.lda = K; p.B = A; p.ldb = M;
   p.M = N; p.N = M; p.K = K;
   p.n_split = n_split;
   p.k_split = ((K + n_split - 1) / n_split + 63) / 64 * 64;
   p.out = C; p.ldo = N; p.split_stride = (int64_t)M * N;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -3;
-  k_gemm4w<EPI_F32_STORE, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
+  k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }

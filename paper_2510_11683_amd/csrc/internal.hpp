@@ -16,12 +16,16 @@ constexpr int kVocabTile = 128;
 
 constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
 
-// The GEMMs address each 256-row operand panel through one buffer descriptor
-// with 32-bit byte offsets below 2^31, so a bf16 operand's leading dimension
-// must stay at or below this.
-constexpr int64_t kMaxPanelLd = (int64_t(1) << 22) - 1;
-// Padding of the H_c^T / dZ^T leading dimension beyond the row capacity.
-constexpr int64_t kPanelPad = 64;
+// Column capacity of H_c^T / dZ^T (the rows of a dW batch; the column
+// offsets of the sample records are 32-bit).
+constexpr int64_t kMaxColumns = int64_t(1) << 30;
+
+// K-slab-major layout of a bf16 operand with R rows per slab: element (r, k)
+// at ((k / 64) R + r) 64 + k % 64 (the GEMMs' operand layout: one 64-deep
+// slab of 256 consecutive rows is 32 KB of contiguous memory).
+__host__ __device__ inline int64_t slab_index(int64_t R, int64_t r, int64_t k) {
+  return ((k >> 6) * R + r) * 64 + (k & 63);
+}
 
 // Device-resident bookkeeping written by the mask kernel, one record per
 // sample.  Samples are processed in units of up to G consecutive samples whose
@@ -59,10 +63,13 @@ struct Workspace {
   int32_t* seg_off;    // [G*(B+1)]    first row of each (sample, response), unit row space
   uint32_t* t24;       // [G*B]        integer timestep of each (sample, response)
   float* seq_scale;    // [G*B]        gradient scale s of each (sample, response)
-  uint16_t* Hc;        // [RP, d]      gathered masked hidden rows (bf16)
-  uint16_t* HcT;       // [d, KT]      the same, transposed; units of a dW batch side by side
-  uint16_t* WT;        // [V, d]       W_head transposed (bf16)
-  uint16_t* Wb;        // [d, V]       W_head rounded to bf16 (fp32 inputs only, else NULL)
+  // (slab-major: a matrix with R rows per slab and K columns, see slab_index)
+  uint16_t* Hc;        // [RP rows, d] gathered masked hidden rows (bf16), slab-major
+  uint16_t* HcT;       // [d rows, KT] the same, transposed, units of a dW batch side by side,
+                       // slab-major
+  uint16_t* WT;        // [V, d]       W_head transposed (bf16), row-major
+  uint16_t* Wb;        // [d, V]       W_head rounded to bf16, row-major (fp32 inputs only,
+                       // else NULL)
   float* part_m;       // [nvt, RP]    per-vocabulary-slice max (log2 units)
   float* part_s;       // [nvt, RP]    per-vocabulary-slice sum of 2^(z*log2e - max)
   float* ztgt;         // [RP]         target logit
@@ -73,20 +80,20 @@ struct Workspace {
   float* inv_rms;      // [RP]         final-RMSNorm 1/rms of each compacted row
   void* mask_scratch;  // mask_scratch_bytes(B, L): the multi-block mask passes
   float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks of a sample
-  uint16_t* dZ;        // stored mode: [RP, V] s (softmax - onehot), bf16 (first the fp16
-                       // exponentials); recompute mode: [RP, chunk], one vocabulary chunk
-  uint16_t* dZT;       // stored mode: [V, KT] the same, transposed, units of a dW batch side
-                       // by side; recompute mode: [chunk, KT], one chunk
+  uint16_t* dZ;        // stored mode: [RP rows, V] s (softmax - onehot), bf16 (first the fp16
+                       // exponentials); recompute mode: [RP rows, chunk], one vocabulary
+                       // chunk; slab-major
+  uint16_t* dZT;       // stored mode: [V rows, KT] the same, transposed, units of a dW batch
+                       // side by side; recompute mode: [chunk rows, KT], one chunk;
+                       // slab-major
   float* dx_part;      // [S, RP, d]   split-vocabulary partial dX
   int64_t P, NP, nvt;
   int64_t G;           // samples per unit
   int64_t RP;          // G * NP: row capacity of a unit
   int64_t n_split;     // capacity of dx_part in splits (the unit's count is in its meta)
   int64_t dw_batch;    // units whose dW contributions share one GEMM
-  int64_t KT;          // dw_batch * RP + pad: leading dimension of H_c^T and dZ^T
+  int64_t KT;          // dw_batch * RP: columns of H_c^T and dZ^T
   int64_t chunk;       // 0: stored exponentials; > 0: recompute backward, vocabulary chunk width
-  int64_t ldzc;        // recompute mode: row pitch of the chunk's dZ (chunk + pad: no
-                       // power-of-two pitch)
   int g_used;          // samples in the current unit (host side; its record meta[g_used - 1]
                        // describes the unit)
   const SampleMeta* unit() const { return meta + (g_used - 1); }
@@ -166,8 +173,8 @@ hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const void* x, b
                                     hipStream_t s);
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s);
 // recompute mode, vocabulary chunk [v0, v0 + width): the chunk's logits from
-// W^T and H_c, turned into dZ = s (softmax - onehot) (bf16, [row][v] and
-// [v][row]); dX^T partials (+)= W[:, chunk] . dZ^T (first chunk: stored);
+// W^T and H_c, turned into dZ = s (softmax - onehot) (bf16, dZ and dZ^T);
+// dX^T partials (+)= W[:, chunk] . dZ^T (first chunk: stored);
 // dW[:, chunk] += H_c^T . dZ
 hipError_t launch_gemm_recompute(const Workspace& ws, int d, int v0, int width, int grid,
                                  hipStream_t s);

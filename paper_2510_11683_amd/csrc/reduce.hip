@@ -13,20 +13,21 @@
 
 namespace bgpo {
 
-// One wave per row: 64 lanes split the d-long dot product.
+// One wave per row: 64 lanes split the d-long dot product (Hc slab-major with
+// RP rows per slab: each group of 8 lanes reads one 128-byte slab row).
 __global__ __launch_bounds__(256) void k_target_logit(const uint16_t* __restrict__ Hc,
                                                       const uint16_t* __restrict__ WT,
                                                       const int32_t* __restrict__ row_tgt,
                                                       const SampleMeta* __restrict__ meta,
-                                                      float* __restrict__ ztgt, int d) {
+                                                      float* __restrict__ ztgt, int d,
+                                                      int64_t RP) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= meta->n_rows) return;
-  const uint16_t* h = Hc + (int64_t)row * d;
   const uint16_t* w = WT + (int64_t)row_tgt[row] * d;
   float acc = 0.f;
   for (int k = lane * 8; k < d; k += 64 * 8) {
-    const uint4 hv = *reinterpret_cast<const uint4*>(h + k);
+    const uint4 hv = *reinterpret_cast<const uint4*>(Hc + slab_index(RP, row, k));
     const uint4 wv = *reinterpret_cast<const uint4*>(w + k);
     const uint32_t ha[4] = {hv.x, hv.y, hv.z, hv.w}, wa[4] = {wv.x, wv.y, wv.z, wv.w};
 #pragma unroll
@@ -42,7 +43,7 @@ __global__ __launch_bounds__(256) void k_target_logit(const uint16_t* __restrict
 
 hipError_t launch_target_logit(const Workspace& ws, int d, hipStream_t s) {
   k_target_logit<<<(unsigned)(ws.RP / 4), 256, 0, s>>>(ws.Hc, ws.WT, ws.row_tgt, ws.unit(), ws.ztgt,
-                                                       d);
+                                                       d, ws.RP);
   return hipGetLastError();
 }
 
@@ -229,30 +230,35 @@ hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, in
 // Eq. per_step_loss, d l / d z = (onehot - p) / t; s carries -loss_scale dg/dl
 // and the 1/t.)  At the target the value comes from the fp32 target logit,
 // s (2^(z_y log2e - lse2) - 1), not from the rounded u.  Padded rows become
-// zeros.  One workgroup per (128-row chunk, slice): the rows are read and
-// rewritten in 256-byte runs, and the transposed copy dZ^T[v][col_off + row]
-// is assembled in LDS and written as 256-byte runs of 128 rows.
-constexpr int kGradRows = 128;
+// zeros.  Both dZ (RP rows per slab) and dZ^T (V rows per slab) are
+// slab-major, and one workgroup takes one 64-id slab of 256 rows: its part of
+// dZ is one contiguous 32 KB block, read and rewritten in place, and its part
+// of dZ^T (64 ids x 256 columns) four contiguous 8 KB blocks, assembled in
+// LDS.
+constexpr int kGradRows = 256;
 static_assert(kRowPad % kGradRows == 0, "padded row counts must hold whole chunks");
 
 __global__ __launch_bounds__(256) void k_softmax_grad(
     const float* __restrict__ part_m, const float* __restrict__ lse2,
     const float* __restrict__ row_scale, const float* __restrict__ ztgt,
     const int32_t* __restrict__ row_tgt, const SampleMeta* __restrict__ meta,
-    uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT, int V, int64_t ldp, int64_t ldzt) {
+    uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT, int V, int64_t ldp) {
   constexpr int kPairs = kGradRows / 2;                  // words per vocabulary id in the tile
   __shared__ float s_c[kGradRows], s_oh[kGradRows];
   __shared__ int s_y[kGradRows];
   // [v][row pair] words (row 2k, row 2k+1), row pair k of vocabulary id v at
-  // word v * kPairs + (k ^ 4 (v / 8)): the 16 lanes that read one row's slice
-  // (v / 8 = 0 .. 15) write 16 different banks, and aligned groups of 4 row
-  // pairs stay together and in order for the 16-byte reads of dZ^T
-  __shared__ __align__(16) uint32_t tile[kVocabTile * kPairs];
-  const int h = blockIdx.x, r0 = blockIdx.y * kGradRows;
+  // word v * kPairs + (k ^ sw(v)), sw(v) = 8 (v / 8) ^ 32 (v % 2): the 64
+  // lanes of a store (8 row pairs x 8 ids 8 apart) hit 64 different banks,
+  // two ids in a row use different halves of the banks for the 16-byte reads
+  // of dZ^T, and aligned groups of 4 row pairs stay together and in order
+  __shared__ __align__(16) uint32_t tile[64 * kPairs];
+  auto sw = [](int v) { return (8 * (v >> 3)) ^ (32 * (v & 1)); };
+  const int slab = blockIdx.x, r0 = blockIdx.y * kGradRows;
   if (r0 >= meta->n_rows_pad) return;   // n_rows_pad is a multiple of 256: chunks are whole
   const int N = meta->n_rows;
   const int tid = threadIdx.x;
-  if (tid < kGradRows) {
+  const int v_lo = slab * 64, h = v_lo / kVocabTile;
+  {
     const int r = r0 + tid;
     float c = 0.f, oh = 0.f;
     int y = -1;
@@ -267,15 +273,15 @@ __global__ __launch_bounds__(256) void k_softmax_grad(
     s_y[tid] = y;
   }
   __syncthreads();
-  const int v_lo = h * kVocabTile;
-  const int nv = min(kVocabTile, V - v_lo);   // 128, or 64 in a last half slice
-  const int cpr = nv / 8;                     // 16-byte chunks per row
-  // rows 2 rp and 2 rp + 1, vocabulary ids v0 .. v0 + 7
-  for (int q = tid; q < kPairs * cpr; q += 256) {
-    const int vc = q % cpr, rp = q / cpr;
+  // rows 2 rp and 2 rp + 1 (each one 128-byte slab row), ids v0 .. v0 + 7
+  uint16_t* const zb = dZ + ((int64_t)slab * ldp + r0) * 64;
+#pragma unroll
+  for (int it = 0; it < kPairs * 8 / 256; ++it) {
+    const int q = tid + 256 * it;
+    const int vc = q & 7, rp = q >> 3;
     const int ra = 2 * rp, v0 = v_lo + vc * 8;
-    uint4* pa = reinterpret_cast<uint4*>(dZ + (int64_t)(r0 + ra) * V + v0);
-    uint4* pb = reinterpret_cast<uint4*>(dZ + (int64_t)(r0 + ra + 1) * V + v0);
+    uint4* pa = reinterpret_cast<uint4*>(zb + ra * 64 + vc * 8);
+    uint4* pb = pa + 8;
     uint32_t oa[4] = {0, 0, 0, 0}, ob[4] = {0, 0, 0, 0};
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -297,29 +303,31 @@ __global__ __launch_bounds__(256) void k_softmax_grad(
     }
     *pa = make_uint4(oa[0], oa[1], oa[2], oa[3]);
     *pb = make_uint4(ob[0], ob[1], ob[2], ob[3]);
-    const int w = rp ^ (4 * vc);              // vl / 8 == vc for all 8 ids below
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int vl = vc * 8 + 2 * k;
-      tile[vl * kPairs + w] = (oa[k] & 0xFFFFu) | (ob[k] << 16);
-      tile[(vl + 1) * kPairs + w] = (oa[k] >> 16) | (ob[k] & 0xFFFF0000u);
+      tile[vl * kPairs + (rp ^ sw(vl))] = (oa[k] & 0xFFFFu) | (ob[k] << 16);
+      tile[(vl + 1) * kPairs + (rp ^ sw(vl + 1))] = (oa[k] >> 16) | (ob[k] & 0xFFFF0000u);
     }
   }
   __syncthreads();
-  // dZ^T: 16 lanes (128 rows, 256 bytes) per vocabulary id; lane c takes row
-  // pairs 4c .. 4c + 3, stored at 4 (c ^ (vl / 8))
-  uint16_t* zt = dZT + meta->col_off;
-  for (int q = tid; q < nv * 16; q += 256) {
-    const int vl = q >> 4, c = q & 15;
-    const uint4 v = *reinterpret_cast<const uint4*>(tile + vl * kPairs + 4 * (c ^ (vl >> 3)));
-    *reinterpret_cast<uint4*>(zt + (int64_t)(v_lo + vl) * ldzt + r0 + 8 * c) = v;
+  // dZ^T: column slab cs (64 columns = 32 row pairs) of id vl is 128 bytes;
+  // lane cc of 8 takes row pairs 4 cc .. 4 cc + 3 of it
+  const int64_t cslab0 = ((int64_t)meta->col_off + r0) / 64;
+#pragma unroll
+  for (int it = 0; it < 64 * 32 / 256; ++it) {
+    const int q = tid + 256 * it;
+    const int cs = q >> 9, vl = (q >> 3) & 63, cc = q & 7;
+    const int rp = 32 * cs + 4 * cc;
+    const uint4 v = *reinterpret_cast<const uint4*>(tile + vl * kPairs + (rp ^ sw(vl)));
+    *reinterpret_cast<uint4*>(dZT + ((cslab0 + cs) * V + v_lo + vl) * 64 + 8 * cc) = v;
   }
 }
 
 hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s) {
-  dim3 grid((unsigned)ws.nvt, (unsigned)(ws.RP / kGradRows));
+  dim3 grid((unsigned)(V / 64), (unsigned)(ws.RP / kGradRows));
   k_softmax_grad<<<grid, 256, 0, s>>>(ws.part_m, ws.lse2, ws.row_scale, ws.ztgt, ws.row_tgt,
-                                      ws.unit(), ws.dZ, ws.dZT, V, ws.RP, ws.KT);
+                                      ws.unit(), ws.dZ, ws.dZT, V, ws.RP);
   return hipGetLastError();
 }
 

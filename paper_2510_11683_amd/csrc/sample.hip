@@ -442,8 +442,9 @@ hipError_t launch_row_rms(const void* x, bool f32, int64_t stride, int B, const 
 
 // Gather: Hc[r, :] = hidden_g[idx[r], :] and HcT[:, col_off + r] for the unit's
 // rows r < N (g = row_seq[r] / B: the row's sample, hidden_g = hidden + g *
-// stride); zeros for N <= r < N_pad.  64x64 tiles staged in LDS for the
-// transposed copy.  With `gamma`, `hidden` holds the pre-norm activations and
+// stride); zeros for N <= r < N_pad.  Both are slab-major (Hc with RP rows
+// per slab, HcT with d), so each 64x64 tile of either is 8 KB of contiguous
+// memory; the tiles are staged in LDS for the transposed copy.  With `gamma`, `hidden` holds the pre-norm activations and
 // the gathered row is the final RMSNorm bf16(x * inv_rms[r] * gamma) (fp32
 // arithmetic, one rounding to bfloat16).  fp32 inputs are rounded to bf16
 // first (load_bf16x8), then treated the same way.
@@ -456,7 +457,7 @@ __global__ __launch_bounds__(256) void k_gather(const T* __restrict__ hidden,
                                                 const float* __restrict__ gamma,
                                                 const float* __restrict__ inv_rms,
                                                 uint16_t* __restrict__ Hc,
-                                                uint16_t* __restrict__ HcT, int d, int64_t ldt) {
+                                                uint16_t* __restrict__ HcT, int d, int64_t RP) {
   __shared__ uint16_t tile[64][72];
   const int r0 = blockIdx.x * 64;
   if (r0 >= meta->n_rows_pad) return;
@@ -487,7 +488,7 @@ __global__ __launch_bounds__(256) void k_gather(const T* __restrict__ hidden,
         v = make_uint4(a[0], a[1], a[2], a[3]);
       }
     }
-    *reinterpret_cast<uint4*>(Hc + (int64_t)r * d + c0 + ch * 8) = v;
+    *reinterpret_cast<uint4*>(Hc + slab_index(RP, r, c0 + ch * 8)) = v;
     *reinterpret_cast<uint4*>(&tile[row][ch * 8]) = v;
   }
   __syncthreads();
@@ -499,7 +500,7 @@ __global__ __launch_bounds__(256) void k_gather(const T* __restrict__ hidden,
 #pragma unroll
     for (int e = 0; e < 4; ++e)
       w[e] = (uint32_t)tile[rch * 8 + 2 * e][c] | ((uint32_t)tile[rch * 8 + 2 * e + 1][c] << 16);
-    *reinterpret_cast<uint4*>(HcT + (int64_t)(c0 + c) * ldt + coff + r0 + rch * 8) =
+    *reinterpret_cast<uint4*>(HcT + slab_index(d, c0 + c, (int64_t)coff + r0 + rch * 8)) =
         make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
@@ -510,11 +511,11 @@ hipError_t launch_gather(const void* hidden, bool f32, int64_t stride, int B, co
   if (f32)
     k_gather<float><<<grid, 256, 0, s>>>(static_cast<const float*>(hidden), stride, B, ws.idx,
                                          ws.row_seq, ws.unit(), gamma, ws.inv_rms, ws.Hc, ws.HcT,
-                                         d, ws.KT);
+                                         d, ws.RP);
   else
     k_gather<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(hidden), stride, B,
                                             ws.idx, ws.row_seq, ws.unit(), gamma, ws.inv_rms,
-                                            ws.Hc, ws.HcT, d, ws.KT);
+                                            ws.Hc, ws.HcT, d, ws.RP);
   return hipGetLastError();
 }
 

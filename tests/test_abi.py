@@ -198,15 +198,16 @@ def test_reserved_field_and_rmsnorm_arguments_rejected_before_hip(b):
                                      fake, fake, fake, None, ws, nbytes.value, None, None) == -1
 
 
-def test_retained_rows_bounded_by_the_dw_panel_range(b):
-    """The dW GEMM reads H_c^T and dZ^T through buffer descriptors whose byte
-    offsets stay below 2^31: with every sample retained, the kept rows (whole
-    units of samples, B*L rounded up to 256 per sample) must stay below 2^22.
-    At B*L = 2^20 a unit holds 3 samples: n_t = 3 keeps 3 * 2^20 rows, n_t = 4
-    two units (6 * 2^20); the constant mode takes any n_t."""
+def test_retained_rows_bounded_by_the_column_range(b):
+    """H_c^T and dZ^T hold one column per kept row (32-bit column offsets in
+    the sample records): with every sample retained, the kept rows (whole
+    units of samples, B*L rounded up to 256 per sample) must stay at or below
+    2^30.  At B*L = 2^20 a unit holds 3 samples: n_t = 1023 keeps 341 units
+    (1023 * 2^20 rows), n_t = 1024 one unit more; the constant mode takes any
+    n_t."""
     big = dict(B=4096, L=256, d=64, V=128, bound=3)
-    assert b.bgpo_workspace_size(_prob(b, n_t=3, retain_samples=1, **big)) > 0
-    for n_t in (4, 64):
+    assert b.bgpo_workspace_size(_prob(b, n_t=1023, retain_samples=1, **big)) > 0
+    for n_t in (1024, 4096):
         with pytest.raises(b.BgpoError) as e:
             b.bgpo_workspace_size(_prob(b, n_t=n_t, retain_samples=1, **big))
         assert e.value.status == -4

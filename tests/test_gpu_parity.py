@@ -39,6 +39,12 @@ def _gpu():
 
 # ---------------------------------------------------------------- GEMM core
 
+def _slab_major(X):
+    """[R, K] -> the K-slab-major operand layout [K/64, R, 64]."""
+    R, K = X.shape
+    return X.reshape(R, K // 64, 64).permute(1, 0, 2).contiguous()
+
+
 @pytest.mark.parametrize("M,N,K", [(300, 200, 192), (512, 768, 1024), (257, 1000, 64)])
 def test_gemm_core_matches_fp32_reference(M, N, K):
     """The GEMM core of the production kernels (bgpo_test_gemm_nt) against
@@ -48,7 +54,7 @@ def test_gemm_core_matches_fp32_reference(M, N, K):
     Bm = torch.randn(N, K, generator=g).to(torch.bfloat16)
     ref = A.double() @ Bm.double().T                      # exact products of bf16 values
     C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
-    lib().bgpo_test_gemm_nt(A.cuda(), Bm.cuda(), C)
+    lib().bgpo_test_gemm_nt(_slab_major(A).cuda(), Bm.cuda(), C)
     torch.cuda.synchronize()
     err = (C.cpu().double() - ref).abs().max().item()
     assert err <= 1e-5 * (K ** 0.5) * ref.abs().max().item() + 1e-5, err
@@ -65,7 +71,7 @@ def test_gemm_core_split_k(M, N, K, n_split):
     Bm = torch.randn(N, K, generator=g).to(torch.bfloat16)
     ref = A.double() @ Bm.double().T
     C = torch.full((n_split, M, N), float("nan"), dtype=torch.float32, device="cuda")
-    lib().bgpo_test_gemm_split(A.cuda(), Bm.cuda(), C, n_split)
+    lib().bgpo_test_gemm_split(_slab_major(A).cuda(), Bm.cuda(), C, n_split)
     torch.cuda.synchronize()
     got = C.cpu().double()
     ks = ((K + n_split - 1) // n_split + 63) // 64 * 64
