@@ -83,6 +83,8 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
     w.lse2 = static_cast<float*>(take(RP * 4));
     w.lp = static_cast<float*>(take(RP * 4));
     w.row_scale = static_cast<float*>(take(RP * 4));
+    w.row_f = static_cast<float*>(take(RP * 4));
+    w.row_bad = static_cast<uint8_t*>(take(RP));
     w.inv_rms = static_cast<float*>(take(RP * 4));
     w.mask_scratch = take(mask_scratch_bytes(dm.B, dm.L));
     w.part_m = static_cast<float*>(take(nvt * RP * 4));
@@ -405,15 +407,18 @@ static int run_forward_unit(const bgpo_problem* p, Workspace& ws, Timer& tm, int
     BGPO_TRY(launch_row_rms(act.at(j0), act.f32, act.stride, dm.B, ws, dm.d, act.eps, s));
   BGPO_TRY(launch_gather(act.at(j0), act.f32, act.stride, dm.B, act.gamma, ws, dm.d, s));
   BGPO_TRY(tm.end(act.gamma ? 2 : 1));
+  // the target logits first: the stored forward's exponent reference
+  BGPO_TRY(tm.begin(BGPO_K_ELL));
+  BGPO_TRY(launch_target_logit(ws, dm.d, s));
+  BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_FWD));
   BGPO_TRY(launch_gemm_fwd(ws, dm.d, dm.V, grid, store_u, s));
   BGPO_TRY(tm.end());
   BGPO_TRY(tm.begin(BGPO_K_ELL));
-  BGPO_TRY(launch_target_logit(ws, dm.d, s));
   BGPO_TRY(launch_combine_rows(ws, dm.V, s));
   BGPO_TRY(launch_seq_terms(ws, dm.B, dm.n_t, j0, adv, ell_old, loss_scale, ell, g, loss, flags,
                             backward, p->bound, dbar, s));
-  BGPO_TRY(tm.end(3));
+  BGPO_TRY(tm.end(2));
   return BGPO_OK;
 }
 
@@ -501,9 +506,12 @@ static bool overlaps(const double* a, const double* b, int64_t n) {
 
 namespace bgpo {
 
-// the gradient part of a unit once its scales are known.  Stored mode: dZ
-// from the kept exponentials, one dX GEMM over the whole vocabulary, the
-// unit's dZ^T columns left for the dW GEMM of its batch.  Recompute mode: per
+// the gradient part of a unit once its scales are known.  Stored mode: the
+// forward kept the exponentials in both layouts; the row factors, the target
+// entries and the scaled H_c^T columns make them dZ (up to the row factor,
+// applied to the dX rows in the reduction), then one dX GEMM over the whole
+// vocabulary; the unit's dZ^T and H_c^T columns are left for the dW GEMM of
+// its batch.  Recompute mode: per
 // vocabulary chunk, the chunk's logits -> its dZ, dX partials accumulated,
 // dW[:, chunk] accumulated.  Then each sample's rows are added into dX in
 // sample order (with the norm backward).  W_dx: the bf16 W_head the dX GEMM
@@ -513,8 +521,8 @@ static int unit_backward(const Workspace& ws, const Act& act, int j0, int j_begi
                          const Dims& dm, int grid, Timer& tm, hipStream_t s) {
   if (!ws.chunk) {
     BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
-    BGPO_TRY(launch_softmax_grad(ws, dm.V, s));
-    BGPO_TRY(tm.end());
+    BGPO_TRY(launch_grad_scale(ws, dm.d, dm.V, s));
+    BGPO_TRY(tm.end(3));
     BGPO_TRY(tm.begin(BGPO_K_DX));
     BGPO_TRY(launch_gemm_dx(ws, W_dx, dm.d, dm.V, grid, s));
     BGPO_TRY(tm.end());

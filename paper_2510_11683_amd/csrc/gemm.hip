@@ -67,6 +67,7 @@ struct GemmParams {
   const float* lse2;         // DZ: per-row log2-sum-exp2, gradient scale and target id
   const float* rscale;
   const int32_t* rtgt;
+  const float* ztgt;         // FWDU: per-row target logit (the exponent reference)
   int v0;                    // DZ: vocabulary id of row 0 of A (the chunk's first id)
 };
 
@@ -148,6 +149,40 @@ __device__ __forceinline__ void epi_f32_16t(const f32x4 (&acc)[TM][TN], float* o
   }
 }
 
+// dZ^T columns of a 256 x 256 tile staged in LDS as [row][vocabulary]
+// (16-byte chunk c of row r at chunk c ^ (r mod 32), bf16): vocabulary rows
+// m0 .. m0 + 255 of dZ^T (slab-major, ldzt rows per slab), columns
+// zt_col + n0 .. + 255.  Wave w's 64 tile rows are one 64-column slab of
+// dZ^T, in which consecutive vocabulary ids are consecutive 128-byte lines:
+// store instruction i writes ids 8 i .. 8 i + 7, lane l the 16 bytes of
+// columns 8 (l mod 8) .. + 7 of id 8 i + l / 8, i.e. 1 KB of contiguous,
+// whole lines per instruction; each lane assembles its 8 columns from 8
+// two-byte reads of the staged rows.
+template <int BM, int ROWS_PER_WAVE>
+__device__ __forceinline__ void store_dzt_columns(const char* stage, uint16_t* dZT, int64_t ldzt,
+                                                  int zt_col, int m0, int n0, int M, int wave,
+                                                  int lane) {
+  static_assert(ROWS_PER_WAVE == 64, "one dZ^T column slab per wave");
+  int lq = lane;
+  asm volatile("" : "+v"(lq));
+  const int cc = lq & 7, vq = lq >> 3;
+  uint16_t* const zt = dZT + ((int64_t)((zt_col + n0) / 64 + wave) * ldzt + m0 + vq) * 64 + cc * 8;
+  const int rbase = wave * ROWS_PER_WAVE + 8 * cc;
+#pragma unroll 4
+  for (int i = 0; i < BM / 8; ++i) {
+    const int cw = (i << 4) + vq * 2;   // id 8 i + vq: chunk i (before the XOR), offset vq
+    uint32_t wv[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int ra = rbase + 2 * t, rb = ra + 1;
+      const uint32_t a = *reinterpret_cast<const uint16_t*>(stage + ra * 512 + (cw ^ ((ra & 31) << 4)));
+      const uint32_t b = *reinterpret_cast<const uint16_t*>(stage + rb * 512 + (cw ^ ((rb & 31) << 4)));
+      wv[t] = a | (b << 16);
+    }
+    if (m0 + 8 * i < M) *reinterpret_cast<uint4*>(zt + (int64_t)i * 512) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+  }
+}
+
 template <int EPI, bool SLAB_A, int BM, int BN, int BK, int STAGES>
 __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
 #if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature
@@ -173,7 +208,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   if (p.dyn_n) { N = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_k) K = p.meta->col_end;    // batched dW: all samples' columns (multiple of 64)
   // first dZ^T column of the unit (EPI_DZ), read once into a scalar register
-  const int zt_col = EPI == EPI_DZ ? __builtin_amdgcn_readfirstlane(p.meta->col_off) : 0;
+  const int zt_col =
+      (EPI == EPI_DZ || EPI == EPI_FWDU) ? __builtin_amdgcn_readfirstlane(p.meta->col_off) : 0;
   int n_split = p.n_split;
   int64_t k_split = p.k_split;
   if (p.dyn_split) {
@@ -383,9 +419,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // 2^(z log2e - m), in log2 units, written to the partials (the slice of
       // wave row wm is partial index mw / 128).  A row's 128 entries sit in
       // its lane and the lanes l ^ 16, l ^ 32, l ^ 48.  EPI_FWDU also keeps
-      // the exponentials u = 2^(z log2e - m) as fp16 in dZ[row][v]; the
-      // softmax-gradient kernel turns them into s (p - onehot) with
-      // p = u 2^(m - lse).  Both variants sum in the same order, so l is
+      // the exponentials against the row's reference R2 (exp_reference of
+      // its target logit), u = 2^(z log2e - m) 2^(m - R2), in bf16, in both
+      // dZ (rows) and dZ^T (columns from the unit's col_off): dZ is
+      // s 2^(R2 - lse2) (u - onehot 2^(lse2 - R2)), so one factor per row
+      // makes them the gradient (applied after the GEMMs), and only the
+      // target entries change.  Both variants sum in the same order, so l is
       // bit-identical between them.
       static_assert(WM == kVocabTile, "one partial per wave slice");
       constexpr bool kStore = EPI == EPI_FWDU;
@@ -401,10 +440,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
               if (mw + 16 * i + mlane + e >= M) acc[i][j][e] = -INFINITY;
       }
       // EPI_FWDU stages the tile's exponentials in LDS (free once the ring is
-      // drained; 256 rows x 256 vocabulary ids x fp16 = the ring's 128 KB) as
+      // drained; 256 rows x 256 vocabulary ids x bf16 = the ring's 128 KB) as
       // [row][vocabulary], 16-byte chunk c of row r at chunk c ^ (r mod 32),
-      // and then writes whole rows (two rows of 256 ids per instruction, each
-      // four 128-byte lines of the slab-major dZ).
+      // and then writes whole rows of dZ (two rows of 256 ids per
+      // instruction, each four 128-byte lines of the slab-major dZ) and the
+      // tile's columns of dZ^T.
       char* stage_u = reinterpret_cast<char*>(smem);
       static_assert(!kStore || (BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2),
                     "staging tile: 512-byte rows that fit the ring");
@@ -427,6 +467,13 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         const float mref = mx > -INFINITY ? mx * kLog2e : 0.f;   // a slice past V has no entries
         float ssum = 0.f;
         const int nl = nw - n0 + 16 * j + (lane & 15);
+        // 2^(m - R2): the slice's exponentials against the row's reference
+        // (padding rows: R2 = 0)
+        float fac = 0.f;
+        if constexpr (kStore) {
+          const int n = n0 + nl;
+          fac = __builtin_amdgcn_exp2f(mref - (n < n_valid ? exp_reference(p.ztgt[n]) : 0.f));
+        }
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
           float u[4];
@@ -440,7 +487,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
             const int ml = mw - m0 + 16 * i + mlane;
             *reinterpret_cast<uint2*>(stage_u + nl * 512 + (((ml >> 3) ^ (nl & 31)) << 4) +
                                       (ml & 7) * 2) =
-                make_uint2(pack_f16x2(u[0], u[1]), pack_f16x2(u[2], u[3]));
+                make_uint2(pack_bf16x2(u[0] * fac, u[1] * fac), pack_bf16x2(u[2] * fac, u[3] * fac));
           }
         }
         float st = ssum + __shfl_xor(ssum, 16, 64);
@@ -469,6 +516,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
           if (n0 + row < N && m < M)
             *reinterpret_cast<uint4*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + n0 + row) * 64 + (m & 63)) = v;
         }
+        store_dzt_columns<BM, ROWS_PER_WAVE>(stage_u, p.dZT, p.ldzt, zt_col, m0, n0, M, wave, lane);
       }
     } else if constexpr (EPI == EPI_DZ) {
       // Recompute backward: the tile holds logits z of vocabulary ids
@@ -523,37 +571,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         if (n0 + row < N && m < M)
           *reinterpret_cast<uint4*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + n0 + row) * 64 + (m & 63)) = v;
       }
-      // dZ^T: lane l of an instruction takes vocabulary row ml = 64 k + l of
-      // the tile (64 lanes read 128 contiguous bytes of one staged row: no
-      // bank conflicts), wave w the 8-row chunks 8 w .. 8 w + 7; each lane
-      // assembles 8 consecutive rows into one 16-byte store.  A wave's 64
-      // rows are one 64-column slab of dZ^T, so a lane's eight stores fill
-      // the 128-byte line of its vocabulary row in that slab (wider per-lane
-      // reads that spread a lane's stores over four rows left four times as
-      // many partly written lines open, overflowing the L2).
-      int lm = lane;
-      asm volatile("" : "+v"(lm));
-#pragma unroll
-      for (int k = 0; k < BM / 64; ++k) {
-        const int ml = 64 * k + lm;
-        const int cw = ((ml >> 3) << 4) + (ml & 7) * 2;   // chunk base (before the XOR) and offset
-        static_assert(ROWS_PER_WAVE == 64, "one dZ^T column slab per wave");
-        uint16_t* const zt = p.dZT + ((int64_t)((zt_col + n0) / 64 + wave) * p.ldzt + m0 + ml) * 64;
-        const bool row_live = m0 + ml < M;
-#pragma unroll
-        for (int c = 0; c < ROWS_PER_WAVE / 8; ++c) {
-          const int r0 = wave * ROWS_PER_WAVE + 8 * c;
-          uint32_t wv[4];
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const int ra = r0 + 2 * t, rb = ra + 1;
-            const uint32_t a = *reinterpret_cast<const uint16_t*>(stage + ra * 512 + (cw ^ ((ra & 31) << 4)));
-            const uint32_t b = *reinterpret_cast<const uint16_t*>(stage + rb * 512 + (cw ^ ((rb & 31) << 4)));
-            wv[t] = a | (b << 16);
-          }
-          if (row_live) *reinterpret_cast<uint4*>(zt + 8 * c) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-        }
-      }
+      store_dzt_columns<BM, ROWS_PER_WAVE>(stage, p.dZT, p.ldzt, zt_col, m0, n0, M, wave, lane);
     } else {
       // fp32 store of the tile, transposed (dX partials, or a full dW tile
       // that started from its previous value), or read-modify-write of a
@@ -599,6 +617,8 @@ hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool sto
   p.group_m = kGroupMFwd;
   if (store_u) {
     p.dZ = ws.dZ; p.ldz = ws.RP;
+    p.dZT = ws.dZT; p.ldzt = V;
+    p.ztgt = ws.ztgt;
     k_gemm4w<EPI_FWDU, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   } else {
     k_gemm4w<EPI_FWD, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);

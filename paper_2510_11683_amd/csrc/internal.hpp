@@ -16,6 +16,17 @@ constexpr int kVocabTile = 128;
 
 constexpr int kFlagNonfinite = 1;   // BGPO_FLAG_NONFINITE
 
+// Stored backward: the forward keeps each row's exponentials against one
+// reference per row, R2 = z_target log2e + kExpRef (log2 units), so that
+// dZ = f (u - onehot 2^(lse2 - R2)) with one factor f = s 2^(R2 - lse2) per
+// row.  A row whose log2-sum-exp exceeds R2 by more than kExpRange (the
+// target's log2 probability below -(kExpRef + kExpRange)) would leave the
+// exponent range of the operands; its exponentials are recomputed against
+// R2 = lse2 after the forward.
+constexpr float kExpRef = 60.f;
+constexpr float kExpRange = 64.f;
+__host__ __device__ inline float exp_reference(float ztgt) { return ztgt * 1.4426950408889634f + kExpRef; }
+
 // Column capacity of H_c^T / dZ^T (the rows of a dW batch; the column
 // offsets of the sample records are 32-bit).
 constexpr int64_t kMaxColumns = int64_t(1) << 30;
@@ -76,6 +87,8 @@ struct Workspace {
   float* lse2;         // [RP]         log2-sum-exp2 of each row (log2 units)
   float* lp;           // [RP]         log p of the target
   float* row_scale;    // [RP]         gradient scale s of each row (0 for padding)
+  float* row_f;        // [RP]         stored backward: dZ row factor s 2^(R2 - lse2) (0 for padding)
+  uint8_t* row_bad;    // [RP]         stored backward: row recomputed against R2 = lse2
   double* dbar;        // [B]          mean log-ratio over all samples (exact objective)
   float* inv_rms;      // [RP]         final-RMSNorm 1/rms of each compacted row
   void* mask_scratch;  // mask_scratch_bytes(B, L): the multi-block mask passes
@@ -162,7 +175,10 @@ hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j0, const f
                             const double* dbar, hipStream_t s);
 hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, int n_t,
                              double* dbar, hipStream_t s);
-hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s);
+// stored backward, after the unit's scales: row factors, the target entries of
+// dZ / dZ^T, H_c^T scaled by the row factors, and the rows outside the
+// exponent range recomputed
+hipError_t launch_grad_scale(const Workspace& ws, int d, int V, hipStream_t s);
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s);
 // dX of sample g of the unit (its rows only; samples of a unit run one after

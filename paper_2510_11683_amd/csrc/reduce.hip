@@ -3,8 +3,9 @@
 //   log-sum-exp       combine the per-vocabulary-tile (max, sum) partials
 //   per-response      l = (1/t) sum log p (Eq. per_step_loss), d, g (Eq. g),
 //                     loss (Algorithm 1, L_j = -g_j/G) and the gradient scale
-//   one-hot           dZ[row, y_row] = s (p_y - 1), the target term of the
-//                     softmax-minus-onehot backward
+//   stored backward   per-row factors of the kept exponentials, their target
+//                     entries (the one-hot term), H_c^T scaled by the
+//                     factors, and rows outside the exponent range recomputed
 //   dX                sum of the split-vocabulary partials, scattered to the
 //                     masked positions
 // Every reduction runs in a fixed order, so results are bit-reproducible.
@@ -224,121 +225,167 @@ hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, in
   return hipGetLastError();
 }
 
-// dZ = s (p - onehot) in bf16, in place over the fp16 exponentials
-// u = 2^(z log2e - m_h) stored by the forward GEMM, with m_h the row's max over
-// the 128-entry vocabulary slice h: p = u 2^(m_h - lse2).  (Differentiating
-// Eq. per_step_loss, d l / d z = (onehot - p) / t; s carries -loss_scale dg/dl
-// and the 1/t.)  At the target the value comes from the fp32 target logit,
-// s (2^(z_y log2e - lse2) - 1), not from the rounded u.  Padded rows become
-// zeros.  Both dZ (RP rows per slab) and dZ^T (V rows per slab) are
-// slab-major, and one workgroup takes one 64-id slab of 256 rows: its part of
-// dZ is one contiguous 32 KB block, read and rewritten in place, and its part
-// of dZ^T (64 ids x 256 columns) four contiguous 8 KB blocks, assembled in
-// LDS.
-constexpr int kGradRows = 256;
-static_assert(kRowPad % kGradRows == 0, "padded row counts must hold whole chunks");
+// Stored backward, once the unit's scales s are known.  The forward kept
+// u = 2^(z log2e - R2) (bf16) in dZ and dZ^T, with R2 = exp_reference(z_y)
+// per row; since p = u 2^(R2 - lse2),
+//     dZ = s (p - onehot) = f (u - onehot 2^(lse2 - R2)),  f = s 2^(R2 - lse2)
+// (differentiating Eq. per_step_loss, d l / d z = (onehot - p) / t; s carries
+// -loss_scale dg/dl and the 1/t).  k_grad_rows sets f per row (0 for padding)
+// and replaces the target entry of both layouts by (p_y - 1) 2^(lse2 - R2),
+// p_y from the fp32 target logit; f scales the dX rows in the reduction and
+// H_c^T's columns (k_scale_hct) for the dW GEMM.  A row with
+// lse2 - R2 > kExpRange (its target log2-probability below
+// -(kExpRef + kExpRange)) is marked: its exponentials may have left the range
+// of bf16 and of the fp32 accumulators, so k_fixup_rows recomputes the row in
+// both layouts against R2 = lse2 (f = s), from fp32 dot products.
+__global__ __launch_bounds__(256) void k_grad_rows(
+    const float* __restrict__ lse2, const float* __restrict__ row_scale,
+    const float* __restrict__ ztgt, const int32_t* __restrict__ row_tgt,
+    const SampleMeta* __restrict__ meta, uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT,
+    float* __restrict__ row_f, uint8_t* __restrict__ row_bad, int V, int64_t RP) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= meta->n_rows_pad) return;
+  float f = 0.f;
+  if (r < meta->n_rows) {
+    const float l2 = lse2[r], z2 = ztgt[r] * kLog2e;
+    const float r2 = exp_reference(ztgt[r]);
+    const bool bad = !(l2 - r2 <= kExpRange);   // (NaN too)
+    const float r2e = bad ? l2 : r2;
+    f = row_scale[r] * __builtin_amdgcn_exp2f(r2e - l2);
+    const float val = (__builtin_amdgcn_exp2f(z2 - l2) - 1.f) * __builtin_amdgcn_exp2f(l2 - r2e);
+    const uint16_t b = (uint16_t)(pack_bf16x2(val, 0.f) & 0xFFFFu);
+    const int y = row_tgt[r];
+    dZ[slab_index(RP, r, y)] = b;
+    dZT[slab_index(V, y, (int64_t)meta->col_off + r)] = b;
+    row_bad[r] = bad;
+  }
+  row_f[r] = f;
+}
 
-__global__ __launch_bounds__(256) void k_softmax_grad(
-    const float* __restrict__ part_m, const float* __restrict__ lse2,
-    const float* __restrict__ row_scale, const float* __restrict__ ztgt,
-    const int32_t* __restrict__ row_tgt, const SampleMeta* __restrict__ meta,
-    uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT, int V, int64_t ldp) {
-  constexpr int kPairs = kGradRows / 2;                  // words per vocabulary id in the tile
-  __shared__ float s_c[kGradRows], s_oh[kGradRows];
-  __shared__ int s_y[kGradRows];
-  // [v][row pair] words (row 2k, row 2k+1), row pair k of vocabulary id v at
-  // word v * kPairs + (k ^ sw(v)), sw(v) = 8 (v / 8) ^ 32 (v % 2): the 64
-  // lanes of a store (8 row pairs x 8 ids 8 apart) hit 64 different banks,
-  // two ids in a row use different halves of the banks for the 16-byte reads
-  // of dZ^T, and aligned groups of 4 row pairs stay together and in order
-  __shared__ __align__(16) uint32_t tile[64 * kPairs];
-  auto sw = [](int v) { return (8 * (v >> 3)) ^ (32 * (v & 1)); };
-  const int slab = blockIdx.x, r0 = blockIdx.y * kGradRows;
-  if (r0 >= meta->n_rows_pad) return;   // n_rows_pad is a multiple of 256: chunks are whole
-  const int N = meta->n_rows;
-  const int tid = threadIdx.x;
-  const int v_lo = slab * 64, h = v_lo / kVocabTile;
-  {
-    const int r = r0 + tid;
-    float c = 0.f, oh = 0.f;
-    int y = -1;
-    if (r < N) {
-      const float l2 = lse2[r], sr = row_scale[r];
-      c = sr * __builtin_amdgcn_exp2f(part_m[(int64_t)h * ldp + r] - l2);
-      y = row_tgt[r];
-      oh = sr * (__builtin_amdgcn_exp2f(fmaf(ztgt[r], kLog2e, -l2)) - 1.f);
-    }
-    s_c[tid] = c;
-    s_oh[tid] = oh;
-    s_y[tid] = y;
-  }
-  __syncthreads();
-  // rows 2 rp and 2 rp + 1 (each one 128-byte slab row), ids v0 .. v0 + 7
-  uint16_t* const zb = dZ + ((int64_t)slab * ldp + r0) * 64;
+// H_c^T[c][col_off + r] *= f_r (bf16, nearest even) over the unit's padded
+// rows; one workgroup per 64 x 64 tile, which is 8 KB of the slab-major H_c^T.
+__global__ __launch_bounds__(256) void k_scale_hct(const float* __restrict__ row_f,
+                                                   const SampleMeta* __restrict__ meta,
+                                                   uint16_t* __restrict__ HcT, int d) {
+  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  if (r0 >= meta->n_rows_pad) return;
+  const int tid = threadIdx.x, cc = tid & 7;
+  float fr[8];
 #pragma unroll
-  for (int it = 0; it < kPairs * 8 / 256; ++it) {
-    const int q = tid + 256 * it;
-    const int vc = q & 7, rp = q >> 3;
-    const int ra = 2 * rp, v0 = v_lo + vc * 8;
-    uint4* pa = reinterpret_cast<uint4*>(zb + ra * 64 + vc * 8);
-    uint4* pb = pa + 8;
-    uint32_t oa[4] = {0, 0, 0, 0}, ob[4] = {0, 0, 0, 0};
+  for (int e = 0; e < 8; ++e) fr[e] = row_f[r0 + cc * 8 + e];
+  uint16_t* base = HcT + slab_index(d, c0, (int64_t)meta->col_off + r0);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int rl = ra + half;
-      if (r0 + rl >= N) continue;
-      const uint4 u = half ? *pb : *pa;
-      const uint32_t uw[4] = {u.x, u.y, u.z, u.w};
-      const float c = s_c[rl], oh = s_oh[rl];
-      const int yo = s_y[rl] - v0;
-      uint32_t* o = half ? ob : oa;
+  for (int it = 0; it < 2; ++it) {
+    const int c = (tid >> 3) + 32 * it;
+    uint4* q = reinterpret_cast<uint4*>(base + (int64_t)c * 64 + cc * 8);
+    const uint4 v = *q;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        float x0 = c * f16_to_f32((uint16_t)(uw[k] & 0xFFFFu));
-        float x1 = c * f16_to_f32((uint16_t)(uw[k] >> 16));
-        if (yo == 2 * k) x0 = oh;
-        if (yo == 2 * k + 1) x1 = oh;
-        o[k] = pack_bf16x2(x0, x1);
-      }
-    }
-    *pa = make_uint4(oa[0], oa[1], oa[2], oa[3]);
-    *pb = make_uint4(ob[0], ob[1], ob[2], ob[3]);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int vl = vc * 8 + 2 * k;
-      tile[vl * kPairs + (rp ^ sw(vl))] = (oa[k] & 0xFFFFu) | (ob[k] << 16);
-      tile[(vl + 1) * kPairs + (rp ^ sw(vl + 1))] = (oa[k] >> 16) | (ob[k] & 0xFFFF0000u);
-    }
-  }
-  __syncthreads();
-  // dZ^T: column slab cs (64 columns = 32 row pairs) of id vl is 128 bytes;
-  // lane cc of 8 takes row pairs 4 cc .. 4 cc + 3 of it
-  const int64_t cslab0 = ((int64_t)meta->col_off + r0) / 64;
-#pragma unroll
-  for (int it = 0; it < 64 * 32 / 256; ++it) {
-    const int q = tid + 256 * it;
-    const int cs = q >> 9, vl = (q >> 3) & 63, cc = q & 7;
-    const int rp = 32 * cs + 4 * cc;
-    const uint4 v = *reinterpret_cast<const uint4*>(tile + vl * kPairs + (rp ^ sw(vl)));
-    *reinterpret_cast<uint4*>(dZT + ((cslab0 + cs) * V + v_lo + vl) * 64 + 8 * cc) = v;
+    for (int e = 0; e < 4; ++e)
+      o[e] = pack_bf16x2(__uint_as_float(w[e] << 16) * fr[2 * e],
+                         __uint_as_float(w[e] & 0xFFFF0000u) * fr[2 * e + 1]);
+    *q = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
-hipError_t launch_softmax_grad(const Workspace& ws, int V, hipStream_t s) {
-  dim3 grid((unsigned)(V / 64), (unsigned)(ws.RP / kGradRows));
-  k_softmax_grad<<<grid, 256, 0, s>>>(ws.part_m, ws.lse2, ws.row_scale, ws.ztgt, ws.row_tgt,
-                                      ws.unit(), ws.dZ, ws.dZT, V, ws.RP);
+// The marked rows of the unit, recomputed in both layouts against
+// R2 = lse2: u = 2^(z log2e - lse2) = p, and p_y - 1 at the target.  One
+// thread per vocabulary id; each workgroup scans the unit's marks 256 rows at
+// a time and takes the marked ones in batches of 16, whose fp32 logits
+// z = H_c[row] . W^T[v] it accumulates in a fixed order over d.  Without
+// marked rows it only reads the marks.
+constexpr int kFixBatch = 16;
+
+__global__ __launch_bounds__(256) void k_fixup_rows(
+    const uint16_t* __restrict__ Hc, const uint16_t* __restrict__ WT,
+    const float* __restrict__ lse2, const float* __restrict__ ztgt,
+    const int32_t* __restrict__ row_tgt, const uint8_t* __restrict__ row_bad,
+    const SampleMeta* __restrict__ meta, uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT,
+    int d, int V, int64_t RP) {
+  __shared__ int s_list[256];
+  __shared__ int s_cnt;
+  __shared__ float s_h[kFixBatch][64];
+  const int tid = threadIdx.x;
+  const int v = blockIdx.x * 256 + tid;
+  const int N = meta->n_rows;
+  const int64_t col_off = meta->col_off;
+  for (int base = 0; base < N; base += 256) {
+    if (tid == 0) s_cnt = 0;
+    __syncthreads();
+    const int rr = base + tid;
+    if (rr < N && row_bad[rr]) s_list[atomicAdd(&s_cnt, 1)] = rr;
+    __syncthreads();
+    const int cnt = s_cnt;
+    for (int b0 = 0; b0 < cnt; b0 += kFixBatch) {
+      const int nb = min(kFixBatch, cnt - b0);
+      float acc[kFixBatch];
+#pragma unroll
+      for (int i = 0; i < kFixBatch; ++i) acc[i] = 0.f;
+      for (int kc = 0; kc < d; kc += 64) {
+        __syncthreads();
+        for (int q = tid; q < kFixBatch * 64; q += 256) {
+          const int i = q >> 6, k = q & 63;
+          s_h[i][k] = i < nb ? __uint_as_float((uint32_t)Hc[slab_index(RP, s_list[b0 + i], kc + k)] << 16)
+                             : 0.f;
+        }
+        __syncthreads();
+        if (v < V) {
+          const uint16_t* w = WT + (int64_t)v * d + kc;
+          for (int kk = 0; kk < 64; kk += 8) {
+            const uint4 wv = *reinterpret_cast<const uint4*>(w + kk);
+            const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float w0 = __uint_as_float(ww[e] << 16), w1 = __uint_as_float(ww[e] & 0xFFFF0000u);
+#pragma unroll
+              for (int i = 0; i < kFixBatch; ++i)
+                acc[i] = fmaf(w1, s_h[i][kk + 2 * e + 1], fmaf(w0, s_h[i][kk + 2 * e], acc[i]));
+            }
+          }
+        }
+      }
+      if (v < V) {
+#pragma unroll
+        for (int i = 0; i < kFixBatch; ++i) {
+          if (i >= nb) break;
+          const int r = s_list[b0 + i];
+          const float l2 = lse2[r];
+          const float val = v == row_tgt[r] ? __builtin_amdgcn_exp2f(fmaf(ztgt[r], kLog2e, -l2)) - 1.f
+                                            : __builtin_amdgcn_exp2f(fmaf(acc[i], kLog2e, -l2));
+          const uint16_t b = (uint16_t)(pack_bf16x2(val, 0.f) & 0xFFFFu);
+          dZ[slab_index(RP, r, v)] = b;
+          dZT[slab_index(V, v, col_off + r)] = b;
+        }
+      }
+    }
+    __syncthreads();   // s_list / s_cnt are rewritten for the next rows
+  }
+}
+
+hipError_t launch_grad_scale(const Workspace& ws, int d, int V, hipStream_t s) {
+  k_grad_rows<<<(unsigned)(ws.RP / 256), 256, 0, s>>>(ws.lse2, ws.row_scale, ws.ztgt, ws.row_tgt,
+                                                      ws.unit(), ws.dZ, ws.dZT, ws.row_f,
+                                                      ws.row_bad, V, ws.RP);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  k_scale_hct<<<dim3((unsigned)(ws.RP / 64), (unsigned)(d / 64)), 256, 0, s>>>(ws.row_f, ws.unit(),
+                                                                             ws.HcT, d);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  k_fixup_rows<<<(unsigned)((V + 255) / 256), 256, 0, s>>>(ws.Hc, ws.WT, ws.lse2, ws.ztgt,
+                                                           ws.row_tgt, ws.row_bad, ws.unit(),
+                                                           ws.dZ, ws.dZT, d, V, ws.RP);
   return hipGetLastError();
 }
 
-// dX[idx[r], :] += sum_s part[s][r][:] over the rows r of one sample of the
-// unit (sm: its record; um: the unit's, which holds the split count), float4
-// per thread; rows are unique within a sample, so there are no write
-// conflicts.
+// dX[idx[r], :] += f_r sum_s part[s][r][:] over the rows r of one sample of
+// the unit (sm: its record; um: the unit's, which holds the split count; f_r
+// the stored backward's row factor, 1 without one), float4 per thread; rows
+// are unique within a sample, so there are no write conflicts.
 __global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ part,
                                                    const int32_t* __restrict__ idx,
                                                    const SampleMeta* __restrict__ sm,
                                                    const SampleMeta* __restrict__ um,
+                                                   const float* __restrict__ rowf,
                                                    float* __restrict__ dX, int d,
                                                    int64_t split_stride) {
   if ((int)blockIdx.x >= sm->s_rows) return;
@@ -351,6 +398,10 @@ __global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ par
     const float4 v = *reinterpret_cast<const float4*>(part + s * split_stride + (int64_t)r * d + c);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
+  if (rowf) {
+    const float f = rowf[r];
+    acc.x *= f; acc.y *= f; acc.z *= f; acc.w *= f;
+  }
   float4* dst = reinterpret_cast<float4*>(dX + (int64_t)idx[r] * d + c);
   float4 o = *dst;
   o.x += acc.x; o.y += acc.y; o.z += acc.z; o.w += acc.w;
@@ -359,14 +410,17 @@ __global__ __launch_bounds__(256) void k_dx_reduce(const float* __restrict__ par
 
 hipError_t launch_dx_reduce(const Workspace& ws, int g, float* dX, int d, hipStream_t s) {
   dim3 grid((unsigned)ws.NP, (unsigned)((d / 4 + 255) / 256));
-  k_dx_reduce<<<grid, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta + g, ws.unit(), dX, d, ws.RP * d);
+  k_dx_reduce<<<grid, 256, 0, s>>>(ws.dx_part, ws.idx, ws.meta + g, ws.unit(),
+                                   ws.chunk ? nullptr : ws.row_f, dX, d, ws.RP * d);
   return hipGetLastError();
 }
 
 // Split reduction followed by the backward of the final RMSNorm
 // h = gamma x r, r = (mean x^2 + eps)^(-1/2), for one row of one sample of the
 // unit per workgroup (x: that sample's activations):
-//   dh       = sum_s part[s][row]                     (d loss / d h)
+//   dh       = f_row sum_s part[s][row]               (d loss / d h; f_row the
+//                                                     stored backward's row
+//                                                     factor, 1 without one)
 //   dx_k    += r gamma_k dh_k - (r^3 / d) x_k sum_i gamma_i dh_i x_i
 //   c_k      = dh_k x_k r  -> part[0][row][k], summed over rows into dgamma
 // Every thread revisits only the elements it wrote, so part[0] needs no
@@ -374,7 +428,7 @@ hipError_t launch_dx_reduce(const Workspace& ws, int g, float* dX, int d, hipStr
 template <typename T>
 __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
     float* __restrict__ part, const int32_t* __restrict__ idx, const SampleMeta* __restrict__ sm,
-    const SampleMeta* __restrict__ um, const T* __restrict__ x,
+    const SampleMeta* __restrict__ um, const float* __restrict__ rowf, const T* __restrict__ x,
     const float* __restrict__ gamma, const float* __restrict__ inv_rms, float* __restrict__ dx,
     int d, int64_t split_stride) {
   __shared__ float red[4];
@@ -382,6 +436,7 @@ __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
   const int r = sm->s_row_off + blockIdx.x;
   const int n_split = um->dx_split;
   const int tid = threadIdx.x;
+  const float f = rowf ? rowf[r] : 1.f;   // the stored backward's row factor
   float* p0 = part + (int64_t)r * d;
   const T* xr = x + (int64_t)idx[r] * d;
   float dot = 0.f;
@@ -391,6 +446,7 @@ __global__ __launch_bounds__(256) void k_dx_reduce_rmsnorm(
       const float4 v = *reinterpret_cast<const float4*>(p0 + sp * split_stride + c);
       acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
     }
+    acc.x *= f; acc.y *= f; acc.z *= f; acc.w *= f;
     *reinterpret_cast<float4*>(p0 + c) = acc;
     const uint2 xv = load_bf16x4(xr + c);
     const float4 g = *reinterpret_cast<const float4*>(gamma + c);
@@ -456,12 +512,12 @@ hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const void* x, b
   const SampleMeta* sm = ws.meta + g;
   if (f32)
     k_dx_reduce_rmsnorm<float><<<(unsigned)ws.NP, 256, 0, s>>>(
-        ws.dx_part, ws.idx, sm, ws.unit(), static_cast<const float*>(x), gamma, ws.inv_rms, dx, d,
-        ws.RP * d);
+        ws.dx_part, ws.idx, sm, ws.unit(), ws.chunk ? nullptr : ws.row_f,
+        static_cast<const float*>(x), gamma, ws.inv_rms, dx, d, ws.RP * d);
   else
     k_dx_reduce_rmsnorm<uint16_t><<<(unsigned)ws.NP, 256, 0, s>>>(
-        ws.dx_part, ws.idx, sm, ws.unit(), static_cast<const uint16_t*>(x), gamma, ws.inv_rms, dx,
-        d, ws.RP * d);
+        ws.dx_part, ws.idx, sm, ws.unit(), ws.chunk ? nullptr : ws.row_f,
+        static_cast<const uint16_t*>(x), gamma, ws.inv_rms, dx, d, ws.RP * d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 g1((unsigned)((d + 255) / 256), (unsigned)(ws.NP / 256));

@@ -280,13 +280,38 @@ def test_mid_parity_peaky_logits(w_std):
     """Trained heads give far peakier softmaxes than N(0, 0.02) weights: with
     W ~ N(0, w_std^2) the logits have std w_std * sqrt(d), most of the
     probability sits on a few tokens and the stored exponentials of the others
-    underflow fp16; off-policy, both bound branches."""
+    are far below the row's reference; off-policy, both bound branches."""
     w = MID.replace(w_std=w_std)
     x = workloads.generate(w)
     op = _oracle_problem(w)
     ell_old = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
                                 backward=False).ell
     ell_old = ell_old + np.random.default_rng(9).normal(0, 1.0, ell_old.shape)
+    ref = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                            ell_old=ell_old, loss_scale=0.25)
+    r = Runner(w, x)
+    r.bwd(ell_old=ell_old, loss_scale=0.25)
+    _check_against_oracle(w, r.out(), ref, range(w.n_t), x["adv"], ell_old, 0.25)
+
+
+def test_mid_parity_rows_outside_exponent_range():
+    """The stored backward keeps a row's exponentials against its target
+    logit plus 60 (log2 units); rows whose log2-sum-exp exceeds that by more
+    than 64 (target log-probability below about -86) are recomputed after the
+    forward.  With W ~ N(0, 1) (logit std 24) about half of the rows are such
+    rows (counted here from float64 logits), off-policy, both bound branches."""
+    w = MID.replace(w_std=1.0)
+    x = workloads.generate(w)
+    H = elbo.bf16_to_f64(x["hidden"]).reshape(-1, w.d)
+    z = H @ elbo.bf16_to_f64(x["W"])
+    lse = z.max(1) + np.log(np.exp(z - z.max(1, keepdims=True)).sum(1))
+    gap2 = (lse - z[np.arange(z.shape[0]), x["targets"].reshape(-1)]) / np.log(2.0)
+    far = gap2[x["resp_mask"].reshape(-1).astype(bool)] > 124
+    assert 0.2 < far.mean() < 0.8
+    op = _oracle_problem(w)
+    ell_old = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                                backward=False).ell
+    ell_old = ell_old + np.random.default_rng(12).normal(0, 1.0, ell_old.shape)
     ref = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
                             ell_old=ell_old, loss_scale=0.25)
     r = Runner(w, x)
@@ -352,10 +377,11 @@ def test_linearity_and_determinism():
 def test_timing_record_counts_kernel_launches():
     """The optional timing record adds, per kernel class, the elapsed time and
     the number of kernel launches: 10 samples in units of 8 give 2 units; per
-    unit one forward, softmax-gradient and dX GEMM launch, one gather, the
-    three row reductions (target logit, log-sum-exp, per-response terms), and
-    one mask and one dX reduction per sample; one dW GEMM for the batch of
-    both units; the W transpose once per call."""
+    unit one forward and dX GEMM launch, the three softmax-gradient kernels
+    (row factors and target entries, H_c^T scaling, recomputed rows), one
+    gather, the three row reductions (target logit, log-sum-exp, per-response
+    terms), and one mask and one dX reduction per sample; one dW GEMM for the
+    batch of both units; the W transpose once per call."""
     w = workloads.TINY.replace(n_t=10)
     r = Runner(w, workloads.generate(w))
     t = lib().Timing()
@@ -363,7 +389,7 @@ def test_timing_record_counts_kernel_launches():
     torch.cuda.synchronize()
     got = {k: n for k, (ms, n) in t.as_dict().items()}
     assert got == {"transpose_w": 1, "mask": 10, "gather": 2, "fwd": 2, "ell": 6,
-                   "softmax_grad": 2, "dx": 2, "dx_reduce": 10, "dw": 1, "recompute": 0}
+                   "softmax_grad": 6, "dx": 2, "dx_reduce": 10, "dw": 1, "recompute": 0}
     assert all(ms > 0 for ms, n in t.as_dict().values() if n)
     r.fwd(timing=t)                                     # forward only: no gradient classes
     got2 = {k: n for k, (ms, n) in t.as_dict().items()}
