@@ -320,9 +320,10 @@ def main():
     # bytes and from the algorithmic bytes, against the 8 TB/s peak
     def algo_bytes(k, launches):                         # per launch
         rows = tokens / launches                         # masked rows one launch processes
+        # (softmax_grad: three small kernels per unit, counter bytes only;
+        # dx_reduce: depends on the split count)
         return {"gather": 6.0 * rows * d,                # read rows, write H_c and H_c^T
-                "softmax_grad": 6.0 * rows * V,          # read u, write dZ and dZ^T (2 bytes each)
-                "transpose_w": 4.0 * d * V}.get(k)       # dx_reduce: depends on the split count
+                "transpose_w": 4.0 * d * V}.get(k)
     for k, e in per_kernel.items():
         if k in GEMM_CLASSES:
             continue

@@ -160,12 +160,19 @@ typedef struct bgpo_problem {
 /* Backward modes and the workspace budget.  Both keep device memory constant
  * in n_t; they trade memory for work:
  *   stored exponentials   the forward GEMM of a unit of samples keeps the
- *                         exponentials of its logits (fp16, rows x V), the
- *                         gradient dZ = s (softmax - onehot) is formed from
- *                         them, and the dX and dW GEMMs read all of it: three
- *                         GEMM passes per sample, a workspace of about
- *                         rows x V x 6 bytes per unit (31 GB at B=8, L=512,
- *                         d=4096, V=126464 with units of 8 samples)
+ *                         exponentials of its logits (bf16, rows x V, in two
+ *                         layouts) against one reference per row, the target
+ *                         logit plus 60 in log2 units, so that
+ *                         dZ = s (softmax - onehot) is one factor per row
+ *                         times them, except at the target; the dX and dW
+ *                         GEMMs read all of it: three GEMM passes per sample,
+ *                         a workspace of about rows x V x 6 bytes per unit
+ *                         (31 GB at B=8, L=512, d=4096, V=126464 with units
+ *                         of 8 samples).  A row whose target log2-probability
+ *                         is below -124 (its exponentials would leave the
+ *                         range of bf16 and of the fp32 accumulators) is
+ *                         recomputed after the forward from fp32 dot
+ *                         products, which is slow but exact in form
  *   recompute             the forward keeps only the per-row log-sum-exp; the
  *                         backward walks the vocabulary in chunks of C
  *                         entries, recomputing that chunk's logits, writing
@@ -193,7 +200,8 @@ enum {
   BGPO_K_FWD = 3,          /* fused LM-head GEMM + online log-sum-exp partials (in the
                               backward it also stores the exponentials) */
   BGPO_K_ELL = 4,          /* partial combine, log p, l, d, g, loss, gradient scale */
-  BGPO_K_SOFTMAX_GRAD = 5, /* stored exponentials -> dZ = s (softmax - onehot), both layouts */
+  BGPO_K_SOFTMAX_GRAD = 5, /* stored exponentials -> dZ = s (softmax - onehot): row factors,
+                              target entries, H_c^T scaled, out-of-range rows recomputed */
   BGPO_K_DX = 6,           /* dZ W^T split over the vocabulary */
   BGPO_K_DX_REDUCE = 7,    /* split reduction + scatter-add into dX (+ RMSNorm backward) */
   BGPO_K_DW = 8,           /* H_c^T dZ accumulated into dW */

@@ -149,15 +149,40 @@ __device__ __forceinline__ void epi_f32_16t(const f32x4 (&acc)[TM][TN], float* o
   }
 }
 
+// Rows of a 256 x 256 tile staged in LDS as [row][vocabulary] (16-byte chunk
+// c of row r at chunk c ^ (r mod 32)) into the slab-major dZ (ldz rows per
+// slab): lane l of a store instruction takes row 2 q + l / 32 of the wave's
+// rows and physical chunk l mod 32, i.e. logical chunk (l mod 32) ^ (row mod
+// 32); an instruction writes two rows, each four whole 128-byte lines (its
+// four vocabulary slabs).  (Eight consecutive rows of one slab per
+// instruction, 1 KB of contiguous lines, measured no faster.)
+template <int BM, int ROWS_PER_WAVE>
+__device__ __forceinline__ void store_dz_rows(const char* stage, uint16_t* dZ, int64_t ldz, int m0,
+                                              int n0, int N, int M, int wave, int lane) {
+  static_assert(BM == 256, "512-byte staged rows");
+  // (the lane's chunk is re-derived here every tile: hoisted out of the
+  // tile loop, its per-row variants would be spilled)
+  int pc = lane & 31;
+  asm volatile("" : "+v"(pc));
+#pragma unroll
+  for (int q = 0; q < ROWS_PER_WAVE / 2; ++q) {
+    const int row = wave * ROWS_PER_WAVE + 2 * q + (lane >> 5);
+    const int m = m0 + 8 * (pc ^ (row & 31));
+    const uint4 v = *reinterpret_cast<const uint4*>(stage + row * 512 + pc * 16);
+    if (n0 + row < N && m < M)
+      *reinterpret_cast<uint4*>(dZ + ((int64_t)(m >> 6) * ldz + n0 + row) * 64 + (m & 63)) = v;
+  }
+}
+
 // dZ^T columns of a 256 x 256 tile staged in LDS as [row][vocabulary]
 // (16-byte chunk c of row r at chunk c ^ (r mod 32), bf16): vocabulary rows
 // m0 .. m0 + 255 of dZ^T (slab-major, ldzt rows per slab), columns
 // zt_col + n0 .. + 255.  Wave w's 64 tile rows are one 64-column slab of
-// dZ^T, in which consecutive vocabulary ids are consecutive 128-byte lines:
-// store instruction i writes ids 8 i .. 8 i + 7, lane l the 16 bytes of
-// columns 8 (l mod 8) .. + 7 of id 8 i + l / 8, i.e. 1 KB of contiguous,
-// whole lines per instruction; each lane assembles its 8 columns from 8
-// two-byte reads of the staged rows.
+// dZ^T, in which consecutive vocabulary ids are consecutive 128-byte lines.
+// Lane l takes columns 8 (l mod 8) .. + 7 of four consecutive ids
+// 32 i + 4 (l / 8) .. + 3: eight 8-byte reads of the staged rows, then four
+// 16-byte stores, store k of every lane writing ids 4 q + k (q = 0 .. 7) of
+// the group, i.e. eight whole lines per instruction.
 template <int BM, int ROWS_PER_WAVE>
 __device__ __forceinline__ void store_dzt_columns(const char* stage, uint16_t* dZT, int64_t ldzt,
                                                   int zt_col, int m0, int n0, int M, int wave,
@@ -166,20 +191,30 @@ __device__ __forceinline__ void store_dzt_columns(const char* stage, uint16_t* d
   int lq = lane;
   asm volatile("" : "+v"(lq));
   const int cc = lq & 7, vq = lq >> 3;
-  uint16_t* const zt = dZT + ((int64_t)((zt_col + n0) / 64 + wave) * ldzt + m0 + vq) * 64 + cc * 8;
+  uint16_t* const zt = dZT + ((int64_t)((zt_col + n0) / 64 + wave) * ldzt + m0 + 4 * vq) * 64 + cc * 8;
   const int rbase = wave * ROWS_PER_WAVE + 8 * cc;
-#pragma unroll 4
-  for (int i = 0; i < BM / 8; ++i) {
-    const int cw = (i << 4) + vq * 2;   // id 8 i + vq: chunk i (before the XOR), offset vq
-    uint32_t wv[4];
+#pragma unroll 2
+  for (int i = 0; i < BM / 32; ++i) {
+    // ids 32 i + 4 vq .. + 3: chunk 4 i + vq / 2, bytes 8 (vq mod 2) .. + 7
+    const int cw = ((4 * i + (vq >> 1)) << 4) + (vq & 1) * 8;
+    uint2 q[8];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int ra = rbase + 2 * t, rb = ra + 1;
-      const uint32_t a = *reinterpret_cast<const uint16_t*>(stage + ra * 512 + (cw ^ ((ra & 31) << 4)));
-      const uint32_t b = *reinterpret_cast<const uint16_t*>(stage + rb * 512 + (cw ^ ((rb & 31) << 4)));
-      wv[t] = a | (b << 16);
+    for (int t = 0; t < 8; ++t) {
+      const int ra = rbase + t;
+      q[t] = *reinterpret_cast<const uint2*>(stage + ra * 512 + (cw ^ ((ra & 31) << 4)));
     }
-    if (m0 + 8 * i < M) *reinterpret_cast<uint4*>(zt + (int64_t)i * 512) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+    if (m0 + 32 * i < M) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        uint32_t wv[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const uint32_t a = k < 2 ? q[2 * t].x : q[2 * t].y, b = k < 2 ? q[2 * t + 1].x : q[2 * t + 1].y;
+          wv[t] = (k & 1) ? __builtin_amdgcn_perm(b, a, 0x07060302u) : __builtin_amdgcn_perm(b, a, 0x05040100u);
+        }
+        *reinterpret_cast<uint4*>(zt + (int64_t)(32 * i + k) * 64) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      }
+    }
   }
 }
 
@@ -501,21 +536,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       }
       if constexpr (kStore) {
         __syncthreads();
-        // lane l of a store instruction: row 2 q + l / 32 of the wave's rows,
-        // stored chunk l mod 32, i.e. logical chunk (l mod 32) ^ (row mod 32)
         constexpr int ROWS_PER_WAVE = BN / (NT / 64);
-        // (the lane's chunk is re-derived here every tile: hoisted out of the
-        // tile loop, its per-row variants would be spilled)
-        int pc = lane & 31;
-        asm volatile("" : "+v"(pc));
-#pragma unroll
-        for (int q = 0; q < ROWS_PER_WAVE / 2; ++q) {
-          const int row = wave * ROWS_PER_WAVE + 2 * q + (lane >> 5);
-          const int m = m0 + 8 * (pc ^ (row & 31));
-          const uint4 v = *reinterpret_cast<const uint4*>(stage_u + row * 512 + pc * 16);
-          if (n0 + row < N && m < M)
-            *reinterpret_cast<uint4*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + n0 + row) * 64 + (m & 63)) = v;
-        }
+        store_dz_rows<BM, ROWS_PER_WAVE>(stage_u, p.dZ, p.ldz, m0, n0, N, M, wave, lane);
         store_dzt_columns<BM, ROWS_PER_WAVE>(stage_u, p.dZT, p.ldzt, zt_col, m0, n0, M, wave, lane);
       }
     } else if constexpr (EPI == EPI_DZ) {
@@ -561,16 +583,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       }
       __syncthreads();
       constexpr int ROWS_PER_WAVE = BN / (NT / 64);
-      int pc = lane & 31;
-      asm volatile("" : "+v"(pc));
-#pragma unroll
-      for (int q = 0; q < ROWS_PER_WAVE / 2; ++q) {
-        const int row = wave * ROWS_PER_WAVE + 2 * q + (lane >> 5);
-        const int m = m0 + 8 * (pc ^ (row & 31));
-        const uint4 v = *reinterpret_cast<const uint4*>(stage + row * 512 + pc * 16);
-        if (n0 + row < N && m < M)
-          *reinterpret_cast<uint4*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + n0 + row) * 64 + (m & 63)) = v;
-      }
+      store_dz_rows<BM, ROWS_PER_WAVE>(stage, p.dZ, p.ldz, m0, n0, N, M, wave, lane);
       store_dzt_columns<BM, ROWS_PER_WAVE>(stage, p.dZT, p.ldzt, zt_col, m0, n0, M, wave, lane);
     } else {
       // fp32 store of the tile, transposed (dX partials, or a full dW tile
