@@ -490,6 +490,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // per-lane offsets)
       float* const pm = p.part_m + (int64_t)vt * p.ldp;
       float* const ps = p.part_s + (int64_t)vt * p.ldp;
+      // the references of the lane's 8 rows, loaded before the column blocks
+      // so that one wait covers them (padding rows: R2 = 0)
+      float r2v[TN];
+      if constexpr (kStore) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int n = nw + 16 * j + (lane & 15);
+          r2v[j] = n < n_valid ? exp_reference(p.ztgt[n]) : 0.f;
+        }
+      }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         float mx = -INFINITY;
@@ -503,12 +513,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         float ssum = 0.f;
         const int nl = nw - n0 + 16 * j + (lane & 15);
         // 2^(m - R2): the slice's exponentials against the row's reference
-        // (padding rows: R2 = 0)
         float fac = 0.f;
-        if constexpr (kStore) {
-          const int n = n0 + nl;
-          fac = __builtin_amdgcn_exp2f(mref - (n < n_valid ? exp_reference(p.ztgt[n]) : 0.f));
-        }
+        if constexpr (kStore) fac = __builtin_amdgcn_exp2f(mref - r2v[j]);
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
           float u[4];
