@@ -560,18 +560,25 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       char* stage = reinterpret_cast<char*>(smem);
       static_assert(BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2,
                     "staging tile: 512-byte rows that fit the ring");
+      // the lane's 8 rows' log2-sum-exp2, scale and target (as a tile row
+      // index, may be outside), loaded before the column blocks so that one
+      // wait covers them
+      float l2v[TN], srv[TN];
+      int ymv[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = nw + 16 * j + (lane & 15);
+        const bool live = n < n_valid;
+        l2v[j] = live ? p.lse2[n] : 0.f;
+        srv[j] = live ? p.rscale[n] : 0.f;
+        ymv[j] = live ? p.rtgt[n] - p.v0 - m0 : -1;
+      }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int nl = nw - n0 + 16 * j + (lane & 15);
-        const int n = n0 + nl;
-        const bool live = n < n_valid;
-        float l2 = 0.f, sr = 0.f;
-        int ym = -1;                    // the row's target as a tile row index (may be outside)
-        if (live) {
-          l2 = p.lse2[n];
-          sr = p.rscale[n];
-          ym = p.rtgt[n] - p.v0 - m0;
-        }
+        const bool live = n0 + nl < n_valid;
+        const float l2 = l2v[j], sr = srv[j];
+        const int ym = ymv[j];
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
           const int ml = mw - m0 + 16 * i + mlane;
