@@ -66,18 +66,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
-typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
-
-// two floats -> packed IEEE half pair (lo = a, hi = b), round to nearest even
-__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
-  const f32x2_t v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2_t));
-}
-
-__device__ __forceinline__ float f16_to_f32(uint16_t h) {
-  return (float)__builtin_bit_cast(_Float16, h);
-}
-
 __device__ __forceinline__ float bf16_to_f32(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 // Head inputs as bf16 bit patterns, 8 or 4 consecutive elements at a time:

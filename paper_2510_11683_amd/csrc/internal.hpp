@@ -93,9 +93,10 @@ struct Workspace {
   float* inv_rms;      // [RP]         final-RMSNorm 1/rms of each compacted row
   void* mask_scratch;  // mask_scratch_bytes(B, L): the multi-block mask passes
   float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks of a sample
-  uint16_t* dZ;        // stored mode: [RP rows, V] s (softmax - onehot), bf16 (first the fp16
-                       // exponentials); recompute mode: [RP rows, chunk], one vocabulary
-                       // chunk; slab-major
+  uint16_t* dZ;        // stored mode: [RP rows, V] the forward's bf16 exponentials against
+                       // the row's reference, i.e. s (softmax - onehot) up to the row factor
+                       // (target entries rewritten); recompute mode: [RP rows, chunk],
+                       // one vocabulary chunk's s (softmax - onehot); slab-major
   uint16_t* dZT;       // stored mode: [V rows, KT] the same, transposed, units of a dW batch
                        // side by side; recompute mode: [chunk rows, KT], one chunk;
                        // slab-major
