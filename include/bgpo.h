@@ -205,7 +205,7 @@ enum {
   BGPO_K_DX = 6,           /* dZ W^T split over the vocabulary */
   BGPO_K_DX_REDUCE = 7,    /* split reduction + scatter-add into dX (+ RMSNorm backward) */
   BGPO_K_DW = 8,           /* H_c^T dZ accumulated into dW */
-  BGPO_K_RECOMPUTE = 9,    /* recompute mode: a vocabulary chunk's logits -> its dZ (both layouts) */
+  BGPO_K_RECOMPUTE = 9,    /* recompute mode: a vocabulary chunk's logits -> its dZ */
   BGPO_K_COUNT = 10
 };
 

@@ -58,10 +58,9 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
   const int64_t n_units = pl.retain ? (dm.n_t + G - 1) / G : 1;
   const int64_t RP = G * NP;
   const int64_t dw_batch = pl.retain ? n_units : pl.dw_batch;
-  // columns of H_c^T and dZ^T (the rows of a dW batch)
+  // the rows of a dW batch: columns of H_c^T, rows of the stored dZ
   const int64_t KT = dw_batch * RP;
   const int64_t chunk = pl.chunk;
-  const int64_t zt_rows = chunk ? chunk : dm.V;     // vocabulary ids of dZ (columns) and dZ^T (rows)
 
   size_t off = 0;
   char* b = static_cast<char*>(base);
@@ -70,7 +69,8 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
     off = align_up(off + bytes, 256);
     return p;
   };
-  // the state of one unit: masks and rows, log-sum-exp partials, H_c, dZ
+  // the state of one unit: masks and rows, log-sum-exp partials, H_c (and a
+  // vocabulary chunk's dZ)
   auto take_unit = [&](Workspace& w) {
     w.meta = static_cast<SampleMeta*>(take(G * sizeof(SampleMeta)));
     w.idx = static_cast<int32_t*>(take(G * P * 4));
@@ -90,7 +90,7 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
     w.part_m = static_cast<float*>(take(nvt * RP * 4));
     w.part_s = static_cast<float*>(take(nvt * RP * 4));
     w.Hc = static_cast<uint16_t*>(take(RP * dm.d * 2));
-    w.dZ = static_cast<uint16_t*>(take(RP * zt_rows * 2));
+    if (chunk) w.dZ = static_cast<uint16_t*>(take(RP * chunk * 2));
   };
   Workspace w;
   w.dbar = static_cast<double*>(take(dm.B * 8));
@@ -98,7 +98,8 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
   w.HcT = static_cast<uint16_t*>(take(KT * dm.d * 2));
   w.WT = static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2));
   w.Wb = pl.f32_in ? static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2)) : nullptr;
-  w.dZT = static_cast<uint16_t*>(take(KT * zt_rows * 2));
+  w.ldz = chunk ? RP : KT + kDzPadRows;
+  w.dZ = chunk ? nullptr : static_cast<uint16_t*>(take(w.ldz * dm.V * 2));
   w.dx_part = static_cast<float*>(take(pl.n_split * RP * dm.d * 4));
   w.P = P;
   w.NP = NP;
@@ -126,14 +127,14 @@ static size_t plan_bytes(const Dims& dm, const Plan& pl) {
 }
 
 // The stored-exponential plan used without a budget: units of up to 8
-// samples while the unit's dZ and H_c and the dZ^T and H_c^T columns of a dW
+// samples while the unit's H_c and the dZ rows and H_c^T columns of a dW
 // batch of two units stay within about 32 GB; dX split capacity up to 16
 // within about 4 GB.  With every sample retained, the same units (at most n_t
 // samples each) each keep their own state and all of them form the one dW
 // batch, so both modes run the same unit compositions.
 static Plan default_plan(const Dims& dm, int retain, int f32) {
   const int64_t NP = padded_positions(dm);
-  const int64_t per_sample = NP * ((int64_t)dm.V + dm.d) * 2 * (1 + kDwUnits);
+  const int64_t per_sample = NP * ((int64_t)dm.V * kDwUnits + (int64_t)dm.d * (1 + kDwUnits)) * 2;
   int64_t G = std::max<int64_t>(1, std::min(max_unit(dm), 32 * kGiB / per_sample));
   if (retain) G = std::min<int64_t>(G, dm.n_t);
   const int64_t RP = G * NP;
@@ -177,9 +178,9 @@ static double recompute_cost(const Dims& dm, const Plan& pl) {
 }
 
 // The same estimate for the stored-exponential backward: three GEMM passes
-// (the dX GEMM at the best split the capacity allows), the softmax-gradient
-// pass over the kept exponentials (6 bytes per entry) and the dW
-// read-modify-write once per batch of units.
+// (the dX GEMM at the best split the capacity allows), the forward's stores
+// of the kept exponentials (2 bytes per entry) and the dW read-modify-write
+// once per batch of units.
 static double stored_cost(const Dims& dm, const Plan& pl) {
   const double NP = (double)padded_positions(dm);
   const double rows = pl.G * NP;
@@ -189,7 +190,7 @@ static double stored_cost(const Dims& dm, const Plan& pl) {
     dx_fill = std::max(dx_fill, mean_fill(rows, col_t, (double)sp));
   const double pass = 2.0 * NP * 0.5 * dm.d * (double)dm.V / 1.35e15;
   const double gemm = pass * (1.0 / mean_fill(rows, std::ceil(dm.V / 256.0), 1.0) + 1.0 / dx_fill + 1.0);
-  const double mem = (6.0 * NP * 0.5 * dm.V + (double)dm.V * dm.d * 8.0 / (pl.G * pl.dw_batch)) / 5e12;
+  const double mem = (2.0 * NP * 0.5 * dm.V + (double)dm.V * dm.d * 8.0 / (pl.G * pl.dw_batch)) / 5e12;
   return gemm + mem;
 }
 
@@ -339,8 +340,8 @@ static int plan_problem(const bgpo_problem* p, Plan* pl) {
     return BGPO_ERR_UNSUPPORTED;
   const int st = choose_plan(p, pl);
   if (st != BGPO_OK) return st;
-  // H_c^T and dZ^T hold KT columns (32-bit column offsets in the sample
-  // records).  One unit's row capacity stays within 65535 * 64 by
+  // H_c^T holds KT columns and the stored dZ KT rows (32-bit offsets in the
+  // sample records).  One unit's row capacity stays within 65535 * 64 by
   // construction; with every sample retained KT grows with n_t and is
   // bounded here.
   static_assert(int64_t(65535) * 64 / 256 * 256 * kDwUnits <= kMaxColumns,
@@ -507,11 +508,11 @@ static bool overlaps(const double* a, const double* b, int64_t n) {
 namespace bgpo {
 
 // the gradient part of a unit once its scales are known.  Stored mode: the
-// forward kept the exponentials in both layouts; the row factors, the target
-// entries and the scaled H_c^T columns make them dZ (up to the row factor,
-// applied to the dX rows in the reduction), then one dX GEMM over the whole
-// vocabulary; the unit's dZ^T and H_c^T columns are left for the dW GEMM of
-// its batch.  Recompute mode: per
+// forward kept the exponentials; the row factors, the target entries and the
+// scaled H_c^T columns make them dZ (up to the row factor, applied to the dX
+// rows in the reduction), then one dX GEMM over the whole vocabulary; the
+// unit's dZ rows and H_c^T columns are left for the dW GEMM of its batch.
+// Recompute mode: per
 // vocabulary chunk, the chunk's logits -> its dZ, dX partials accumulated,
 // dW[:, chunk] accumulated.  Then each sample's rows are added into dX in
 // sample order (with the norm backward).  W_dx: the bf16 W_head the dX GEMM
@@ -708,8 +709,8 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const void* W
   int prev_used = 0;       // samples of the previous unit (its record is meta[prev_used - 1])
   for (int j0 = prob->j_begin; j0 < j_end; j0 += (int)ws.G) {
     const int n_s = std::min<int>(j_end - j0, (int)ws.G);
-    // a unit after the first of its batch puts its dZ^T / H_c^T columns after
-    // the previous unit's (whose last record the first mask launch reads
+    // a unit after the first of its batch puts its dZ rows / H_c^T columns
+    // after the previous unit's (whose last record the first mask launch reads
     // before any record is rewritten)
     const SampleMeta* prev = in_batch ? ws.meta + (prev_used - 1) : nullptr;
     st = run_forward_unit(prob, ws, tm, grid, j0, n_s, act, targets, resp_mask, adv, ell_old,

@@ -1,19 +1,22 @@
 // The bf16 MFMA GEMM core for gfx950 and its epilogues.
 //
-// Every contraction of the ELBO head is written in one "NT" form,
-//     C[m][n] = sum_k A[m][k] * B[n][k]      (K contiguous in both),
-// so both operands load as 16-byte K-contiguous vectors that match the MFMA
-// operand layouts directly:
+// Every contraction of the ELBO head is written in one form,
+//     C[m][n] = sum_k A[m][k] * B[n][k],
+// B always K-contiguous, so that its 16-byte vectors match the MFMA operand
+// layout directly:
 //   forward               Z^T[v][row] = WT[v][:] . Hc[row][:]     (K = d)
 //   dX (split over V)     dX^T[c][row] = W[c][:] . dZ[row][:]     (K = V)
-//   dW                    dW^T[v][c]  += dZT[v][:] . HcT[c][:]    (K = rows)
+//   dW                    dW^T[v][c]  += dZ[:][v] . HcT[c][:]     (K = rows)
 // Operand layouts: the head weights (WT, and W in the dX GEMM) are
-// row-major; the per-unit operands (Hc, dZ, dZT, HcT) are K-slab-major:
-// element (r, k) of a matrix with R rows per slab sits at
-// ((k / 64) R + r) 64 + k % 64, so the 64-deep slab of a 256-row panel that
-// one pipeline stage loads is 32 KB of contiguous memory.  (Row-major, with
-// rows V or the row count long, each slab of a panel touched 256 rows far
-// apart, and the loads ran slower.)
+// row-major; the per-unit operands (Hc, dZ, HcT) are K-slab-major: element
+// (r, k) of a matrix with R rows per slab sits at ((k / 64) R + r) 64 +
+// k % 64, so the 64-deep slab of a 256-row panel that one pipeline stage
+// loads is 32 KB of contiguous memory.  (Row-major, with rows V or the row
+// count long, each slab of a panel touched 256 rows far apart, and the loads
+// ran slower.)  The dW GEMM reads dZ, the dX GEMM's operand, as its A with
+// the roles of the two indices swapped (M = vocabulary contiguous within a
+// slab, K = rows): its fragments come from the transposing LDS read, so the
+// exponentials are kept in one layout only.
 // The logits are produced as Z^T (vocabulary along M) so that each lane holds
 // vocabulary entries of few rows: the per-row max / sum-exp reductions are
 // in-lane plus lane swaps.  dX and dW are produced transposed and stored
@@ -41,11 +44,19 @@ namespace bgpo {
 
 enum EpiKind { EPI_FWD = 0, EPI_FWDU = 1, EPI_F32_STORE = 2, EPI_F32_ACCUM = 3, EPI_DZ = 4 };
 
+// Layouts of the A operand.  A_ROW: row-major, lda elements per row (W^T, W).
+// A_MSLAB: the transpose stored slab-major, i.e. element (m, k) at
+// ((m / 64) lda + k) 64 + m % 64 with lda = K rows per slab (dZ as the dW
+// GEMM's A): M is contiguous, so its fragments are read with the transposing
+// LDS read.
+enum ALayout { A_ROW = 0, A_MSLAB = 1 };
+
 struct GemmParams {
   const uint16_t* A;
-  int64_t lda;               // row-major A: elements per row; slab-major A: rows per slab
+  int64_t lda;               // A_ROW: elements per row; A_MSLAB: rows (K) per slab
   const uint16_t* B;
   int64_t ldb;               // rows per slab (B is always slab-major)
+  int dyn_boff;              // B starts at row meta->col_off (the unit's rows of dZ)
   int M, N, K;               // static extents
   int dyn_m, dyn_n, dyn_k;   // extents taken from the device sample metadata
   int dyn_split;             // K split taken from the metadata (dX)
@@ -60,10 +71,8 @@ struct GemmParams {
   float* part_m;             // FWD: per-128-vocabulary-slice (max, sum) partials [M/WM][ldp]
   float* part_s;
   int64_t ldp;
-  uint16_t* dZ;              // FWDU: exponentials u; DZ: the chunk's dZ (slab-major, ldz rows
-  int64_t ldz;               // per slab)
-  uint16_t* dZT;             // DZ: the chunk's dZ^T (slab-major, ldzt rows per slab; columns
-  int64_t ldzt;              // from the unit's col_off)
+  uint16_t* dZ;              // FWDU: exponentials u, rows from the unit's col_off; DZ: the
+  int64_t ldz;               // chunk's dZ (slab-major, ldz rows per slab)
   const float* lse2;         // DZ: per-row log2-sum-exp2, gradient scale and target id
   const float* rscale;
   const int32_t* rtgt;
@@ -84,6 +93,33 @@ struct Cfg {
   // rows already alternate 128-byte halves)
   __device__ static __forceinline__ int swz(int row) { return (row >> 1) % KCH; }
 };
+
+// The chunk swizzle of an A_MSLAB operand in LDS: 16-byte chunk c (8 M ids)
+// of K row k sits at chunk c ^ mslab_swz(k).  A transposing fragment read
+// takes 32 bytes (two chunks) of each of 16 K rows: rows 8 g + e (e < 4) of
+// lane groups g = 0, 1, and those rows + 4.  The XOR term moves the four rows
+// of one group (bits 0 and 1 of k) to distinct 32-byte segments, and, among
+// rows of one parity (one 128-byte half of the 256 bytes that the banks
+// span), the rows of the two groups (bit 3) too; it is even, so a pair of
+// chunks stays adjacent, and it ignores bit 2, so the rows k and k + 4 of
+// the two reads share it.
+__device__ __forceinline__ int mslab_swz(int k) {
+  return 2 * (((k ^ (k >> 3)) & 1) | (k & 2));
+}
+
+// One buffer load of 16 bytes per lane straight into LDS (lds_dst + 16 per
+// lane), as inline assembly.  The compiler's own form of this load makes it
+// wait for all outstanding loads before every LDS read that it cannot prove
+// independent of them (the transposing reads of an A_MSLAB operand, which
+// carry no type information); the ring's explicit waits already order them.
+__device__ __forceinline__ void lds_load16_asm(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
+                                               uint32_t soff, const void* lds_dst) {
+  const uint32_t la = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_dst;
+  asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(soff), "s"(__builtin_amdgcn_readfirstlane(la))
+               : "memory", "m0");
+}
 
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding: vmcnt
 // in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
@@ -149,76 +185,7 @@ __device__ __forceinline__ void epi_f32_16t(const f32x4 (&acc)[TM][TN], float* o
   }
 }
 
-// Rows of a 256 x 256 tile staged in LDS as [row][vocabulary] (16-byte chunk
-// c of row r at chunk c ^ (r mod 32)) into the slab-major dZ (ldz rows per
-// slab): lane l of a store instruction takes row 2 q + l / 32 of the wave's
-// rows and physical chunk l mod 32, i.e. logical chunk (l mod 32) ^ (row mod
-// 32); an instruction writes two rows, each four whole 128-byte lines (its
-// four vocabulary slabs).  (Eight consecutive rows of one slab per
-// instruction, 1 KB of contiguous lines, measured no faster.)
-template <int BM, int ROWS_PER_WAVE>
-__device__ __forceinline__ void store_dz_rows(const char* stage, uint16_t* dZ, int64_t ldz, int m0,
-                                              int n0, int N, int M, int wave, int lane) {
-  static_assert(BM == 256, "512-byte staged rows");
-  // (the lane's chunk is re-derived here every tile: hoisted out of the
-  // tile loop, its per-row variants would be spilled)
-  int pc = lane & 31;
-  asm volatile("" : "+v"(pc));
-#pragma unroll
-  for (int q = 0; q < ROWS_PER_WAVE / 2; ++q) {
-    const int row = wave * ROWS_PER_WAVE + 2 * q + (lane >> 5);
-    const int m = m0 + 8 * (pc ^ (row & 31));
-    const uint4 v = *reinterpret_cast<const uint4*>(stage + row * 512 + pc * 16);
-    if (n0 + row < N && m < M)
-      *reinterpret_cast<uint4*>(dZ + ((int64_t)(m >> 6) * ldz + n0 + row) * 64 + (m & 63)) = v;
-  }
-}
-
-// dZ^T columns of a 256 x 256 tile staged in LDS as [row][vocabulary]
-// (16-byte chunk c of row r at chunk c ^ (r mod 32), bf16): vocabulary rows
-// m0 .. m0 + 255 of dZ^T (slab-major, ldzt rows per slab), columns
-// zt_col + n0 .. + 255.  Wave w's 64 tile rows are one 64-column slab of
-// dZ^T, in which consecutive vocabulary ids are consecutive 128-byte lines.
-// Lane l takes columns 8 (l mod 8) .. + 7 of four consecutive ids
-// 32 i + 4 (l / 8) .. + 3: eight 8-byte reads of the staged rows, then four
-// 16-byte stores, store k of every lane writing ids 4 q + k (q = 0 .. 7) of
-// the group, i.e. eight whole lines per instruction.
-template <int BM, int ROWS_PER_WAVE>
-__device__ __forceinline__ void store_dzt_columns(const char* stage, uint16_t* dZT, int64_t ldzt,
-                                                  int zt_col, int m0, int n0, int M, int wave,
-                                                  int lane) {
-  static_assert(ROWS_PER_WAVE == 64, "one dZ^T column slab per wave");
-  int lq = lane;
-  asm volatile("" : "+v"(lq));
-  const int cc = lq & 7, vq = lq >> 3;
-  uint16_t* const zt = dZT + ((int64_t)((zt_col + n0) / 64 + wave) * ldzt + m0 + 4 * vq) * 64 + cc * 8;
-  const int rbase = wave * ROWS_PER_WAVE + 8 * cc;
-#pragma unroll 2
-  for (int i = 0; i < BM / 32; ++i) {
-    // ids 32 i + 4 vq .. + 3: chunk 4 i + vq / 2, bytes 8 (vq mod 2) .. + 7
-    const int cw = ((4 * i + (vq >> 1)) << 4) + (vq & 1) * 8;
-    uint2 q[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int ra = rbase + t;
-      q[t] = *reinterpret_cast<const uint2*>(stage + ra * 512 + (cw ^ ((ra & 31) << 4)));
-    }
-    if (m0 + 32 * i < M) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        uint32_t wv[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const uint32_t a = k < 2 ? q[2 * t].x : q[2 * t].y, b = k < 2 ? q[2 * t + 1].x : q[2 * t + 1].y;
-          wv[t] = (k & 1) ? __builtin_amdgcn_perm(b, a, 0x07060302u) : __builtin_amdgcn_perm(b, a, 0x05040100u);
-        }
-        *reinterpret_cast<uint4*>(zt + (int64_t)(32 * i + k) * 64) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-      }
-    }
-  }
-}
-
-template <int EPI, bool SLAB_A, int BM, int BN, int BK, int STAGES>
+template <int EPI, int AL, int BM, int BN, int BK, int STAGES>
 __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
 #if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature
   constexpr int WM = 128, WN = 128;
@@ -227,9 +194,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   constexpr int TM = WM / 16, TN = WN / 16;
   // 64-deep slabs hold two 32-deep MFMA sub-steps between barriers
   static_assert(C::NWAVES == 4 && BK == 64, "four waves, 64-deep slabs");
-  // A is slab-major in the dW GEMM (dZ^T), row-major (W^T, W) in the others;
-  // B is always slab-major
-  constexpr bool kSlabA = SLAB_A;
+  // A is row-major (W^T, W) or M-slab-major (dZ, with transposing fragment
+  // reads); B is always K-slab-major
+  constexpr bool kMSlabA = AL == A_MSLAB;
+  static_assert(!kMSlabA || BM / 64 == C::NWAVES, "one 64-row M slab of A per wave");
   __shared__ uint4 smem[STAGES * (BM + BN) * KCH];
   uint4* As = smem;                           // [STAGES][BM][KCH]
   uint4* Bs = smem + STAGES * BM * KCH;       // [STAGES][BN][KCH]
@@ -242,9 +210,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   if (p.dyn_m) { M = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_n) { N = p.meta->n_rows_pad; n_valid = p.meta->n_rows; }
   if (p.dyn_k) K = p.meta->col_end;    // batched dW: all samples' columns (multiple of 64)
-  // first dZ^T column of the unit (EPI_DZ), read once into a scalar register
-  const int zt_col =
-      (EPI == EPI_DZ || EPI == EPI_FWDU) ? __builtin_amdgcn_readfirstlane(p.meta->col_off) : 0;
+  // first row of the unit in dZ (EPI_FWDU), read once into a scalar register
+  const int zt_col = EPI == EPI_FWDU ? __builtin_amdgcn_readfirstlane(p.meta->col_off) : 0;
+  // first row of B (the unit's rows of a dZ shared by a dW batch)
+  const int b_row0 = p.dyn_boff ? __builtin_amdgcn_readfirstlane(p.meta->col_off) : 0;
   int n_split = p.n_split;
   int64_t k_split = p.k_split;
   if (p.dyn_split) {
@@ -328,22 +297,33 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
     // scalar offset; a slab-major panel gets a descriptor per slab (its
     // slabs lie rows-per-slab x 128 bytes apart, beyond 32-bit offsets), with
     // rows 128 bytes apart inside it.
-    const char* const a_tile = reinterpret_cast<const char*>(p.A + (int64_t)m0 * (kSlabA ? 64 : p.lda));
-    const char* const b_tile = reinterpret_cast<const char*>(p.B + (int64_t)n0 * 64);
+    const char* const a_tile = reinterpret_cast<const char*>(
+        p.A + (kMSlabA ? (int64_t)(m0 / 64) * p.lda * 64 : (int64_t)m0 * p.lda));
+    const char* const b_tile = reinterpret_cast<const char*>(p.B + ((int64_t)n0 + b_row0) * 64);
     const int64_t a_slab = p.lda * 128, b_slab = p.ldb * 128;   // bytes per slab (slab-major)
-    const int a_row = kSlabA ? 128 : (int)p.lda * 2;            // bytes per row
+    const int a_row = (int)p.lda * 2;                           // bytes per row (A_ROW)
     const __amdgpu_buffer_rsrc_t a_rsrc =
         __builtin_amdgcn_make_buffer_rsrc((void*)a_tile, (short)0, 0x7FFFFFFF, 0x00020000);
     constexpr int RPI = 64 / KCH;                        // rows per load instruction
     constexpr int A_INS = BM / RPI / C::NWAVES, B_INS = BN / RPI / C::NWAVES;
     static_assert(A_INS + B_INS == BK / 4, "one slab load per 256 / BK MFMAs");
     uint32_t a_voff[A_INS], b_voff[B_INS];
+    // A_MSLAB: wave w loads M slab w of the tile (the matrix's last slab for
+    // slabs past M), K rows 8 q .. 8 q + 7 of it per instruction q, into
+    // LDS [M slab][K row][8 chunks of 8 M ids], chunk-swizzled by K row
+    const int64_t a_wslab =
+        kMSlabA ? (int64_t)(min(m0 / 64 + wave, (M + 63) / 64 - 1) - m0 / 64) * a_slab : 0;
 #pragma unroll
     for (int q = 0; q < A_INS; ++q) {
-      const int g = wave * A_INS + q, row = g * RPI + lane / KCH;
-      const int c = (lane % KCH) ^ C::swz(row);
-      const int rr = min(m0 + row, M - 1) - m0;
-      a_voff[q] = (uint32_t)(rr * a_row + c * 16);
+      if constexpr (kMSlabA) {
+        const int k = 8 * q + lane / KCH;
+        a_voff[q] = (uint32_t)(k * 128 + ((lane % KCH) ^ mslab_swz(k)) * 16);
+      } else {
+        const int g = wave * A_INS + q, row = g * RPI + lane / KCH;
+        const int c = (lane % KCH) ^ C::swz(row);
+        const int rr = min(m0 + row, M - 1) - m0;
+        a_voff[q] = (uint32_t)(rr * a_row + c * 16);
+      }
     }
 #pragma unroll
     for (int q = 0; q < B_INS; ++q) {
@@ -357,27 +337,31 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // slab c + S is loaded into slab c's stage right after the barrier that
       // ends slab c, and slabs past the tile's K range re-load its last slab.
       constexpr int NINS = A_INS + B_INS;
+      auto lds_load = [&](__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint4* dst) {
+        if constexpr (kMSlabA)
+          lds_load16_asm(r, voff, soff, dst);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16,
+                                                   voff, soff, 0, 0);
+      };
       auto issue_one = [&](int q, int stage, int e) {   // load instruction e of slab q
         const int qc = min(q, nk - 1);
         const int64_t ks = kb / BK + qc;                  // slab index in K
         if (e < A_INS) {
           uint4* dst = As + stage * BM * KCH + (wave * A_INS + e) * 64;
-          if constexpr (kSlabA) {
-            const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-                (void*)(a_tile + ks * a_slab), (short)0, 0x7FFFFFFF, 0x00020000);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                r, (__attribute__((address_space(3))) void*)dst, 16, a_voff[e], 0, 0, 0);
+          if constexpr (kMSlabA) {
+            // K slab ks of the wave's M slab: 64 rows of 128 bytes
+            lds_load(__builtin_amdgcn_make_buffer_rsrc((void*)(a_tile + a_wslab + ks * 8192), (short)0,
+                                                       0x7FFFFFFF, 0x00020000),
+                     a_voff[e], 0, dst);
           } else {
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                a_rsrc, (__attribute__((address_space(3))) void*)dst, 16, a_voff[e],
-                (int)(ks * BK * 2), 0, 0);
+            lds_load(a_rsrc, a_voff[e], (uint32_t)(ks * BK * 2), dst);
           }
         } else {
           uint4* dst = Bs + stage * BN * KCH + (wave * B_INS + e - A_INS) * 64;
-          const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-              (void*)(b_tile + ks * b_slab), (short)0, 0x7FFFFFFF, 0x00020000);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              r, (__attribute__((address_space(3))) void*)dst, 16, b_voff[e - A_INS], 0, 0, 0);
+          lds_load(__builtin_amdgcn_make_buffer_rsrc((void*)(b_tile + ks * b_slab), (short)0, 0x7FFFFFFF,
+                                                     0x00020000),
+                   b_voff[e - A_INS], 0, dst);
         }
       };
 #pragma unroll
@@ -396,6 +380,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         if (r < TN) {
           const int row = brow + 16 * r;
           db[r] = __builtin_bit_cast(bf16x8, Bs[st * BN * KCH + row * KCH + (ch ^ C::swz(row))]);
+        } else if constexpr (kMSlabA) {
+          // A[m][k .. k + 7] of M id m = 16 i + lane % 16 of the wave's rows,
+          // k = 32 ks + 8 (lane / 16), from LDS [M slab][K row][M]: two
+          // transposing reads, each returning to lane 4 q + t of a 16-lane
+          // group element t of the 8 bytes that lanes q, q + 4, q + 8, q + 12
+          // address; lane 4 e + q of group g addresses K row 8 g + e (+ 4)
+          // at M ids 16 i + 4 q .. + 3
+          const int i = r - TN, g = lane >> 4, jl = lane & 15;
+          const int kr = 32 * ks + 8 * g + (jl >> 2);
+          const int mm = wm * WM + 16 * i + 4 * (jl & 3);   // M id within the tile
+          const char* base = reinterpret_cast<const char*>(As + st * BM * KCH) + (mm >> 6) * 8192 +
+                             (((mm & 63) >> 3) ^ mslab_swz(kr)) * 16 + (mm & 7) * 2;
+          typedef short v4s __attribute__((ext_vector_type(4)));
+          typedef __attribute__((address_space(3))) v4s lds_v4s;
+          const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(base + kr * 128));
+          const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(base + (kr + 4) * 128));
+          const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+          da[i] = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
         } else {
           const int row = arow + 16 * (r - TN);
           da[r - TN] =
@@ -455,11 +457,13 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // wave row wm is partial index mw / 128).  A row's 128 entries sit in
       // its lane and the lanes l ^ 16, l ^ 32, l ^ 48.  EPI_FWDU also keeps
       // the exponentials against the row's reference R2 (exp_reference of
-      // its target logit), u = 2^(z log2e - m) 2^(m - R2), in bf16, in both
-      // dZ (rows) and dZ^T (columns from the unit's col_off): dZ is
-      // s 2^(R2 - lse2) (u - onehot 2^(lse2 - R2)), so one factor per row
-      // makes them the gradient (applied after the GEMMs), and only the
-      // target entries change.  Both variants sum in the same order, so l is
+      // its target logit), u = 2^(z log2e - m) 2^(m - R2), in bf16, in dZ
+      // (rows from the unit's col_off, the layout both backward GEMMs read):
+      // dZ is s 2^(R2 - lse2) (u - onehot 2^(lse2 - R2)), so one factor per
+      // row makes them the gradient (applied after the GEMMs), and only the
+      // target entries change.  A lane's 4 values of a block are 4
+      // consecutive vocabulary ids of one row, one 8-byte store straight from
+      // the registers.  Both variants sum in the same order, so l is
       // bit-identical between them.
       static_assert(WM == kVocabTile, "one partial per wave slice");
       constexpr bool kStore = EPI == EPI_FWDU;
@@ -474,15 +478,6 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
             for (int e = 0; e < 4; ++e)
               if (mw + 16 * i + mlane + e >= M) acc[i][j][e] = -INFINITY;
       }
-      // EPI_FWDU stages the tile's exponentials in LDS (free once the ring is
-      // drained; 256 rows x 256 vocabulary ids x bf16 = the ring's 128 KB) as
-      // [row][vocabulary], 16-byte chunk c of row r at chunk c ^ (r mod 32),
-      // and then writes whole rows of dZ (two rows of 256 ids per
-      // instruction, each four 128-byte lines of the slab-major dZ) and the
-      // tile's columns of dZ^T.
-      char* stage_u = reinterpret_cast<char*>(smem);
-      static_assert(!kStore || (BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2),
-                    "staging tile: 512-byte rows that fit the ring");
       // one 16-row column block of the wave tile at a time, so that only its
       // 32 values per lane are live outside the accumulators
       const int vt = mw / WM;
@@ -524,11 +519,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
             ssum += u[e];
           }
           if constexpr (kStore) {
-            // vocabulary ids ml .. ml + 3 of row nl into the staging tile
-            const int ml = mw - m0 + 16 * i + mlane;
-            *reinterpret_cast<uint2*>(stage_u + nl * 512 + (((ml >> 3) ^ (nl & 31)) << 4) +
-                                      (ml & 7) * 2) =
-                make_uint2(pack_bf16x2(u[0] * fac, u[1] * fac), pack_bf16x2(u[2] * fac, u[3] * fac));
+            // vocabulary ids m .. m + 3 of row n0 + nl (m + 3 stays in m's slab)
+            const int m = mw + 16 * i + mlane;
+            if (n0 + nl < N && m < M)
+              *reinterpret_cast<uint2*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + zt_col + n0 + nl) * 64 +
+                                        (m & 63)) =
+                  make_uint2(pack_bf16x2(u[0] * fac, u[1] * fac), pack_bf16x2(u[2] * fac, u[3] * fac));
           }
         }
         float st = ssum + __shfl_xor(ssum, 16, 64);
@@ -540,12 +536,6 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      if constexpr (kStore) {
-        __syncthreads();
-        constexpr int ROWS_PER_WAVE = BN / (NT / 64);
-        store_dz_rows<BM, ROWS_PER_WAVE>(stage_u, p.dZ, p.ldz, m0, n0, N, M, wave, lane);
-        store_dzt_columns<BM, ROWS_PER_WAVE>(stage_u, p.dZT, p.ldzt, zt_col, m0, n0, M, wave, lane);
-      }
     } else if constexpr (EPI == EPI_DZ) {
       // Recompute backward: the tile holds logits z of vocabulary ids
       // v0 + m (M) for rows n (N); each becomes
@@ -553,13 +543,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // in bf16 (RNE), s_n and lse2_n of the row (the derivative of the
       // scaled loss term w.r.t. the logit, Eq. per_step_loss with the
       // gradient scale of the response's bound term); padding rows get exact
-      // zeros.  The bf16 tile is staged in LDS as [row][vocabulary] (16-byte
-      // chunk c of row r at chunk c ^ (r mod 32), as the exponentials above),
-      // written as whole rows of dZ (the dX GEMM's operand) and read back
-      // down its columns for dZ^T (the dW GEMM's), both slab-major.
-      char* stage = reinterpret_cast<char*>(smem);
-      static_assert(BM == 256 && BN == 256 && STAGES * (BM + BN) * KCH * 16 >= BM * BN * 2,
-                    "staging tile: 512-byte rows that fit the ring");
+      // zeros.  Stored like the forward's exponentials: 8 bytes per lane and
+      // block straight into the chunk's slab-major dZ, which the dX GEMM reads
+      // as its B operand and the dW GEMM as its M-slab-major A operand.
       // the lane's 8 rows' log2-sum-exp2, scale and target (as a tile row
       // index, may be outside), loaded before the column blocks so that one
       // wait covers them
@@ -588,16 +574,13 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
             const float pz = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -l2));
             x[e] = live ? sr * (ml + e == ym ? pz - 1.f : pz) : 0.f;
           }
-          *reinterpret_cast<uint2*>(stage + nl * 512 + (((ml >> 3) ^ (nl & 31)) << 4) +
-                                    (ml & 7) * 2) =
-              make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+          const int m = m0 + ml;
+          if (n0 + nl < N && m < M)
+            *reinterpret_cast<uint2*>(p.dZ + ((int64_t)(m >> 6) * p.ldz + n0 + nl) * 64 + (m & 63)) =
+                make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      __syncthreads();
-      constexpr int ROWS_PER_WAVE = BN / (NT / 64);
-      store_dz_rows<BM, ROWS_PER_WAVE>(stage, p.dZ, p.ldz, m0, n0, N, M, wave, lane);
-      store_dzt_columns<BM, ROWS_PER_WAVE>(stage, p.dZT, p.ldzt, zt_col, m0, n0, M, wave, lane);
     } else {
       // fp32 store of the tile, transposed (dX partials, or a full dW tile
       // that started from its previous value), or read-modify-write of a
@@ -642,44 +625,46 @@ hipError_t launch_gemm_fwd(const Workspace& ws, int d, int V, int grid, bool sto
   p.part_m = ws.part_m; p.part_s = ws.part_s; p.ldp = ws.RP;
   p.group_m = kGroupMFwd;
   if (store_u) {
-    p.dZ = ws.dZ; p.ldz = ws.RP;
-    p.dZT = ws.dZT; p.ldzt = V;
+    p.dZ = ws.dZ; p.ldz = ws.ldz;
     p.ztgt = ws.ztgt;
-    k_gemm4w<EPI_FWDU, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    k_gemm4w<EPI_FWDU, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   } else {
-    k_gemm4w<EPI_FWD, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    k_gemm4w<EPI_FWD, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s) {
-  // dX^T[c][row] = W[c][:] . dZ[row][:], stored transposed: dx_part[row][c]
+  // dX^T[c][row] = W[c][:] . dZ[row][:] over the unit's rows of dZ, stored
+  // transposed: dx_part[row][c]
   GemmParams p = base_params();
   p.A = W; p.lda = V;
-  p.B = ws.dZ; p.ldb = ws.RP;
+  p.B = ws.dZ; p.ldb = ws.ldz; p.dyn_boff = 1;
   p.M = d; p.K = V; p.dyn_n = 1; p.meta = ws.unit();
   p.dyn_split = 1;
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
-  k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s) {
+  // dW^T[v][c] += dZ[:][v] . H_c^T[c][:] over the batch's rows (dZ read
+  // M-slab-major)
   GemmParams p = base_params();
-  p.A = ws.dZT; p.lda = V;
+  p.A = ws.dZ; p.lda = ws.ldz;
   p.B = ws.HcT; p.ldb = d;
   p.M = V; p.N = d; p.dyn_k = 1; p.meta = ws.unit();
   p.group_m = kGroupMdW;
   p.out = dW; p.ldo = V;
-  k_gemm4w<EPI_F32_ACCUM, true, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  k_gemm4w<EPI_F32_ACCUM, A_MSLAB, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_recompute(const Workspace& ws, int d, int v0, int width, int grid,
                                  hipStream_t s) {
-  // Z^T[v][row] for the chunk's ids v0 .. v0 + width - 1, epilogue -> dZ, dZ^T
+  // Z^T[v][row] for the chunk's ids v0 .. v0 + width - 1, epilogue -> dZ
   GemmParams p = base_params();
   p.A = ws.WT + (int64_t)v0 * d; p.lda = d;
   p.B = ws.Hc; p.ldb = ws.RP;
@@ -688,8 +673,7 @@ hipError_t launch_gemm_recompute(const Workspace& ws, int d, int v0, int width, 
   p.group_m = kGroupMFwd;
   p.lse2 = ws.lse2; p.rscale = ws.row_scale; p.rtgt = ws.row_tgt; p.v0 = v0;
   p.dZ = ws.dZ; p.ldz = ws.RP;
-  p.dZT = ws.dZT; p.ldzt = ws.chunk;
-  k_gemm4w<EPI_DZ, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  k_gemm4w<EPI_DZ, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -705,22 +689,23 @@ hipError_t launch_gemm_dx_chunk(const Workspace& ws, const uint16_t* W, int d, i
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
   if (first)
-    k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   else
-    k_gemm4w<EPI_F32_ACCUM, false, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+    k_gemm4w<EPI_F32_ACCUM, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_dw_chunk(const Workspace& ws, float* dW, int d, int V, int v0, int width,
                                 int grid, hipStream_t s) {
-  // dW^T[v0 + m][c] += dZ^T[m][:] . H_c^T[c][:] (K = the unit's rows)
+  // dW^T[v0 + m][c] += dZ[:][m] . H_c^T[c][:] (K = the unit's rows; dZ read
+  // M-slab-major)
   GemmParams p = base_params();
-  p.A = ws.dZT; p.lda = ws.chunk;
+  p.A = ws.dZ; p.lda = ws.RP;
   p.B = ws.HcT; p.ldb = d;
   p.M = width; p.N = d; p.dyn_k = 1; p.meta = ws.unit();
   p.group_m = kGroupMdW;
   p.out = dW + v0; p.ldo = V;
-  k_gemm4w<EPI_F32_ACCUM, true, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  k_gemm4w<EPI_F32_ACCUM, A_MSLAB, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -748,7 +733,7 @@ extern "C" int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C,
   p.out = C; p.ldo = N;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -3;
-  k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
+  k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
@@ -769,6 +754,6 @@ extern "C" int bgpo_test_gemm_split(const uint16_t* A, const uint16_t* B, float*
   p.out = C; p.ldo = N; p.split_stride = (int64_t)M * N;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -3;
-  k_gemm4w<EPI_F32_STORE, false, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
+  k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }

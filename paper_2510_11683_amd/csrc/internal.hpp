@@ -27,9 +27,14 @@ constexpr float kExpRef = 60.f;
 constexpr float kExpRange = 64.f;
 __host__ __device__ inline float exp_reference(float ztgt) { return ztgt * 1.4426950408889634f + kExpRef; }
 
-// Column capacity of H_c^T / dZ^T (the rows of a dW batch; the column
-// offsets of the sample records are 32-bit).
+// Column capacity of H_c^T, row capacity of the stored dZ (the rows of a dW
+// batch; the offsets of the sample records are 32-bit).
 constexpr int64_t kMaxColumns = int64_t(1) << 30;
+
+// Rows per slab of the stored dZ: KT plus this padding, so that the slabs of
+// one vocabulary tile (which the dW GEMM reads side by side) do not lie a
+// power of two apart.
+constexpr int64_t kDzPadRows = 64;
 
 // K-slab-major layout of a bf16 operand with R rows per slab: element (r, k)
 // at ((k / 64) R + r) 64 + k % 64 (the GEMMs' operand layout: one 64-deep
@@ -46,7 +51,7 @@ __host__ __device__ inline int64_t slab_index(int64_t R, int64_t r, int64_t k) {
 struct SampleMeta {
   int32_t n_rows;      // masked rows of the unit up to and including this sample
   int32_t n_rows_pad;  // n_rows rounded up to kRowPad
-  int32_t col_off;     // first column of the unit in H_c^T / dZ^T
+  int32_t col_off;     // first column of the unit in H_c^T (and row in the stored dZ)
   int32_t col_end;     // col_off + n_rows rounded up to 64: K of the dW GEMM
   int32_t dx_split;    // vocabulary splits of the unit's dX GEMM
   int32_t dx_kslab;    // 64-wide vocabulary slabs per split
@@ -93,20 +98,19 @@ struct Workspace {
   float* inv_rms;      // [RP]         final-RMSNorm 1/rms of each compacted row
   void* mask_scratch;  // mask_scratch_bytes(B, L): the multi-block mask passes
   float* gpart;        // [NP/256, d]  dgamma partial sums over 256-row chunks of a sample
-  uint16_t* dZ;        // stored mode: [RP rows, V] the forward's bf16 exponentials against
+  uint16_t* dZ;        // stored mode: [KT rows, V] the forward's bf16 exponentials against
                        // the row's reference, i.e. s (softmax - onehot) up to the row factor
-                       // (target entries rewritten); recompute mode: [RP rows, chunk],
-                       // one vocabulary chunk's s (softmax - onehot); slab-major
-  uint16_t* dZT;       // stored mode: [V rows, KT] the same, transposed, units of a dW batch
-                       // side by side; recompute mode: [chunk rows, KT], one chunk;
-                       // slab-major
+                       // (target entries rewritten), the units of a dW batch one after the
+                       // other (unit rows from its col_off); recompute mode: [RP rows,
+                       // chunk], one vocabulary chunk's s (softmax - onehot); slab-major
   float* dx_part;      // [S, RP, d]   split-vocabulary partial dX
   int64_t P, NP, nvt;
   int64_t G;           // samples per unit
   int64_t RP;          // G * NP: row capacity of a unit
   int64_t n_split;     // capacity of dx_part in splits (the unit's count is in its meta)
   int64_t dw_batch;    // units whose dW contributions share one GEMM
-  int64_t KT;          // dw_batch * RP: columns of H_c^T and dZ^T
+  int64_t KT;          // dw_batch * RP: columns of H_c^T, rows of the stored dZ
+  int64_t ldz;         // rows per slab of dZ: KT + kDzPadRows (stored), RP (recompute)
   int64_t chunk;       // 0: stored exponentials; > 0: recompute backward, vocabulary chunk width
   int g_used;          // samples in the current unit (host side; its record meta[g_used - 1]
                        // describes the unit)
@@ -133,9 +137,9 @@ struct Plan {
 // retain = 0: the state of one unit of G samples at a time, dw_batch units
 //             per dW GEMM; the size does not depend on n_t.
 // retain = 1: the same units (G capped at n_t), each keeping its own state
-//             (units[0 .. ceil(n_t / G)): meta, rows, partials, H_c and dZ;
-//             H_c^T / dZ^T hold all units' columns; one dW batch), so memory
-//             grows with n_t.
+//             (units[0 .. ceil(n_t / G)): meta, rows, partials, H_c; H_c^T
+//             and dZ hold all units' columns and rows; one dW batch), so
+//             memory grows with n_t.
 size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* ws,
                         Workspace* units);
 
@@ -177,8 +181,8 @@ hipError_t launch_seq_terms(const Workspace& ws, int B, int n_t, int j0, const f
 hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, int n_t,
                              double* dbar, hipStream_t s);
 // stored backward, after the unit's scales: row factors, the target entries of
-// dZ / dZ^T, H_c^T scaled by the row factors, and the rows outside the
-// exponent range recomputed
+// dZ, H_c^T scaled by the row factors, and the rows outside the exponent range
+// recomputed
 hipError_t launch_grad_scale(const Workspace& ws, int d, int V, hipStream_t s);
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s);
@@ -190,7 +194,7 @@ hipError_t launch_dx_reduce_rmsnorm(const Workspace& ws, int g, const void* x, b
                                     hipStream_t s);
 hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid, hipStream_t s);
 // recompute mode, vocabulary chunk [v0, v0 + width): the chunk's logits from
-// W^T and H_c, turned into dZ = s (softmax - onehot) (bf16, dZ and dZ^T);
+// W^T and H_c, turned into dZ = s (softmax - onehot) (bf16);
 // dX^T partials (+)= W[:, chunk] . dZ^T (first chunk: stored);
 // dW[:, chunk] += H_c^T . dZ
 hipError_t launch_gemm_recompute(const Workspace& ws, int d, int v0, int width, int grid,

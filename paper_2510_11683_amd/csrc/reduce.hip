@@ -226,23 +226,24 @@ hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, in
 }
 
 // Stored backward, once the unit's scales s are known.  The forward kept
-// u = 2^(z log2e - R2) (bf16) in dZ and dZ^T, with R2 = exp_reference(z_y)
+// u = 2^(z log2e - R2) (bf16) in dZ (the unit's rows from its col_off, ldz
+// rows per slab), with R2 = exp_reference(z_y)
 // per row; since p = u 2^(R2 - lse2),
 //     dZ = s (p - onehot) = f (u - onehot 2^(lse2 - R2)),  f = s 2^(R2 - lse2)
 // (differentiating Eq. per_step_loss, d l / d z = (onehot - p) / t; s carries
 // -loss_scale dg/dl and the 1/t).  k_grad_rows sets f per row (0 for padding)
-// and replaces the target entry of both layouts by (p_y - 1) 2^(lse2 - R2),
+// and replaces the target entry by (p_y - 1) 2^(lse2 - R2),
 // p_y from the fp32 target logit; f scales the dX rows in the reduction and
 // H_c^T's columns (k_scale_hct) for the dW GEMM.  A row with
 // lse2 - R2 > kExpRange (its target log2-probability below
 // -(kExpRef + kExpRange)) is marked: its exponentials may have left the range
-// of bf16 and of the fp32 accumulators, so k_fixup_rows recomputes the row in
-// both layouts against R2 = lse2 (f = s), from fp32 dot products.
+// of bf16 and of the fp32 accumulators, so k_fixup_rows recomputes the row
+// against R2 = lse2 (f = s), from fp32 dot products.
 __global__ __launch_bounds__(256) void k_grad_rows(
     const float* __restrict__ lse2, const float* __restrict__ row_scale,
     const float* __restrict__ ztgt, const int32_t* __restrict__ row_tgt,
-    const SampleMeta* __restrict__ meta, uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT,
-    float* __restrict__ row_f, uint8_t* __restrict__ row_bad, int V, int64_t RP) {
+    const SampleMeta* __restrict__ meta, uint16_t* __restrict__ dZ, float* __restrict__ row_f,
+    uint8_t* __restrict__ row_bad, int64_t ldz) {
   const int r = blockIdx.x * 256 + threadIdx.x;
   if (r >= meta->n_rows_pad) return;
   float f = 0.f;
@@ -255,8 +256,7 @@ __global__ __launch_bounds__(256) void k_grad_rows(
     const float val = (__builtin_amdgcn_exp2f(z2 - l2) - 1.f) * __builtin_amdgcn_exp2f(l2 - r2e);
     const uint16_t b = (uint16_t)(pack_bf16x2(val, 0.f) & 0xFFFFu);
     const int y = row_tgt[r];
-    dZ[slab_index(RP, r, y)] = b;
-    dZT[slab_index(V, y, (int64_t)meta->col_off + r)] = b;
+    dZ[slab_index(ldz, (int64_t)meta->col_off + r, y)] = b;
     row_bad[r] = bad;
   }
   row_f[r] = f;
@@ -289,8 +289,7 @@ __global__ __launch_bounds__(256) void k_scale_hct(const float* __restrict__ row
   }
 }
 
-// The marked rows of the unit, recomputed in both layouts against
-// R2 = lse2: u = 2^(z log2e - lse2) = p, and p_y - 1 at the target.  One
+// The marked rows of the unit, recomputed against R2 = lse2: u = 2^(z log2e - lse2) = p, and p_y - 1 at the target.  One
 // thread per vocabulary id; each workgroup scans the unit's marks 256 rows at
 // a time and takes the marked ones in batches of 16, whose fp32 logits
 // z = H_c[row] . W^T[v] it accumulates in a fixed order over d.  Without
@@ -301,8 +300,8 @@ __global__ __launch_bounds__(256) void k_fixup_rows(
     const uint16_t* __restrict__ Hc, const uint16_t* __restrict__ WT,
     const float* __restrict__ lse2, const float* __restrict__ ztgt,
     const int32_t* __restrict__ row_tgt, const uint8_t* __restrict__ row_bad,
-    const SampleMeta* __restrict__ meta, uint16_t* __restrict__ dZ, uint16_t* __restrict__ dZT,
-    int d, int V, int64_t RP) {
+    const SampleMeta* __restrict__ meta, uint16_t* __restrict__ dZ, int d, int V, int64_t RP,
+    int64_t ldz) {
   __shared__ int s_list[256];
   __shared__ int s_cnt;
   __shared__ float s_h[kFixBatch][64];
@@ -354,8 +353,7 @@ __global__ __launch_bounds__(256) void k_fixup_rows(
           const float val = v == row_tgt[r] ? __builtin_amdgcn_exp2f(fmaf(ztgt[r], kLog2e, -l2)) - 1.f
                                             : __builtin_amdgcn_exp2f(fmaf(acc[i], kLog2e, -l2));
           const uint16_t b = (uint16_t)(pack_bf16x2(val, 0.f) & 0xFFFFu);
-          dZ[slab_index(RP, r, v)] = b;
-          dZT[slab_index(V, v, col_off + r)] = b;
+          dZ[slab_index(ldz, col_off + r, v)] = b;
         }
       }
     }
@@ -365,15 +363,15 @@ __global__ __launch_bounds__(256) void k_fixup_rows(
 
 hipError_t launch_grad_scale(const Workspace& ws, int d, int V, hipStream_t s) {
   k_grad_rows<<<(unsigned)(ws.RP / 256), 256, 0, s>>>(ws.lse2, ws.row_scale, ws.ztgt, ws.row_tgt,
-                                                      ws.unit(), ws.dZ, ws.dZT, ws.row_f,
-                                                      ws.row_bad, V, ws.RP);
+                                                      ws.unit(), ws.dZ, ws.row_f, ws.row_bad,
+                                                      ws.ldz);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   k_scale_hct<<<dim3((unsigned)(ws.RP / 64), (unsigned)(d / 64)), 256, 0, s>>>(ws.row_f, ws.unit(),
                                                                              ws.HcT, d);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   k_fixup_rows<<<(unsigned)((V + 255) / 256), 256, 0, s>>>(ws.Hc, ws.WT, ws.lse2, ws.ztgt,
                                                            ws.row_tgt, ws.row_bad, ws.unit(),
-                                                           ws.dZ, ws.dZT, d, V, ws.RP);
+                                                           ws.dZ, d, V, ws.RP, ws.ldz);
   return hipGetLastError();
 }
 
