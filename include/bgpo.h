@@ -160,15 +160,15 @@ typedef struct bgpo_problem {
 /* Backward modes and the workspace budget.  Both keep device memory constant
  * in n_t; they trade memory for work:
  *   stored exponentials   the forward GEMM of a unit of samples keeps the
- *                         exponentials of its logits (bf16, rows x V, in two
- *                         layouts) against one reference per row, the target
- *                         logit plus 60 in log2 units, so that
- *                         dZ = s (softmax - onehot) is one factor per row
- *                         times them, except at the target; the dX and dW
- *                         GEMMs read all of it: three GEMM passes per sample,
- *                         a workspace of about rows x V x 6 bytes per unit
- *                         (31 GB at B=8, L=512, d=4096, V=126464 with units
- *                         of 8 samples).  A row whose target log2-probability
+ *                         exponentials of its logits (bf16, rows x V, one
+ *                         layout that the dX and dW GEMMs both read) against
+ *                         one reference per row, the target logit plus 60 in
+ *                         log2 units, so that dZ = s (softmax - onehot) is
+ *                         one factor per row times them, except at the
+ *                         target: three GEMM passes per sample, a workspace
+ *                         of about rows x V x 4 bytes per unit (the two units
+ *                         of a dW batch; 23 GB at B=8, L=512, d=4096,
+ *                         V=126464 with units of 8 samples).  A row whose target log2-probability
  *                         is below -124 (its exponentials would leave the
  *                         range of bf16 and of the fp32 accumulators) is
  *                         recomputed after the forward from fp32 dot
@@ -176,7 +176,7 @@ typedef struct bgpo_problem {
  *   recompute             the forward keeps only the per-row log-sum-exp; the
  *                         backward walks the vocabulary in chunks of C
  *                         entries, recomputing that chunk's logits, writing
- *                         its dZ (rows x C, two layouts) and accumulating dX
+ *                         its dZ (rows x C) and accumulating dX
  *                         and dW before the next chunk: four GEMM passes per
  *                         sample, nothing of size rows x V is ever stored
  * ws_budget = 0 and vocab_chunk = 0 give the stored mode with units of up to
