@@ -112,10 +112,12 @@ __device__ __forceinline__ int mslab_swz(int k) {
 // wait for all outstanding loads before every LDS read that it cannot prove
 // independent of them (the transposing reads of an A_MSLAB operand, which
 // carry no type information); the ring's explicit waits already order them.
+// The LDS-DMA load reads M0 one wait state after the scalar write at the
+// earliest (the s_nop; the compiler does not see inside the statement).
 __device__ __forceinline__ void lds_load16_asm(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
                                                uint32_t soff, const void* lds_dst) {
   const uint32_t la = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_dst;
-  asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+  asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
                :
                : "v"(voff), "s"(rsrc), "s"(soff), "s"(__builtin_amdgcn_readfirstlane(la))
                : "memory", "m0");
