@@ -131,6 +131,25 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// A per-row value for each of a lane's 8 accumulator rows, row
+// nw + 16 j + (lane % 16) for j = 0 .. 7: the wave's 128 rows in two
+// coalesced loads (lane l takes rows nw + l and nw + 64 + l, f of the loaded
+// value, or `fill` at rows not below n_valid), then lane shuffles.  With one
+// load per row the compiler issued and waited for the eight loads one after
+// the other, and where a row's value was first used inside a conditional
+// block it waited again there for every outstanding store.  (Clamped
+// unconditional loads, to have both in flight under one wait, changed the
+// register allocation: spill reloads then waited inside the column loop.)
+template <typename T, typename F>
+__device__ __forceinline__ void rows_of_lane(const T* src, int nw, int n_valid, int lane, T fill,
+                                             F f, T (&out)[8]) {
+  const int na = nw + lane, nb = nw + 64 + lane;
+  const T a = na < n_valid ? f(src[na]) : fill;
+  const T b = nb < n_valid ? f(src[nb]) : fill;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) out[j] = __shfl(j < 4 ? a : b, 16 * (j & 3) + (lane & 15), 64);
+}
+
 // ---------------------------------------------------------------------------
 // The production kernel: one wave per SIMD on v_mfma_f32_16x16x32_bf16.
 //
@@ -489,14 +508,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       float* const ps = p.part_s + (int64_t)vt * p.ldp;
       // the references of the lane's 8 rows, loaded before the column blocks
       // so that one wait covers them (padding rows: R2 = 0)
+      static_assert(TN == 8, "8 rows per lane");
       float r2v[TN];
-      if constexpr (kStore) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int n = nw + 16 * j + (lane & 15);
-          r2v[j] = n < n_valid ? exp_reference(p.ztgt[n]) : 0.f;
-        }
-      }
+      if constexpr (kStore)
+        rows_of_lane(p.ztgt, nw, n_valid, lane, 0.f, [](float z) { return exp_reference(z); }, r2v);
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         float mx = -INFINITY;
@@ -553,14 +568,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
       // wait covers them
       float l2v[TN], srv[TN];
       int ymv[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = nw + 16 * j + (lane & 15);
-        const bool live = n < n_valid;
-        l2v[j] = live ? p.lse2[n] : 0.f;
-        srv[j] = live ? p.rscale[n] : 0.f;
-        ymv[j] = live ? p.rtgt[n] - p.v0 - m0 : -1;
-      }
+      const int ysh = p.v0 + m0;
+      rows_of_lane(p.lse2, nw, n_valid, lane, 0.f, [](float v) { return v; }, l2v);
+      rows_of_lane(p.rscale, nw, n_valid, lane, 0.f, [](float v) { return v; }, srv);
+      rows_of_lane(p.rtgt, nw, n_valid, lane, -1, [ysh](int y) { return y - ysh; }, ymv);
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int nl = nw - n0 + 16 * j + (lane & 15);
