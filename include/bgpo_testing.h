@@ -33,6 +33,20 @@ int bgpo_test_gemm_nt(const uint16_t* A, const uint16_t* B, float* C, int32_t M,
 int bgpo_test_gemm_split(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
                          int32_t K, int32_t n_split, void* stream);
 
+/* The dW GEMM's kernel alone, in its operand layouts: A is read with its
+ * indices' roles swapped (the layout of the kept exponentials, M contiguous
+ * within 64-wide slabs, through the transposing LDS reads) and the product
+ * is added to C:
+ *   C[n][m] += sum_k A[m][k] * B[n][k]   (fp32 accumulation into C)
+ * A bf16 with element (m, k) at index ((m / 64) K + k) 64 + m % 64, i.e.
+ * [M/64][K][64]; B bf16 in the K-slab-major layout, element (n, k) at
+ * ((k / 64) N + n) 64 + k % 64, i.e. [K/64][N][64]; C float [N, M]
+ * row-major, read and written; all device memory.  Requires N >= 1 and M, K
+ * positive multiples of 64.  Returns 0, -1 (invalid argument) or -3 (HIP
+ * error).  Enqueued on `stream` (hipStream_t). */
+int bgpo_test_gemm_tn(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
+                      int32_t K, void* stream);
+
 /* The multi-block form of the mask and compaction step (the three passes the
  * library uses above 65536 positions: mask words with per-block counts, a
  * one-block scan of the counts, a scatter), run at any size, with the same

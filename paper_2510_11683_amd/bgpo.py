@@ -90,13 +90,15 @@ def _load():
     lib.bgpo_moments_summary.argtypes = [vp, vp, vp, ctypes.c_int64, i32, vp, vp, sz, vp]
     lib.bgpo_test_gemm_nt.argtypes = [vp, vp, vp, i32, i32, i32, vp]
     lib.bgpo_test_gemm_split.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp]
+    lib.bgpo_test_gemm_tn.argtypes = [vp, vp, vp, i32, i32, i32, vp]
     lib.bgpo_test_mask_scratch_bytes.restype = sz
     lib.bgpo_test_mask_scratch_bytes.argtypes = [P(_Problem)]
     lib.bgpo_test_mask_multiblock.argtypes = [P(_Problem), vp, i32, vp, vp, vp, vp, sz, vp]
     for f in ("bgpo_workspace_size", "bgpo_workspace_plan", "bgpo_sample_masks", "bgpo_elbo_fwd",
               "bgpo_elbo_bwd_accumulate", "bgpo_elbo_bwd_accumulate_noalloc", "bgpo_elbo_fwd_rmsnorm",
               "bgpo_elbo_bwd_accumulate_rmsnorm", "bgpo_moments_update", "bgpo_moments_summary",
-              "bgpo_test_gemm_nt", "bgpo_test_gemm_split", "bgpo_test_mask_multiblock"):
+              "bgpo_test_gemm_nt", "bgpo_test_gemm_split", "bgpo_test_gemm_tn",
+              "bgpo_test_mask_multiblock"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -386,6 +388,19 @@ def bgpo_test_gemm_split(A, B, C, n_split: int, stream=None):
                                      _ptr(C, "C", (torch.float32,), (n_split, M, N)), M, N, K,
                                      int(n_split), _stream(stream)),
            "bgpo_test_gemm_split")
+
+
+def bgpo_test_gemm_tn(A, B, C, stream=None):
+    """Test hook: C[n, m] += sum_k A[m, k] B[n, k] through the dW GEMM's kernel,
+    in its operand layouts: A [M/64, K, 64] (element (m, k) at
+    [m // 64, k, m % 64]), B K-slab-major [K/64, N, 64] (element (n, k) at
+    [k // 64, n, k % 64]), C float32 [N, M]."""
+    MS, K, _ = A.shape
+    KS, N, _ = B.shape
+    M = MS * 64
+    _check(_lib.bgpo_test_gemm_tn(_ptr(A, "A", _BF16, (MS, K, 64)), _ptr(B, "B", _BF16, (K // 64, N, 64)),
+                                  _ptr(C, "C", (torch.float32,), (N, M)), M, N, K, _stream(stream)),
+           "bgpo_test_gemm_tn")
 
 
 def device_inputs(x: dict, device="cuda") -> dict:

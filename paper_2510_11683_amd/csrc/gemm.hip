@@ -770,3 +770,22 @@ extern "C" int bgpo_test_gemm_split(const uint16_t* A, const uint16_t* B, float*
   k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
+
+// ---- test hook: the dW GEMM's kernel alone (A M-slab-major, read through the
+// transposing LDS reads; B K-slab-major), C[n][m] += sum_k A[m][k] B[n][k] ----
+extern "C" int bgpo_test_gemm_tn(const uint16_t* A, const uint16_t* B, float* C, int32_t M, int32_t N,
+                                 int32_t K, void* stream) {
+  using namespace bgpo;
+  if (!A || !B || !C || M <= 0 || N <= 0 || K <= 0 || K % 64 || M % 64) return -1;
+  if ((int64_t)((M + 255) / 256) * ((N + 255) / 256) >= (int64_t(1) << 30)) return -1;
+  GemmParams p = base_params();
+  p.A = A; p.lda = K;          // [M/64][K][64]
+  p.B = B; p.ldb = N;          // [K/64][N][64]
+  p.M = M; p.N = N; p.K = K;
+  p.group_m = kGroupMdW;
+  p.out = C; p.ldo = M;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -3;
+  k_gemm4w<EPI_F32_ACCUM, A_MSLAB, BGPO_TILE4><<<gemm_grid(dev), kGemmThreads4, 0, (hipStream_t)stream>>>(p);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}

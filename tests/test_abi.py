@@ -119,6 +119,20 @@ def test_null_pointers_and_workspace_rejected_before_hip(b):
                                         ws_small, nbytes.value, None, None) == -1
 
 
+def test_gemm_hooks_check_shapes_before_hip(b):
+    """The GEMM-core test hooks refuse shapes their layouts cannot hold before
+    any device call (the pointers are never dereferenced)."""
+    lib = b._lib
+    fake = ctypes.c_void_p(0x1000)
+    for M, N, K in ((64, 64, 0), (64, 64, 96), (0, 64, 64), (64, 0, 64)):
+        assert lib.bgpo_test_gemm_nt(fake, fake, fake, M, N, K, None) == -1
+        assert lib.bgpo_test_gemm_tn(fake, fake, fake, M, N, K, None) == -1
+    # the dW GEMM's A layout holds whole 64-wide slabs of M
+    assert lib.bgpo_test_gemm_tn(fake, fake, fake, 96, 64, 64, None) == -1
+    assert lib.bgpo_test_gemm_tn(None, fake, fake, 64, 64, 64, None) == -1
+    assert lib.bgpo_test_gemm_split(fake, fake, fake, 64, 64, 64, 0, None) == -1
+
+
 def test_problem_struct_layout(b):
     # matches the C struct: 8 int32, uint64, uint32, int32, int64, float, 3 int32, uint64
     assert ctypes.sizeof(b._Problem) == 80

@@ -60,6 +60,30 @@ def test_gemm_core_matches_fp32_reference(M, N, K):
     assert err <= 1e-5 * (K ** 0.5) * ref.abs().max().item() + 1e-5, err
 
 
+@pytest.mark.parametrize("M,N,K", [(320, 200, 192), (512, 768, 1024), (64, 1000, 64),
+                                   (4288, 576, 256), (256, 256, 8192)])
+def test_gemm_core_transposed_a_matches_fp32_reference(M, N, K):
+    """The dW GEMM's kernel (bgpo_test_gemm_tn): A read with its indices
+    swapped through the transposing LDS reads, accumulated into C. Ragged
+    tiles in M (by 64-wide slabs) and N, one slab of K and 128; twice in a
+    row from a nonzero C, so both the read-modify-write of partial tiles and
+    the accumulator preload of full tiles are checked against exact products
+    of the bf16 operands."""
+    g = torch.Generator().manual_seed(M * 5 + N + K)
+    A = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    Bm = torch.randn(N, K, generator=g).to(torch.bfloat16)
+    C0 = torch.randn(N, M, generator=g)
+    prod = Bm.double() @ A.double().T                     # [N, M], exact products of bf16 values
+    A_l = A.reshape(M // 64, 64, K).permute(0, 2, 1).contiguous()      # [M/64, K, 64]
+    C = C0.clone().cuda()
+    for rep in (1, 2):
+        lib().bgpo_test_gemm_tn(A_l.cuda(), _slab_major(Bm).cuda(), C)
+        torch.cuda.synchronize()
+        ref = C0.double() + rep * prod
+        err = (C.cpu().double() - ref).abs().max().item()
+        assert err <= 2e-5 * (K ** 0.5) * prod.abs().max().item() + 1e-4, (rep, err)
+
+
 @pytest.mark.parametrize("M,N,K,n_split", [(300, 200, 640, 4), (257, 520, 192, 3), (64, 64, 64, 4),
                                            (512, 256, 4096, 7)])
 def test_gemm_core_split_k(M, N, K, n_split):
