@@ -72,7 +72,7 @@ def test_gemm_core_transposed_a_matches_fp32_reference(M, N, K):
     g = torch.Generator().manual_seed(M * 5 + N + K)
     A = torch.randn(M, K, generator=g).to(torch.bfloat16)
     Bm = torch.randn(N, K, generator=g).to(torch.bfloat16)
-    C0 = torch.randn(N, M, generator=g)
+    C0 = torch.randn(N, M, generator=g, dtype=torch.float32)
     prod = Bm.double() @ A.double().T                     # [N, M], exact products of bf16 values
     A_l = A.reshape(M // 64, 64, K).permute(0, 2, 1).contiguous()      # [M/64, K, 64]
     C = C0.clone().cuda()

@@ -18,7 +18,17 @@ from hypothesis import given, settings, strategies as st
 from oracle import elbo
 from test_oracle_elbo import _rand_problem
 
-torch.set_default_dtype(torch.float64)
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    """torch's autograd pins in this module run in float64; the default is
+    restored afterwards, so that other modules (collected in the same
+    process) keep float32."""
+    prev = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(prev)
 MODES = (elbo.BOUND_PAPER, elbo.BOUND_TAYLOR, elbo.BOUND_JENSEN, elbo.BOUND_EXACT)
 
 

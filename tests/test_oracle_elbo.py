@@ -32,7 +32,17 @@ from scipy.special import logsumexp
 import workloads
 from oracle import elbo
 
-torch.set_default_dtype(torch.float64)
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    """torch's autograd pins in this module run in float64; the default is
+    restored afterwards, so that other modules (collected in the same
+    process) keep float32."""
+    prev = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(prev)
 
 
 def _rand_problem(seed, B=2, L=6, d=4, V=8, n_t=3, w_scale=0.5):

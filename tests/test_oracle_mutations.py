@@ -8,9 +8,20 @@ mis-indexed operand.
 """
 import numpy as np
 import pytest
+import torch
 
 from oracle import elbo
 import test_oracle_elbo as pins
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    """The pins' torch autograd references run in float64 (as in their own
+    module); the default is restored afterwards."""
+    prev = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(prev)
 
 ALL_PINS = [
     pins.check_log_softmax,
