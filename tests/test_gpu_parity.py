@@ -318,13 +318,19 @@ def test_mid_parity_peaky_logits(w_std):
     _check_against_oracle(w, r.out(), ref, range(w.n_t), x["adv"], ell_old, 0.25)
 
 
-def test_mid_parity_rows_outside_exponent_range():
+@pytest.mark.parametrize("n_t", [3, 12], ids=["one_unit", "two_units_one_dw_batch"])
+def test_mid_parity_rows_outside_exponent_range(n_t):
     """The stored backward keeps a row's exponentials against its target
     logit plus 60 (log2 units); rows whose log2-sum-exp exceeds that by more
     than 64 (target log-probability below about -86) are recomputed after the
     forward.  With W ~ N(0, 1) (logit std 24) about half of the rows are such
-    rows (counted here from float64 logits), off-policy, both bound branches."""
-    w = MID.replace(w_std=1.0)
+    rows (counted here from float64 logits), off-policy, both bound branches.
+    With 12 samples the second unit's rows sit after the first's in the dZ
+    of their shared dW batch, so its recomputed rows are written there too."""
+    w = MID.replace(w_std=1.0, n_t=n_t)
+    if n_t == 12:
+        plan = lib().bgpo_workspace_plan(problem(w))
+        assert plan["samples_per_unit"] == 8 and plan["dw_batch"] == 2 and plan["mode"] == "stored"
     x = workloads.generate(w)
     H = elbo.bf16_to_f64(x["hidden"]).reshape(-1, w.d)
     z = H @ elbo.bf16_to_f64(x["W"])
