@@ -380,7 +380,8 @@ def main():
         "input_gen_s": gen_s,
     }
     if not args.no_variants:
-        out["variants"] = {"per_sample_rmsnorm": per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens),
+        out["variants"] = {"forward_only": forward_only_leg(w, prob, dev, ws, args, tokens),
+                           "per_sample_rmsnorm": per_sample_rmsnorm_leg(w, prob, dev, ws, args, tokens),
                            "exact_objective_off_policy": exact_objective_leg(w, prob, dev, ws, args,
                                                                              tokens)}
     # the remaining legs allocate their own workspaces and buffers
@@ -579,6 +580,34 @@ def retained_memory_leg(w, prob, dev, n_ts=(1, 4, 16)):
     res["constant_mode_workspace_bytes"] = bgpo.bgpo_workspace_size(
         dataclasses.replace(prob, bound=bgpo.BGPO_BOUND_EXACT))
     return res
+
+
+def forward_only_leg(w, prob, dev, ws, args, tokens_main):
+    """bgpo_elbo_fwd over all samples (l of every sample, no gradient: how
+    l_old is produced with the old head weights), same workspace."""
+    import torch
+    from paper_2510_11683_amd import bgpo
+    ell = torch.zeros(w.B, w.n_t, dtype=torch.float64, device="cuda")
+    nm = torch.zeros(w.B, w.n_t, dtype=torch.int32, device="cuda")
+
+    def step():
+        bgpo.bgpo_elbo_fwd(prob, dev["hidden"], dev["W"], dev["targets"], dev["resp_mask"], ell, nm,
+                           None, ws)
+    steps = max(1, min(args.steps, 3))
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    tokens = int(nm.sum().item())
+    assert tokens == tokens_main
+    return {"value": tokens / (ms / 1e3), "unit": "masked tokens/s", "ms_per_step": ms,
+            "steps": steps, "mfma_frac_2dV": 2.0 * w.d * w.V * tokens / (ms / 1e3) / (PEAK_BF16_TFLOPS * 1e12)}
 
 
 def exact_objective_leg(w, prob, dev, ws, args, tokens_main):
