@@ -462,7 +462,7 @@ def memory_vs_n_t(w, prob, dev, x, n_ts=(1, 4, 16, 64)):
     return res
 
 
-def budget_sweep_leg(w, dev, budgets_gib=(2, 4, 8, 16, 32), n_ts=(1, 64)):
+def budget_sweep_leg(w, dev, budgets_gib=(2, 4, 8, 16, 32, 48), n_ts=(1, 64)):
     """Masked tokens/s and peak device memory of one backward call over all
     samples under each workspace budget (the layout it picks: stored
     exponentials with smaller units, or the recompute backward), for

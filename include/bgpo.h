@@ -180,10 +180,12 @@ typedef struct bgpo_problem {
  *                         and dW before the next chunk: four GEMM passes per
  *                         sample, nothing of size rows x V is ever stored
  * ws_budget = 0 and vocab_chunk = 0 give the stored mode with units of up to
- * 8 samples within about 32 GB.  A nonzero ws_budget picks the largest
- * stored-mode unit (and dW batch, dX split capacity) whose workspace fits;
- * if none does, the recompute mode with the unit and chunk width of least
- * estimated extra traffic that fits; if nothing fits, BGPO_ERR_BUDGET.
+ * 8 samples within about 32 GB.  A nonzero ws_budget takes that layout if
+ * it fits, with the dW batch raised to up to 4 units while the budget allows
+ * (fewer read-modify-writes of dW); below it, the stored-mode layout (unit,
+ * dW batch, dX split capacity) of least estimated time that fits; if none
+ * does, the recompute mode with the unit and chunk width of least estimated
+ * extra traffic that fits; if nothing fits, BGPO_ERR_BUDGET.
  * vocab_chunk > 0 forces the recompute mode with that chunk (units sized by
  * ws_budget, or within 32 GB when it is 0).  The smallest layout is the
  * recompute mode with units of one sample and chunks of 256 entries: about

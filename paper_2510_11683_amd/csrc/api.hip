@@ -36,6 +36,10 @@ static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 constexpr int64_t kMaxUnit = 8;
 constexpr int64_t kDwUnits = 2;   // units per dW GEMM in the constant-memory mode
+// units per dW GEMM that a workspace budget above the default layout may buy
+// (each halving of the dW read-modify-writes saves about 1 % of the step at
+// the LLaDA head shape)
+constexpr int64_t kDwUnitsMax = 4;
 constexpr int64_t kGiB = int64_t(1) << 30;
 
 static int64_t padded_positions(const Dims& dm) {
@@ -206,11 +210,20 @@ static int choose_plan(const bgpo_problem* p, Plan* out) {
   }
   const int64_t NP = padded_positions(dm);
   if (p->vocab_chunk == 0) {
-    // the default layout if it fits, else the stored-mode layout of least
-    // estimated time that fits
+    // the default layout if it fits (with the largest dW batch the budget
+    // allows on top of it), else the stored-mode layout of least estimated
+    // time that fits
     const Plan dflt = default_plan(dm, 0, f32);
     if (plan_bytes(dm, dflt) <= budget) {
       *out = dflt;
+      for (int64_t dwb = kDwUnitsMax; dwb > dflt.dw_batch; --dwb) {
+        Plan pl = dflt;
+        pl.dw_batch = dwb;
+        if (dwb * dflt.G * NP <= kMaxColumns && plan_bytes(dm, pl) <= budget) {
+          *out = pl;
+          break;
+        }
+      }
       return BGPO_OK;
     }
     bool found = false;
@@ -344,7 +357,7 @@ static int plan_problem(const bgpo_problem* p, Plan* pl) {
   // sample records).  One unit's row capacity stays within 65535 * 64 by
   // construction; with every sample retained KT grows with n_t and is
   // bounded here.
-  static_assert(int64_t(65535) * 64 / 256 * 256 * kDwUnits <= kMaxColumns,
+  static_assert(int64_t(65535) * 64 / 256 * 256 * kDwUnitsMax <= kMaxColumns,
                 "constant-mode KT must fit the column range");
   Workspace w;
   workspace_layout(Dims{p->B, p->L, p->d, p->V, p->n_t}, *pl, nullptr, &w, nullptr);

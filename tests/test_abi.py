@@ -256,6 +256,21 @@ def test_budget_picks_layouts_that_fit(b):
     assert e.value.status == b.BGPO_ERR_BUDGET
 
 
+def test_budget_above_the_default_raises_the_dw_batch(b):
+    """A budget the default layout fits in keeps its units and raises its dW
+    batch (fewer read-modify-writes of dW) as far as the budget allows, up to
+    four units; without a budget the default batch of two stays."""
+    dflt = b.bgpo_workspace_plan(_prob(b))
+    assert dflt["dw_batch"] == 2
+    seen = []
+    for budget in (24, 32, 40, 48, 64):
+        plan = b.bgpo_workspace_plan(_prob(b, ws_budget=budget * GiB))
+        assert plan["workspace_bytes"] <= budget * GiB
+        assert plan["samples_per_unit"] == dflt["samples_per_unit"] and plan["mode"] == "stored"
+        seen.append(plan["dw_batch"])
+    assert seen == sorted(seen) and seen[0] == 2 and seen[-1] == 4
+
+
 def test_forced_vocab_chunk_and_fp32_copy(b):
     """vocab_chunk > 0 forces the recompute layout (much smaller than the
     stored one at the same unit size); fp32 inputs add a bf16 copy of W."""

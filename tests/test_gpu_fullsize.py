@@ -123,13 +123,16 @@ def test_llada_head_B8_L512_nt64_all_samples():
     assert n > 100_000
 
 
-@pytest.mark.parametrize("budget", [2 * GiB, 8 * GiB], ids=["budget_2GiB_recompute", "budget_8GiB_stored"])
+@pytest.mark.parametrize("budget", [2 * GiB, 8 * GiB, 48 * GiB],
+                         ids=["budget_2GiB_recompute", "budget_8GiB_stored", "budget_48GiB_dw_batch_4"])
 def test_llada_head_B8_L512_nt64_under_budget(budget):
     from paper_2510_11683_amd import bgpo
     w = workloads.LLADA_L512_NT64
     plan = bgpo.bgpo_workspace_plan(bgpo.Problem(w.B, w.L, w.d, w.V, w.n_t, ws_budget=budget))
     assert plan["workspace_bytes"] <= budget
     assert plan["mode"] == ("recompute" if budget == 2 * GiB else "stored")
+    if budget == 48 * GiB:
+        assert plan["dw_batch"] == 4
     n = _run_and_compare(w, ws_budget=budget)
     assert n > 100_000
 
