@@ -289,7 +289,8 @@ __global__ __launch_bounds__(256) void k_scale_hct(const float* __restrict__ row
   }
 }
 
-// The marked rows of the unit, recomputed against R2 = lse2: u = 2^(z log2e - lse2) = p, and p_y - 1 at the target.  One
+// The marked rows of the unit, recomputed against R2 = lse2:
+// u = 2^(z log2e - lse2) = p, and p_y - 1 at the target.  One
 // thread per vocabulary id; each workgroup scans the unit's marks 256 rows at
 // a time and takes the marked ones in batches of 16, whose fp32 logits
 // z = H_c[row] . W^T[v] it accumulates in a fixed order over d.  Without
