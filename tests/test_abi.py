@@ -213,8 +213,8 @@ def test_reserved_field_and_rmsnorm_arguments_rejected_before_hip(b):
 
 
 def test_retained_rows_bounded_by_the_column_range(b):
-    """H_c^T and dZ^T hold one column per kept row (32-bit column offsets in
-    the sample records): with every sample retained, the kept rows (whole
+    """H_c^T holds one column and the kept dZ one row per kept row (32-bit
+    offsets in the sample records): with every sample retained, the kept rows (whole
     units of samples, B*L rounded up to 256 per sample) must stay at or below
     2^30.  At B*L = 2^20 a unit holds 3 samples: n_t = 1023 keeps 341 units
     (1023 * 2^20 rows), n_t = 1024 one unit more; the constant mode takes any

@@ -407,8 +407,9 @@ def test_linearity_and_determinism():
 def test_timing_record_counts_kernel_launches():
     """The optional timing record adds, per kernel class, the elapsed time and
     the number of kernel launches: 10 samples in units of 8 give 2 units; per
-    unit one forward and dX GEMM launch, the three softmax-gradient kernels
-    (row factors and target entries, H_c^T scaling, recomputed rows), one
+    unit one forward and dX GEMM launch, the three row-factor kernels of the
+    gradient (row factors and target entries, H_c^T scaling, recomputed
+    rows; class BGPO_K_SOFTMAX_GRAD), one
     gather, the three row reductions (target logit, log-sum-exp, per-response
     terms), and one mask and one dX reduction per sample; one dW GEMM for the
     batch of both units; the W transpose once per call."""
