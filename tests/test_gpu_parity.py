@@ -61,7 +61,7 @@ def test_gemm_core_matches_fp32_reference(M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(320, 200, 192), (512, 768, 1024), (64, 1000, 64),
-                                   (4288, 576, 256), (256, 256, 8192)])
+                                   (4288, 576, 256), (256, 256, 8192), (128, 1, 128)])
 def test_gemm_core_transposed_a_matches_fp32_reference(M, N, K):
     """The dW GEMM's kernel (bgpo_test_gemm_tn): A read with its indices
     swapped through the transposing LDS reads, accumulated into C. Ragged
