@@ -323,7 +323,7 @@ def main():
         # (softmax_grad: three small kernels per unit, counter bytes only;
         # dx_reduce: depends on the split count)
         return {"gather": 6.0 * rows * d,                # read rows, write H_c and H_c^T
-                "transpose_w": 4.0 * d * V}.get(k)
+                "transpose_w": 6.0 * d * V}.get(k)       # read W, write W^T and W slab-major
     for k, e in per_kernel.items():
         if k in GEMM_CLASSES:
             continue

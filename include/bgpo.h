@@ -167,8 +167,10 @@ typedef struct bgpo_problem {
  *                         one factor per row times them, except at the
  *                         target: three GEMM passes per sample, a workspace
  *                         of about rows x V x 4 bytes per unit (the two units
- *                         of a dW batch; 23 GB at B=8, L=512, d=4096,
- *                         V=126464 with units of 8 samples).  A row whose target log2-probability
+ *                         of a dW batch; 24 GB at B=8, L=512, d=4096,
+ *                         V=126464 with units of 8 samples).  The dX GEMM
+ *                         reads a slab-major bf16 copy of W_head (2 d V
+ *                         bytes, re-staged every call).  A row whose target log2-probability
  *                         is below -124 (its exponentials would leave the
  *                         range of bf16 and of the fp32 accumulators) is
  *                         recomputed after the forward from fp32 dot
@@ -190,8 +192,8 @@ typedef struct bgpo_problem {
  * ws_budget, or within 32 GB when it is 0).  The smallest layout is the
  * recompute mode with units of one sample and chunks of 256 entries: about
  * 2 d V + B L (8 d + V / 16) bytes (the first term is the transposed head,
- * re-staged every call; with BGPO_F32 inputs a bf16 copy of W_head adds
- * another 2 d V).  bgpo_workspace_size reports the size of the chosen layout
+ * re-staged every call; the recompute mode reads a bf16 W_head in place,
+ * and with BGPO_F32 inputs its slab-major bf16 copy adds another 2 d V).  bgpo_workspace_size reports the size of the chosen layout
  * (at most ws_budget). */
 
 /* Kernel classes reported by the optional timing record. */
@@ -234,8 +236,10 @@ int bgpo_workspace_size(const bgpo_problem* prob, size_t* bytes);
 
 /* The layout bgpo_workspace_size measures for `prob` (see the backward
  * modes above): samples per unit, units per dW GEMM (stored mode), capacity of
- * the dX split partials, vocabulary chunk width (0 = stored exponentials) and
- * the workspace bytes.  Returns BGPO_OK or the status of bgpo_workspace_size.
+ * the dX split partials, vocabulary chunk width (0 = stored exponentials), the
+ * workspace bytes and whether the layout keeps a slab-major copy of W_head
+ * (the default layout and the budget layouts of least estimated time do; a
+ * tight budget may trade it for a larger unit).  Returns BGPO_OK or the status of bgpo_workspace_size.
  * Host only. */
 typedef struct bgpo_plan_info {
   int32_t samples_per_unit;
@@ -243,6 +247,8 @@ typedef struct bgpo_plan_info {
   int32_t dx_splits;
   int32_t vocab_chunk;
   uint64_t workspace_bytes;
+  int32_t w_copy;       /* 1: the workspace holds the slab-major bf16 copy of W_head
+                           that the dX GEMM reads; 0: the dX GEMM reads W_head itself */
 } bgpo_plan_info;
 
 int bgpo_workspace_plan(const bgpo_problem* prob, bgpo_plan_info* info);

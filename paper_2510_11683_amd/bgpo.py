@@ -47,7 +47,7 @@ class _Problem(ctypes.Structure):
 class _PlanInfo(ctypes.Structure):
     _fields_ = [("samples_per_unit", ctypes.c_int32), ("dw_batch", ctypes.c_int32),
                 ("dx_splits", ctypes.c_int32), ("vocab_chunk", ctypes.c_int32),
-                ("workspace_bytes", ctypes.c_uint64)]
+                ("workspace_bytes", ctypes.c_uint64), ("w_copy", ctypes.c_int32)]
 
 
 class Timing(ctypes.Structure):

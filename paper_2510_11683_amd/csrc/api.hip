@@ -101,7 +101,9 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
   w.gpart = static_cast<float*>(take((NP / 256) * dm.d * 4));
   w.HcT = static_cast<uint16_t*>(take(KT * dm.d * 2));
   w.WT = static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2));
-  w.Wb = pl.f32_in ? static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2)) : nullptr;
+  // the slab-major bf16 W of the dX GEMM (without it the GEMM reads the
+  // caller's bf16 W in place)
+  w.Wk = pl.w_copy ? static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2)) : nullptr;
   w.ldz = chunk ? RP : KT + kDzPadRows;
   w.dZ = chunk ? nullptr : static_cast<uint16_t*>(take(w.ldz * dm.V * 2));
   w.dx_part = static_cast<float*>(take(pl.n_split * RP * dm.d * 4));
@@ -136,7 +138,7 @@ static size_t plan_bytes(const Dims& dm, const Plan& pl) {
 // within about 4 GB.  With every sample retained, the same units (at most n_t
 // samples each) each keep their own state and all of them form the one dW
 // batch, so both modes run the same unit compositions.
-static Plan default_plan(const Dims& dm, int retain, int f32) {
+static Plan default_plan(const Dims& dm, int retain) {
   const int64_t NP = padded_positions(dm);
   const int64_t per_sample = NP * ((int64_t)dm.V * kDwUnits + (int64_t)dm.d * (1 + kDwUnits)) * 2;
   int64_t G = std::max<int64_t>(1, std::min(max_unit(dm), 32 * kGiB / per_sample));
@@ -144,7 +146,7 @@ static Plan default_plan(const Dims& dm, int retain, int f32) {
   const int64_t RP = G * NP;
   const int64_t n_split = std::max<int64_t>(1, std::min<int64_t>(16, 4 * kGiB / (RP * dm.d * 4)));
   const int64_t dw_batch = kDwUnits * RP <= kMaxColumns ? kDwUnits : 1;
-  return Plan{G, dw_batch, n_split, 0, retain, f32};
+  return Plan{G, dw_batch, n_split, 0, retain, 1};
 }
 
 // Estimated time (arbitrary units) per sample of the recompute backward for
@@ -182,9 +184,9 @@ static double recompute_cost(const Dims& dm, const Plan& pl) {
 }
 
 // The same estimate for the stored-exponential backward: three GEMM passes
-// (the dX GEMM at the best split the capacity allows), the forward's stores
-// of the kept exponentials (2 bytes per entry) and the dW read-modify-write
-// once per batch of units.
+// (the dX GEMM at the best split the capacity allows, about 2 % faster on
+// the slab-major copy of W), the forward's stores of the kept exponentials
+// (2 bytes per entry) and the dW read-modify-write once per batch of units.
 static double stored_cost(const Dims& dm, const Plan& pl) {
   const double NP = (double)padded_positions(dm);
   const double rows = pl.G * NP;
@@ -193,7 +195,9 @@ static double stored_cost(const Dims& dm, const Plan& pl) {
   for (int64_t sp = 1; sp <= pl.n_split; ++sp)
     dx_fill = std::max(dx_fill, mean_fill(rows, col_t, (double)sp));
   const double pass = 2.0 * NP * 0.5 * dm.d * (double)dm.V / 1.35e15;
-  const double gemm = pass * (1.0 / mean_fill(rows, std::ceil(dm.V / 256.0), 1.0) + 1.0 / dx_fill + 1.0);
+  const double dx_rate = pl.w_copy ? 0.98 : 1.0;
+  const double gemm =
+      pass * (1.0 / mean_fill(rows, std::ceil(dm.V / 256.0), 1.0) + dx_rate / dx_fill + 1.0);
   const double mem = (2.0 * NP * 0.5 * dm.V + (double)dm.V * dm.d * 8.0 / (pl.G * pl.dw_batch)) / 5e12;
   return gemm + mem;
 }
@@ -205,7 +209,7 @@ static int choose_plan(const bgpo_problem* p, Plan* out) {
   const int f32 = p->in_dtype == BGPO_F32;
   const uint64_t budget = p->ws_budget;
   if (p->retain_samples || (budget == 0 && p->vocab_chunk == 0)) {
-    *out = default_plan(dm, p->retain_samples, f32);
+    *out = default_plan(dm, p->retain_samples);
     return BGPO_OK;
   }
   const int64_t NP = padded_positions(dm);
@@ -213,7 +217,7 @@ static int choose_plan(const bgpo_problem* p, Plan* out) {
     // the default layout if it fits (with the largest dW batch the budget
     // allows on top of it), else the stored-mode layout of least estimated
     // time that fits
-    const Plan dflt = default_plan(dm, 0, f32);
+    const Plan dflt = default_plan(dm, 0);
     if (plan_bytes(dm, dflt) <= budget) {
       *out = dflt;
       for (int64_t dwb = kDwUnitsMax; dwb > dflt.dw_batch; --dwb) {
@@ -233,14 +237,16 @@ static int choose_plan(const bgpo_problem* p, Plan* out) {
       for (int64_t dwb = kDwUnits; dwb >= 1; --dwb) {
         if (dwb * G * NP > kMaxColumns) continue;
         const int64_t ns_max = std::max<int64_t>(1, std::min<int64_t>(16, 4 * kGiB / (G * NP * p->d * 4)));
-        for (int64_t ns = 1; ns <= ns_max; ++ns) {
-          const Plan pl{G, dwb, ns, 0, 0, f32};
-          if (plan_bytes(dm, pl) > budget) break;   // more splits only take more memory
-          const double c = stored_cost(dm, pl);
-          if (!found || c < best_cost) {
-            found = true;
-            best = pl;
-            best_cost = c;
+        for (int wc = 1; wc >= f32; --wc) {   // with and (bf16 inputs) without the W copy
+          for (int64_t ns = 1; ns <= ns_max; ++ns) {
+            const Plan pl{G, dwb, ns, 0, 0, wc};
+            if (plan_bytes(dm, pl) > budget) break;   // more splits only take more memory
+            const double c = stored_cost(dm, pl);
+            if (!found || c < best_cost) {
+              found = true;
+              best = pl;
+              best_cost = c;
+            }
           }
         }
       }
@@ -449,7 +455,7 @@ using namespace bgpo;
 
 extern "C" {
 
-int bgpo_version(void) { return (3 << 16) | 0; }
+int bgpo_version(void) { return (3 << 16) | 1; }
 
 const char* bgpo_status_string(int status) {
   switch (status) {
@@ -483,6 +489,7 @@ int bgpo_workspace_plan(const bgpo_problem* prob, bgpo_plan_info* info) {
   info->dw_batch = (int32_t)w.dw_batch;
   info->dx_splits = (int32_t)w.n_split;
   info->vocab_chunk = (int32_t)w.chunk;
+  info->w_copy = pl.w_copy;
   return BGPO_OK;
 }
 
@@ -528,17 +535,17 @@ namespace bgpo {
 // Recompute mode: per
 // vocabulary chunk, the chunk's logits -> its dZ, dX partials accumulated,
 // dW[:, chunk] accumulated.  Then each sample's rows are added into dX in
-// sample order (with the norm backward).  W_dx: the bf16 W_head the dX GEMM
-// reads.
+// sample order (with the norm backward).  W: the caller's W_head (bf16
+// inputs), read by the dX GEMM when the plan keeps no slab-major copy.
 static int unit_backward(const Workspace& ws, const Act& act, int j0, int j_begin,
-                         const uint16_t* W_dx, float* dX, float* dgamma, float* dW,
+                         const uint16_t* W, float* dX, float* dgamma, float* dW,
                          const Dims& dm, int grid, Timer& tm, hipStream_t s) {
   if (!ws.chunk) {
     BGPO_TRY(tm.begin(BGPO_K_SOFTMAX_GRAD));
     BGPO_TRY(launch_grad_scale(ws, dm.d, dm.V, s));
     BGPO_TRY(tm.end(3));
     BGPO_TRY(tm.begin(BGPO_K_DX));
-    BGPO_TRY(launch_gemm_dx(ws, W_dx, dm.d, dm.V, grid, s));
+    BGPO_TRY(launch_gemm_dx(ws, W, dm.d, dm.V, grid, s));
     BGPO_TRY(tm.end());
   } else {
     for (int v0 = 0; v0 < dm.V; v0 += (int)ws.chunk) {
@@ -547,7 +554,7 @@ static int unit_backward(const Workspace& ws, const Act& act, int j0, int j_begi
       BGPO_TRY(launch_gemm_recompute(ws, dm.d, v0, width, grid, s));
       BGPO_TRY(tm.end());
       BGPO_TRY(tm.begin(BGPO_K_DX));
-      BGPO_TRY(launch_gemm_dx_chunk(ws, W_dx, dm.d, dm.V, v0, width, v0 == 0, grid, s));
+      BGPO_TRY(launch_gemm_dx_chunk(ws, W, dm.d, dm.V, v0, width, v0 == 0, grid, s));
       BGPO_TRY(tm.end());
       BGPO_TRY(tm.begin(BGPO_K_DW));
       BGPO_TRY(launch_gemm_dw_chunk(ws, dW, dm.d, dm.V, v0, width, grid, s));
@@ -586,9 +593,8 @@ static int bwd_retained(const bgpo_problem* prob, const Plan& pl, const Act& act
   std::vector<Workspace> U(n_units);
   workspace_layout(dm, pl, workspace, nullptr, U.data());
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
-  BGPO_TRY(launch_transpose_w(W_head, act.f32, ws.WT, ws.Wb, dm.d, dm.V, s));
+  BGPO_TRY(launch_transpose_w(W_head, act.f32, ws.WT, ws.Wk, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
-  const uint16_t* W_dx = act.f32 ? ws.Wb : static_cast<const uint16_t*>(W_head);
   for (int u = 0; u < n_units; ++u) {
     const int j0 = u * G, n_s = std::min(G, dm.n_t - j0);
     const int st = run_forward_unit(prob, U[u], tm, grid, j0, n_s, act, targets, resp_mask,
@@ -610,7 +616,8 @@ static int bwd_retained(const bgpo_problem* prob, const Plan& pl, const Act& act
     BGPO_TRY(launch_seq_terms(U[u], dm.B, dm.n_t, j0, adv, ell_old, loss_scale, ell, g, loss,
                               status_flags, true, prob->bound, dbar, s));
     BGPO_TRY(tm.end());
-    const int st = unit_backward(U[u], act, j0, 0, W_dx, dX, dgamma, dW, dm, grid, tm, s);
+    const int st = unit_backward(U[u], act, j0, 0, static_cast<const uint16_t*>(W_head), dX,
+                                 dgamma, dW, dm, grid, tm, s);
     if (st != BGPO_OK) return st;
   }
   BGPO_TRY(tm.begin(BGPO_K_DW));
@@ -697,9 +704,8 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const void* W
   Workspace ws;
   workspace_layout(dm, pl, workspace, &ws, nullptr);
   BGPO_TRY(tm.begin(BGPO_K_TRANSPOSE_W));
-  BGPO_TRY(launch_transpose_w(W_head, act.f32, ws.WT, ws.Wb, dm.d, dm.V, s));
+  BGPO_TRY(launch_transpose_w(W_head, act.f32, ws.WT, ws.Wk, dm.d, dm.V, s));
   BGPO_TRY(tm.end());
-  const uint16_t* W_dx = act.f32 ? ws.Wb : static_cast<const uint16_t*>(W_head);
   // exact objective off-policy: a forward pass over every sample gives the
   // mean log-ratio, which scales every sample's gradient (on-policy it is 0)
   const double* dbar = nullptr;
@@ -730,7 +736,8 @@ static int elbo_bwd_impl(const bgpo_problem* prob, const Act& act, const void* W
                           loss_scale, ell, g, loss, n_masked, t_out, status_flags, true, store_u,
                           prev, dbar, s);
     if (st != BGPO_OK) return st;
-    st = unit_backward(ws, act, j0, prob->j_begin, W_dx, dX, dgamma, dW, dm, grid, tm, s);
+    st = unit_backward(ws, act, j0, prob->j_begin, static_cast<const uint16_t*>(W_head), dX,
+                       dgamma, dW, dm, grid, tm, s);
     if (st != BGPO_OK) return st;
     prev_used = n_s;
     // stored mode: one dW GEMM per batch of units, K over all their rows (the

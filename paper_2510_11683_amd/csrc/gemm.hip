@@ -44,16 +44,20 @@ namespace bgpo {
 
 enum EpiKind { EPI_FWD = 0, EPI_FWDU = 1, EPI_F32_STORE = 2, EPI_F32_ACCUM = 3, EPI_DZ = 4 };
 
-// Layouts of the A operand.  A_ROW: row-major, lda elements per row (W^T, W).
-// A_MSLAB: the transpose stored slab-major, i.e. element (m, k) at
-// ((m / 64) lda + k) 64 + m % 64 with lda = K rows per slab (dZ as the dW
-// GEMM's A): M is contiguous, so its fragments are read with the transposing
-// LDS read.
-enum ALayout { A_ROW = 0, A_MSLAB = 1 };
+// Layouts of the A operand.  A_ROW: row-major, lda elements per row (W^T in
+// the forward).  A_KSLAB: slab-major over K, element (m, k) at
+// ((k / 64) lda + m) 64 + k % 64 with lda = M rows per slab (W in the dX
+// GEMM: a tile's K slab is one contiguous run of 128-byte rows instead of
+// rows a whole vocabulary apart).  A_MSLAB: the transpose stored slab-major,
+// element (m, k) at ((m / 64) lda + k) 64 + m % 64 with lda = K rows per slab
+// (dZ as the dW GEMM's A): M is contiguous, so its fragments are read with
+// the transposing LDS read.
+enum ALayout { A_ROW = 0, A_MSLAB = 1, A_KSLAB = 2 };
 
 struct GemmParams {
   const uint16_t* A;
-  int64_t lda;               // A_ROW: elements per row; A_MSLAB: rows (K) per slab
+  int64_t lda;               // A_ROW: elements per row; A_KSLAB: rows (M) per slab;
+                             // A_MSLAB: rows (K) per slab
   const uint16_t* B;
   int64_t ldb;               // rows per slab (B is always slab-major)
   int dyn_boff;              // B starts at row meta->col_off (the unit's rows of dZ)
@@ -232,7 +236,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
   static_assert(C::NWAVES == 4 && BK == 64, "four waves, 64-deep slabs");
   // A is row-major (W^T, W) or M-slab-major (dZ, with transposing fragment
   // reads); B is always K-slab-major
-  constexpr bool kMSlabA = AL == A_MSLAB;
+  constexpr bool kMSlabA = AL == A_MSLAB, kKSlabA = AL == A_KSLAB;
   static_assert(!kMSlabA || BM / 64 == C::NWAVES, "one 64-row M slab of A per wave");
   __shared__ uint4 smem[STAGES * (BM + BN) * KCH];
   uint4* As = smem;                           // [STAGES][BM][KCH]
@@ -334,7 +338,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
     // slabs lie rows-per-slab x 128 bytes apart, beyond 32-bit offsets), with
     // rows 128 bytes apart inside it.
     const char* const a_tile = reinterpret_cast<const char*>(
-        p.A + (kMSlabA ? (int64_t)(m0 / 64) * p.lda * 64 : (int64_t)m0 * p.lda));
+        p.A + (kMSlabA   ? (int64_t)(m0 / 64) * p.lda * 64
+               : kKSlabA ? (int64_t)m0 * 64
+                         : (int64_t)m0 * p.lda));
     const char* const b_tile = reinterpret_cast<const char*>(p.B + ((int64_t)n0 + b_row0) * 64);
     const int64_t a_slab = p.lda * 128, b_slab = p.ldb * 128;   // bytes per slab (slab-major)
     const int a_row = (int)p.lda * 2;                           // bytes per row (A_ROW)
@@ -358,7 +364,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
         const int g = wave * A_INS + q, row = g * RPI + lane / KCH;
         const int c = (lane % KCH) ^ C::swz(row);
         const int rr = min(m0 + row, M - 1) - m0;
-        a_voff[q] = (uint32_t)(rr * a_row + c * 16);
+        a_voff[q] = (uint32_t)(rr * (kKSlabA ? 128 : a_row) + c * 16);
       }
     }
 #pragma unroll
@@ -388,6 +394,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm4w(GemmParams p) {
           if constexpr (kMSlabA) {
             // K slab ks of the wave's M slab: 64 rows of 128 bytes
             lds_load(__builtin_amdgcn_make_buffer_rsrc((void*)(a_tile + a_wslab + ks * 8192), (short)0,
+                                                       0x7FFFFFFF, 0x00020000),
+                     a_voff[e], 0, dst);
+          } else if constexpr (kKSlabA) {
+            lds_load(__builtin_amdgcn_make_buffer_rsrc((void*)(a_tile + ks * a_slab), (short)0,
                                                        0x7FFFFFFF, 0x00020000),
                      a_voff[e], 0, dst);
           } else {
@@ -679,13 +689,20 @@ hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, 
   // dX^T[c][row] = W[c][:] . dZ[row][:] over the unit's rows of dZ, stored
   // transposed: dx_part[row][c]
   GemmParams p = base_params();
-  p.A = W; p.lda = V;
+  if (ws.Wk) {
+    p.A = ws.Wk; p.lda = d;
+  } else {
+    p.A = W; p.lda = V;
+  }
   p.B = ws.dZ; p.ldb = ws.ldz; p.dyn_boff = 1;
   p.M = d; p.K = V; p.dyn_n = 1; p.meta = ws.unit();
   p.dyn_split = 1;
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
-  k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  if (ws.Wk)
+    k_gemm4w<EPI_F32_STORE, A_KSLAB, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  else
+    k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -722,13 +739,21 @@ hipError_t launch_gemm_dx_chunk(const Workspace& ws, const uint16_t* W, int d, i
   // dX^T[c][row] (+)= W[c][v0 ..] . dZ[row][..] over the chunk, split over
   // the chunk as the unit's record says; the first chunk stores the partials
   GemmParams p = base_params();
-  p.A = W + v0; p.lda = V;
+  if (ws.Wk) {
+    p.A = ws.Wk + (int64_t)v0 * d; p.lda = d;   // v0 / 64 whole slabs of d rows
+  } else {
+    p.A = W + v0; p.lda = V;
+  }
   p.B = ws.dZ; p.ldb = ws.RP;
   p.M = d; p.K = width; p.dyn_n = 1; p.meta = ws.unit();
   p.dyn_split = 1;
   p.group_m = kGroupMdX;
   p.out = ws.dx_part; p.ldo = d; p.split_stride = ws.RP * d;
-  if (first)
+  if (ws.Wk && first)
+    k_gemm4w<EPI_F32_STORE, A_KSLAB, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  else if (ws.Wk)
+    k_gemm4w<EPI_F32_ACCUM, A_KSLAB, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
+  else if (first)
     k_gemm4w<EPI_F32_STORE, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);
   else
     k_gemm4w<EPI_F32_ACCUM, A_ROW, BGPO_TILE4><<<grid, kGemmThreads4, 0, s>>>(p);

@@ -84,8 +84,8 @@ struct Workspace {
   uint16_t* HcT;       // [d rows, KT] the same, transposed, units of a dW batch side by side,
                        // slab-major
   uint16_t* WT;        // [V, d]       W_head transposed (bf16), row-major
-  uint16_t* Wb;        // [d, V]       W_head rounded to bf16, row-major (fp32 inputs only,
-                       // else NULL)
+  uint16_t* Wk;        // [d rows, V]  W_head in bf16, slab-major: the dX GEMM's A operand
+                       // (NULL without Plan::w_copy)
   float* part_m;       // [nvt, RP]    per-vocabulary-slice max (log2 units)
   float* part_s;       // [nvt, RP]    per-vocabulary-slice sum of 2^(z*log2e - max)
   float* ztgt;         // [RP]         target logit
@@ -129,7 +129,9 @@ struct Plan {
   int64_t n_split;    // capacity of the dX split partials, in splits
   int64_t chunk;      // 0: stored exponentials; > 0: recompute in vocabulary chunks of this width
   int retain;         // every unit keeps its own state (memory grows with n_t)
-  int f32_in;         // fp32 inputs: keep a bf16 copy of W_head
+  int w_copy;         // keep the slab-major bf16 copy of W_head that the dX GEMM reads
+                      // (else it reads the caller's bf16 W_head row-major; always 1 for
+                      // fp32 inputs)
 };
 
 // Views into the caller's workspace for plan `pl` (base may be NULL: sizes
@@ -144,9 +146,9 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
                         Workspace* units);
 
 // ---- launchers (return hipSuccess or the launch error) ----
-// W_head -> W^T (bf16); fp32 W (f32) is rounded to bf16, and its rounded copy
-// in natural layout goes to Wb
-hipError_t launch_transpose_w(const void* W, bool f32, uint16_t* WT, uint16_t* Wb, int d, int V,
+// W_head -> W^T (bf16, row-major) and W (bf16, slab-major with d rows per
+// slab); fp32 W (f32) is rounded to bf16 as it is read
+hipError_t launch_transpose_w(const void* W, bool f32, uint16_t* WT, uint16_t* Wk, int d, int V,
                               hipStream_t s);
 // Mask and compaction of sample j, sample g of its unit: rows go after those of
 // the unit's earlier samples (prev = record of sample g - 1); for g = 0, prev
@@ -184,6 +186,7 @@ hipError_t launch_mean_ratio(const double* ell, const double* ell_old, int B, in
 // dZ, H_c^T scaled by the row factors, and the rows outside the exponent range
 // recomputed
 hipError_t launch_grad_scale(const Workspace& ws, int d, int V, hipStream_t s);
+// (W: the caller's bf16 W_head, read row-major when ws.Wk is NULL)
 hipError_t launch_gemm_dx(const Workspace& ws, const uint16_t* W, int d, int V, int grid,
                           hipStream_t s);
 // dX of sample g of the unit (its rows only; samples of a unit run one after
@@ -199,6 +202,7 @@ hipError_t launch_gemm_dw(const Workspace& ws, float* dW, int d, int V, int grid
 // dW[:, chunk] += H_c^T . dZ
 hipError_t launch_gemm_recompute(const Workspace& ws, int d, int v0, int width, int grid,
                                  hipStream_t s);
+// (W: the caller's bf16 W_head, read row-major when ws.Wk is NULL)
 hipError_t launch_gemm_dx_chunk(const Workspace& ws, const uint16_t* W, int d, int V, int v0,
                                 int width, bool first, int grid, hipStream_t s);
 hipError_t launch_gemm_dw_chunk(const Workspace& ws, float* dW, int d, int V, int v0, int width,

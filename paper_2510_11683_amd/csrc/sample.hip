@@ -520,13 +520,14 @@ hipError_t launch_gather(const void* hidden, bool f32, int64_t stride, int B, co
 }
 
 // ---------------------------------------------------------------------------
-// W_head [d, V] -> WT [V, d], 64x64 tiles through LDS.  fp32 W is rounded to
-// bf16 as it is read, and the rounded rows also go to Wb [d, V] (the dX GEMM's
-// operand).
+// W_head [d, V] -> WT [V, d] (row-major) and, unless Wk is NULL, Wk: W in
+// slab-major order with d rows per slab (the dX GEMM's operand; each 64x64
+// tile is 8 KB of contiguous memory there).  64x64 tiles through LDS; fp32 W
+// is rounded to bf16 as it is read.
 template <typename T>
 __global__ __launch_bounds__(256) void k_transpose_w(const T* __restrict__ W,
                                                      uint16_t* __restrict__ WT,
-                                                     uint16_t* __restrict__ Wb, int d, int V) {
+                                                     uint16_t* __restrict__ Wk, int d, int V) {
   __shared__ uint16_t tile[64][72];
   const int v0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
   const int tid = threadIdx.x;
@@ -536,7 +537,7 @@ __global__ __launch_bounds__(256) void k_transpose_w(const T* __restrict__ W,
     const int kr = q >> 3, ch = q & 7;
     const uint4 v = load_bf16x8(W + (int64_t)(k0 + kr) * V + v0 + ch * 8);
     *reinterpret_cast<uint4*>(&tile[kr][ch * 8]) = v;
-    if (Wb) *reinterpret_cast<uint4*>(Wb + (int64_t)(k0 + kr) * V + v0 + ch * 8) = v;
+    if (Wk) *reinterpret_cast<uint4*>(Wk + slab_index(d, k0 + kr, v0 + ch * 8)) = v;
   }
   __syncthreads();
 #pragma unroll
@@ -552,14 +553,13 @@ __global__ __launch_bounds__(256) void k_transpose_w(const T* __restrict__ W,
   }
 }
 
-hipError_t launch_transpose_w(const void* W, bool f32, uint16_t* WT, uint16_t* Wb, int d, int V,
+hipError_t launch_transpose_w(const void* W, bool f32, uint16_t* WT, uint16_t* Wk, int d, int V,
                               hipStream_t s) {
   dim3 grid((unsigned)(V / 64), (unsigned)(d / 64));
   if (f32)
-    k_transpose_w<float><<<grid, 256, 0, s>>>(static_cast<const float*>(W), WT, Wb, d, V);
+    k_transpose_w<float><<<grid, 256, 0, s>>>(static_cast<const float*>(W), WT, Wk, d, V);
   else
-    k_transpose_w<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(W), WT, nullptr, d,
-                                                 V);
+    k_transpose_w<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(W), WT, Wk, d, V);
   return hipGetLastError();
 }
 

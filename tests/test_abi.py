@@ -271,16 +271,39 @@ def test_budget_above_the_default_raises_the_dw_batch(b):
     assert seen == sorted(seen) and seen[0] == 2 and seen[-1] == 4
 
 
+def test_w_copy_kept_where_it_pays(b):
+    """The default layout keeps the slab-major copy of W (2 d V bytes, the dX
+    GEMM's operand); a tight budget drops it for bf16 inputs when that buys
+    a larger unit (4 GiB at the benchmark shape: units of 2 without it, of 1
+    with it), while fp32 inputs, which need a bf16 W anyway, keep it; the
+    recompute layouts keep it for fp32 inputs only."""
+    assert b.bgpo_workspace_plan(_prob(b))["w_copy"] == 1
+    tight = b.bgpo_workspace_plan(_prob(b, ws_budget=4 * GiB))
+    assert (tight["mode"], tight["w_copy"], tight["samples_per_unit"]) == ("stored", 0, 2)
+    tight32 = b.bgpo_workspace_plan(_prob(b, ws_budget=4 * GiB, in_dtype=b.BGPO_F32))
+    assert tight32["w_copy"] == 1 and tight32["samples_per_unit"] == 1
+    for dt, wc in ((b.BGPO_BF16, 0), (b.BGPO_F32, 1)):
+        assert b.bgpo_workspace_plan(_prob(b, vocab_chunk=4096, in_dtype=dt))["w_copy"] == wc
+    assert b.bgpo_workspace_plan(_prob(b, retain_samples=1, bound=3))["w_copy"] == 1
+
+
 def test_forced_vocab_chunk_and_fp32_copy(b):
     """vocab_chunk > 0 forces the recompute layout (much smaller than the
-    stored one at the same unit size); fp32 inputs add a bf16 copy of W."""
+    stored one at the same unit size).  The stored layout always holds a
+    slab-major bf16 copy of W (the dX GEMM's operand), so fp32 inputs cost
+    nothing more there; the recompute layout reads a bf16 W in place and
+    adds the copy (2 d V bytes) only for fp32 inputs."""
     stored = b.bgpo_workspace_size(_prob(b))
     chunked = b.bgpo_workspace_size(_prob(b, vocab_chunk=8192))
     assert chunked < stored / 4
     small = dict(B=2, L=64, d=128, V=1024, n_t=4)
     w16 = b.bgpo_workspace_size(_prob(b, **small))
     w32 = b.bgpo_workspace_size(_prob(b, in_dtype=b.BGPO_F32, **small))
-    assert w32 - w16 >= 2 * 128 * 1024
+    assert w32 == w16
+    r16 = b.bgpo_workspace_size(_prob(b, vocab_chunk=256, **small))
+    r32 = b.bgpo_workspace_size(_prob(b, vocab_chunk=256, in_dtype=b.BGPO_F32, **small))
+    assert r32 - r16 >= 2 * 128 * 1024
+    assert w16 - r16 >= 2 * 128 * 1024
     # a chunk wider than the vocabulary is the whole vocabulary
     assert (b.bgpo_workspace_size(_prob(b, vocab_chunk=4096, **small)) ==
             b.bgpo_workspace_size(_prob(b, vocab_chunk=1024, **small)))

@@ -103,6 +103,50 @@ def test_fp32_inputs_rmsnorm_bit_identical_to_host_rounding():
     assert np.abs(res[0][0]).max() > 0
 
 
+def test_fp32_inputs_recompute_bit_identical_to_bf16():
+    """The recompute mode's dX GEMM reads a bf16 W_head in place (row-major)
+    and an fp32 one from its slab-major bf16 copy: the same products in the
+    same order, so dX and dW agree bit for bit (MID, chunks of 1024: 4 full
+    and a last one of 192 ids)."""
+    b = lib()
+    w = MID
+    x = workloads.generate(w, keep_f32=True)
+    ell_old = _off_policy_ell_old(w, x, 43, 2.0)
+    outs = []
+    for kw in ({}, {"in_dtype": b.BGPO_F32}):
+        assert b.bgpo_workspace_plan(problem(w, vocab_chunk=1024, **kw))["mode"] == "recompute"
+        r = Runner(w, x, vocab_chunk=1024, **kw)
+        r.bwd(ell_old=ell_old)
+        outs.append(r.out())
+    for k in ("ell", "g", "nm", "t", "dX", "dW"):
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+    assert np.abs(outs[0]["dW"]).max() > 0
+
+
+def test_stored_without_the_w_copy_bit_identical():
+    """A budget just below the default layout keeps its units, dW batch and
+    split capacity and drops the slab-major copy of W (the dX GEMM then reads
+    W_head row-major): the same products in the same order, so every output
+    is bit-identical to the default layout's (tiny, off-policy)."""
+    b = lib()
+    w = workloads.TINY
+    x = workloads.generate(w)
+    dflt = b.bgpo_workspace_plan(problem(w))
+    tight = b.bgpo_workspace_plan(problem(w, ws_budget=dflt["workspace_bytes"] - 1))
+    assert dflt["w_copy"] == 1 and tight["w_copy"] == 0
+    for k in ("samples_per_unit", "dw_batch", "dx_splits", "vocab_chunk"):
+        assert tight[k] == dflt[k], k
+    ell_old = _off_policy_ell_old(w, x, 45, 0.5)
+    outs = []
+    for kw in ({}, {"ws_budget": dflt["workspace_bytes"] - 1}):
+        r = Runner(w, x, **kw)
+        r.bwd(ell_old=ell_old)
+        outs.append(r.out())
+    for k in ("ell", "g", "nm", "t", "dX", "dW"):
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+    assert outs[0]["loss"] == outs[1]["loss"]
+
+
 # ---------------------------------------------------------------- recompute backward
 
 @pytest.mark.parametrize("chunk", [256, 1024, 4096, 8192], ids=lambda c: f"chunk{c}")
