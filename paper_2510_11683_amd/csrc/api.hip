@@ -74,7 +74,11 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
     return p;
   };
   // the state of one unit: masks and rows, log-sum-exp partials, H_c (and a
-  // vocabulary chunk's dZ)
+  // vocabulary chunk's dZ).  Every unit's state comes first, at the head of
+  // the workspace: the forward GEMM reads H_c one K slab (rows x 128 bytes)
+  // after another, a new span of memory per slab, and with H_c at the tail
+  // of a large allocation the forward ran up to 5 % slower (measured), at
+  // its head not.
   auto take_unit = [&](Workspace& w) {
     w.meta = static_cast<SampleMeta*>(take(G * sizeof(SampleMeta)));
     w.idx = static_cast<int32_t*>(take(G * P * 4));
@@ -96,7 +100,10 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
     w.Hc = static_cast<uint16_t*>(take(RP * dm.d * 2));
     if (chunk) w.dZ = static_cast<uint16_t*>(take(RP * chunk * 2));
   };
-  Workspace w;
+  Workspace w{};
+  take_unit(w);
+  const size_t unit_bytes = off;   // the same for every unit (all pieces 256-byte aligned)
+  off = unit_bytes * n_units;
   w.dbar = static_cast<double*>(take(dm.B * 8));
   w.gpart = static_cast<float*>(take((NP / 256) * dm.d * 4));
   w.HcT = static_cast<uint16_t*>(take(KT * dm.d * 2));
@@ -105,7 +112,7 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
   // caller's bf16 W in place)
   w.Wk = pl.w_copy ? static_cast<uint16_t*>(take((size_t)dm.V * dm.d * 2)) : nullptr;
   w.ldz = chunk ? RP : KT + kDzPadRows;
-  w.dZ = chunk ? nullptr : static_cast<uint16_t*>(take(w.ldz * dm.V * 2));
+  if (!chunk) w.dZ = static_cast<uint16_t*>(take(w.ldz * dm.V * 2));
   w.dx_part = static_cast<float*>(take(pl.n_split * RP * dm.d * 4));
   w.P = P;
   w.NP = NP;
@@ -117,12 +124,14 @@ size_t workspace_layout(const Dims& dm, const Plan& pl, void* base, Workspace* w
   w.KT = KT;
   w.chunk = chunk;
   w.g_used = (int)G;
-  take_unit(w);
+  const size_t end = off;
   for (int64_t u = 1; u < n_units; ++u) {
     Workspace wu = w;
+    off = unit_bytes * u;
     take_unit(wu);
     if (units) units[u] = wu;
   }
+  off = end;
   if (units) units[0] = w;
   if (ws) *ws = w;
   return off;
