@@ -262,13 +262,16 @@ __global__ __launch_bounds__(256) void k_grad_rows(
   row_f[r] = f;
 }
 
-// H_c^T[c][col_off + r] *= f_r (bf16, nearest even) over the unit's padded
-// rows; one workgroup per 64 x 64 tile, which is 8 KB of the slab-major H_c^T.
+// H_c^T[c][col_off + r] *= f_r (bf16, nearest even) over the unit's columns
+// up to col_end (its rows rounded up to 64), not its 256-row padding: the next
+// unit of the dW batch starts at col_end, and with every sample retained its
+// columns already hold its rows when this runs.  One workgroup per 64 x 64
+// tile, which is 8 KB of the slab-major H_c^T.
 __global__ __launch_bounds__(256) void k_scale_hct(const float* __restrict__ row_f,
                                                    const SampleMeta* __restrict__ meta,
                                                    uint16_t* __restrict__ HcT, int d) {
   const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-  if (r0 >= meta->n_rows_pad) return;
+  if (r0 >= meta->col_end - meta->col_off) return;
   const int tid = threadIdx.x, cc = tid & 7;
   float fr[8];
 #pragma unroll

@@ -151,3 +151,57 @@ def test_llada_head_B8_L512_ragged_nt16_off_policy():
 def test_largest_workload_B16_L1024_stratified_all_samples():
     w = workloads.STRESS_L1024
     assert _run_and_compare(w, full_dx=False, seqs=(3, 12)) > 0
+
+
+def test_llada_head_B8_L256_nt16_exact_objective_retained_and_two_pass():
+    """The exact ratio objective (Section 3.1, the mean log-ratio d-bar over
+    all samples in every coefficient) off-policy at the LLaDA head shape,
+    both ways the library computes it: two passes in constant memory (a
+    forward over every sample for d-bar, then the usual units) and every
+    sample's state retained (each forward once; 16 samples in two units of
+    8, one dW batch).  Both match the float64 oracle; the two share kernels
+    and unit compositions, so l, g, the loss and dX agree bit for bit and dW
+    up to the order of its fp32 accumulation."""
+    import dataclasses
+    from paper_2510_11683_amd import bgpo
+    w = workloads.LLADA_L256
+    x = workloads.generate(w)
+    op = dataclasses.replace(_oracle_problem(w), bound=elbo.BOUND_EXACT)
+    ell_old = elbo.elbo_collapsed(op, x["hidden"], x["W"], x["targets"], x["resp_mask"],
+                                  x["adv"], backward=False).ell
+    ell_old = ell_old + np.random.default_rng(13).normal(0.0, 1.0, ell_old.shape)
+    cols = np.unique(np.concatenate([x["targets"].reshape(-1)[:4096],
+                                     np.random.default_rng(5).choice(w.V, 2048, replace=False)]))
+    ref = elbo.elbo_collapsed(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                              ell_old=ell_old, dw_cols=cols.astype(np.int64))
+    outs = []
+    for retain in (0, 1):
+        pr = bgpo.Problem(w.B, w.L, w.d, w.V, w.n_t, seed=w.philox_seed,
+                          seq_id_base=w.seq_id_base, t_mode=w.t_mode, bound=elbo.BOUND_EXACT,
+                          retain_samples=retain)
+        r = Runner(w, x)
+        r.ws = bgpo.alloc_workspace(pr)
+        d = r.dev
+        eo = torch.as_tensor(ell_old, dtype=torch.float64).cuda()
+        bgpo.bgpo_elbo_bwd_accumulate(pr, d["hidden"], d["W"], d["targets"], d["resp_mask"],
+                                      d["adv"], eo, 1.0 / 8, r.dX, r.dW, r.ell, r.g, r.loss, r.nm,
+                                      r.t, r.flags, r.ws)
+        o = r.out()
+        o["dW"] = o["dW"][:, cols]
+        outs.append(o)
+        del r
+        torch.cuda.empty_cache()
+    for o in outs:
+        assert o["flags"] == 0
+        assert np.array_equal(o["nm"], ref.n_masked)
+        assert np.array_equal(o["t"].astype(np.float64), ref.t)
+        np.testing.assert_allclose(o["ell"], ref.ell, rtol=ELL_RTOL, atol=0)
+        np.testing.assert_allclose(o["g"], ref.g, rtol=ELL_RTOL, atol=ELL_RTOL * np.abs(ref.g).max())
+        assert abs(o["loss"] - ref.loss) <= ELL_RTOL * np.abs(ref.g).sum() / 8
+        assert rel_maxnorm(o["dX"], ref.dX) <= GRAD_RTOL, rel_maxnorm(o["dX"], ref.dX)
+        assert rel_maxnorm(o["dW"], ref.dW) <= GRAD_RTOL, rel_maxnorm(o["dW"], ref.dW)
+    two, ret = outs
+    for k in ("ell", "g", "nm", "t", "dX"):
+        assert np.array_equal(two[k], ret[k]), k
+    assert two["loss"] == ret["loss"]
+    assert rel_maxnorm(ret["dW"], two["dW"]) <= 1e-5
