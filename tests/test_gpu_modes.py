@@ -297,3 +297,50 @@ def test_recompute_graph_capture_replays_match_eager():
         for k in ("ell", "g", "nm", "t", "dX", "dW"):
             assert np.array_equal(o[k], eager[k]), k
         assert o["loss"] == eager["loss"] and o["flags"] == 0
+
+
+def test_retained_rmsnorm_per_sample_bit_identical_to_two_pass():
+    """The exact objective off-policy through the final RMSNorm with per-sample
+    activations (MID, 12 samples: two units of one dW batch), with every
+    sample's state retained and in two passes: the same kernels on the same
+    units, so dx, dgamma, dW, l, g and the loss agree bit for bit (the
+    two-pass path is checked against the oracle in the row-f1 tests)."""
+    b = lib()
+    w = MID.replace(n_t=12)
+    x = workloads.generate(w)
+    rng = np.random.default_rng(61)
+    xs = workloads.f32_to_bf16_bits(
+        (rng.standard_normal((w.n_t, w.B, w.L, w.d)) *
+         np.exp(rng.uniform(-1, 1, (w.n_t, w.B, w.L, 1)))).astype(np.float32))
+    xs = torch.from_numpy(xs.reshape(w.n_t, w.B, w.L, w.d).view(np.int16)).view(torch.bfloat16).cuda()
+    gamma = torch.from_numpy(workloads.norm_weight(w)).cuda()
+    dev = b.device_inputs(x)
+    # l_old near l (an input both runs share): the forward entry point's l
+    # plus N(0, 1), so that the exact objective's exp(mean log-ratio) is finite
+    p0 = problem(w, sample_stride=w.B * w.L * w.d)
+    ell0 = torch.zeros(w.B, w.n_t, dtype=torch.float64, device="cuda")
+    nm0 = torch.zeros(w.B, w.n_t, dtype=torch.int32, device="cuda")
+    b.bgpo_elbo_fwd_rmsnorm(p0, xs, gamma, dev["W"], dev["targets"], dev["resp_mask"], ell0, nm0,
+                            None, b.alloc_workspace(p0))
+    torch.cuda.synchronize()
+    ell_old = ell0 + torch.from_numpy(np.random.default_rng(62).normal(0.0, 1.0, (w.B, w.n_t))).cuda()
+    res = []
+    for retain in (0, 1):
+        p = dataclasses.replace(problem(w, sample_stride=w.B * w.L * w.d, bound=3),
+                                retain_samples=retain)
+        ws = b.alloc_workspace(p)
+        dx = torch.zeros(w.n_t, w.B, w.L, w.d, dtype=torch.float32, device="cuda")
+        dgam = torch.zeros(w.d, dtype=torch.float32, device="cuda")
+        dW = torch.zeros(w.d, w.V, dtype=torch.float32, device="cuda")
+        ell = torch.zeros(w.B, w.n_t, dtype=torch.float64, device="cuda")
+        g = torch.zeros_like(ell)
+        loss = torch.zeros(1, dtype=torch.float64, device="cuda")
+        nm = torch.zeros(w.B, w.n_t, dtype=torch.int32, device="cuda")
+        b.bgpo_elbo_bwd_accumulate_rmsnorm(p, xs, gamma, dev["W"], dev["targets"],
+                                           dev["resp_mask"], dev["adv"], ell_old, 0.25, dx, dgam,
+                                           dW, ell, g, loss, nm, None, None, ws)
+        torch.cuda.synchronize()
+        res.append([t.cpu().numpy() for t in (dx, dgam, dW, ell, g, loss, nm)])
+    for name, a, c in zip(("dx", "dgamma", "dW", "ell", "g", "loss", "nm"), *res):
+        assert np.array_equal(a, c), name
+    assert np.abs(res[0][2]).max() > 0 and np.abs(res[0][0]).max() > 0
