@@ -344,3 +344,29 @@ def test_retained_rmsnorm_per_sample_bit_identical_to_two_pass():
     for name, a, c in zip(("dx", "dgamma", "dW", "ell", "g", "loss", "nm"), *res):
         assert np.array_equal(a, c), name
     assert np.abs(res[0][2]).max() > 0 and np.abs(res[0][0]).max() > 0
+
+
+def test_dw_batches_of_four_with_a_ragged_last_batch():
+    """A budget above the default layout raises the dW batch to four units:
+    40 samples in units of 8 then give one dW GEMM over four units and one
+    over the last unit alone.  Against the oracle (off-policy, both bound
+    branches), and l, g, the loss and dX bit-identical to the default batches
+    of two (the dW batching changes only dW's fp32 accumulation order)."""
+    b = lib()
+    w = MID.replace(n_t=40)
+    x = workloads.generate(w)
+    plan = b.bgpo_workspace_plan(problem(w, ws_budget=1 << 40))
+    assert (plan["samples_per_unit"], plan["dw_batch"], plan["mode"]) == (8, 4, "stored")
+    ell_old = _off_policy_ell_old(w, x, 47, 1.0)
+    ref = elbo.elbo_literal(_oracle_problem(w), x["hidden"], x["W"], x["targets"],
+                            x["resp_mask"], x["adv"], ell_old=ell_old)
+    outs = []
+    for kw in ({}, {"ws_budget": 1 << 40}):
+        r = Runner(w, x, **kw)
+        r.bwd(ell_old=ell_old)
+        outs.append(r.out())
+    _check_against_oracle(w, outs[1], ref, range(w.n_t), x["adv"], ell_old)
+    for k in ("ell", "g", "nm", "t", "dX"):
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+    assert outs[0]["loss"] == outs[1]["loss"]
+    assert rel_maxnorm(outs[1]["dW"], outs[0]["dW"]) <= 1e-5
