@@ -108,7 +108,14 @@ def test_gemm_core_split_k(M, N, K, n_split):
 
 # ---------------------------------------------------------------- masks
 
-@pytest.mark.parametrize("w", workloads.CONFIGS + (MID,), ids=lambda w: w.name)
+# MID with the responses' global ids offset (seq = seq_id_base + b enters the
+# Philox counters of t and of the masks), iid and stratified
+MID_SEQ = MID.replace(name="mid_seq_id_base_1000003", seq_id_base=1000003)
+MID_SEQ_STRAT = MID_SEQ.replace(name="mid_seq_id_base_1000003_stratified", t_mode=1)
+
+
+@pytest.mark.parametrize("w", workloads.CONFIGS + (MID, MID_SEQ, MID_SEQ_STRAT),
+                         ids=lambda w: w.name)
 def test_masks_bit_exact(w):
     x = workloads.generate(w, with_weights=False, with_hidden=False)
     resp = torch.from_numpy(x["resp_mask"]).cuda()
@@ -550,3 +557,20 @@ def test_memory_constant_in_n_t():
         del r
     assert len({p[0] for p in peaks}) == 1, peaks
     assert len({p[1] for p in peaks}) == 1, peaks
+
+
+@pytest.mark.parametrize("w", [MID_SEQ, MID_SEQ_STRAT], ids=lambda w: w.name)
+def test_mid_parity_with_seq_id_base(w):
+    """The full backward with the responses' global ids offset: masks, t, l,
+    g and the gradients against the oracle (off-policy)."""
+    w = w.replace(n_t=3)
+    x = workloads.generate(w)
+    op = _oracle_problem(w)
+    ell_old = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                                backward=False).ell
+    ell_old = ell_old + np.random.default_rng(17).normal(0, 1.0, ell_old.shape)
+    ref = elbo.elbo_literal(op, x["hidden"], x["W"], x["targets"], x["resp_mask"], x["adv"],
+                            ell_old=ell_old)
+    r = Runner(w, x)
+    r.bwd(ell_old=ell_old)
+    _check_against_oracle(w, r.out(), ref, range(w.n_t), x["adv"], ell_old)
